@@ -1,0 +1,179 @@
+/*
+ * ds.h -- C ABI of the MI355X (gfx950) active-set batched Sinkhorn library.
+ *
+ * One call solves a window of W independent entropic optimal-transport
+ * problems ("lanes") by log-domain Sinkhorn scaling over a candidate axis,
+ * screens each lane's non-current marginal after every audited cycle, checks
+ * screen-positive lanes with the two-sided L1 stopping rule, and physically
+ * compacts passing lanes out of every lane-indexed tensor so later updates run
+ * at the width of the unfinished set (DrainSinkhorn, arxiv 2607.24741, Sec. 3).
+ *
+ * Problem (eq:eot, Sec. 2), per lane t with points x_i (i < n_t), y_j (j < m_t):
+ *     min_pi <C, pi> + eps_t sum_ij pi_ij (log pi_ij - 1),  pi 1 = a,  pi^T 1 = b,
+ *     C_ij = ||x_i - y_j||^2.
+ * The outputs are the dual potentials (f, g) of the convention
+ *     pi_ij = exp((f_i + g_j - C_ij) / eps_t),
+ * reached by the cycle of eq:sinkhorn-cycle (f-half first) from the cold start
+ * f = g = 0, which fixes the gauge (f + c, g - c) of Sec. 4.2.
+ *
+ * One iteration = one full cycle = one candidate-update slot (Sec. 3.1, 4.1).
+ * A lane's completion depth l_t is the first audit at which
+ *     r = max(||pi 1 - a||_1, ||pi^T 1 - b||_1) <= tol   (eq:release-contract)
+ * holds; audits run after cycle k when k % audit_every == 0 and at max_iter.
+ *
+ * Conventions for every entry point:
+ *   - Array pointers inside ds_problem / ds_result are DEVICE pointers (fp32 or
+ *     int32, C-contiguous, lane-major). ds_stats and its width_trace are HOST.
+ *   - The caller owns all memory. Inputs are never written. ds_solve performs no
+ *     device allocation: all scratch lives in the caller's workspace.
+ *   - All device work is enqueued on the caller's stream (a hipStream_t passed
+ *     as void*; NULL = the null stream). ds_solve returns after the outputs are
+ *     complete (it synchronises that stream). Distinct workspaces may be used
+ *     concurrently from different host threads; one workspace must not be
+ *     shared by overlapping calls.
+ *   - Errors: every entry point returns ds_err. Problems detectable on the host
+ *     (null required pointer, non-positive sizes, tol <= 0, max_iter < 1,
+ *     audit_every < 1, unknown mode, d > 512, W > 4096, workspace too small)
+ *     return before any device work with the outputs untouched. Lane sizes and
+ *     eps are validated on the device before the first update: a bad lane makes
+ *     the call return DS_E_INVALID (outputs undefined) and
+ *     ds_last_error_message() names the first bad lane. A HIP failure returns
+ *     DS_E_HIP. Numerical trouble inside one lane is not a call error: it is
+ *     reported through that lane's status.
+ */
+#ifndef DRAINSINKHORN_DS_H
+#define DRAINSINKHORN_DS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DS_API_VERSION 1
+
+typedef enum {
+  DS_OK = 0,
+  DS_E_INVALID = 1,     /* bad argument or bad lane data (see message)          */
+  DS_E_WORKSPACE = 2,   /* workspace pointer NULL / misaligned / too small        */
+  DS_E_HIP = 3,         /* a HIP runtime call or kernel launch failed             */
+  DS_E_UNSUPPORTED = 4, /* valid request outside the implemented envelope         */
+  DS_E_INTERNAL = 5
+} ds_err;
+
+/* Execution modes (Sec. 3.3). Width-one execution is a call with W = 1. */
+typedef enum {
+  DS_MODE_ACTIVE = 0,  /* verifier-gated retirement + physical compaction        */
+  DS_MODE_STATIC = 1,  /* every lane updated at width W until all have passed;
+                          returns each lane's state at that common boundary and
+                          its first passing depth                               */
+  DS_MODE_LOGICAL = 2  /* passing lanes frozen in place, kernels keep width W    */
+} ds_mode;
+
+typedef enum {
+  DS_LANE_CONVERGED = 0, /* passed the two-sided check at depth l_t              */
+  DS_LANE_MAX_ITER = 1,  /* still failing at max_iter; state of cycle max_iter   */
+  DS_LANE_NONFINITE = 2  /* non-finite residual at an audit; residual = NaN      */
+} ds_lane_status;
+
+enum {
+  DS_F_SHADOW = 1u,     /* also run the full check on screen-negative lanes and
+                           count already-releasable lanes the screen missed      */
+  DS_F_TIMING = 2u,     /* time every update launch with HIP events (ds_stats)  */
+  DS_F_FORCE_VALU = 4u, /* use the vector-ALU update kernels for any d <= 32     */
+  DS_F_FORCE_MFMA = 8u  /* use the matrix-core update kernels for any d <= 32    */
+};
+
+/* One window of W lanes. Device pointers. */
+typedef struct {
+  int32_t W;            /* lanes, 1..4096                                          */
+  int32_t n_max, m_max; /* padded point counts per lane (>= 1)                     */
+  int32_t d;            /* point dimension, 1..512                                 */
+  const float* X;       /* [W, n_max, d] source points                             */
+  const float* Y;       /* [W, m_max, d] target points                             */
+  const float* a;       /* [W, n_max] source masses, > 0 on the valid prefix       */
+  const float* b;       /* [W, m_max] target masses, > 0 on the valid prefix       */
+  const float* eps;     /* [W] entropic regularisation, finite and > 0             */
+  const int32_t* n;     /* [W] valid prefix sizes 1..n_max; NULL => all n_max      */
+  const int32_t* m;     /* [W] valid prefix sizes 1..m_max; NULL => all m_max      */
+} ds_problem;
+/* Points beyond a lane's prefix are never read. A zero mass on the valid prefix
+ * removes that point from the problem (its output potential is 0). A negative
+ * or non-finite mass or coordinate makes that lane NONFINITE at its first audit. */
+
+typedef struct {
+  float tol;           /* two-sided stopping tolerance tau_stop, > 0              */
+  float screen_tol;    /* one-sided screen threshold tau_screen; <= 0 => tol      */
+  int32_t max_iter;    /* cycles, >= 1                                            */
+  int32_t audit_every; /* audit grid spacing in cycles, >= 1                      */
+  int32_t mode;        /* ds_mode                                                 */
+  uint32_t flags;      /* DS_F_*                                                  */
+} ds_options;
+
+/* Outputs, in caller lane order. Device pointers. */
+typedef struct {
+  float* f;            /* [W, n_max]; entries past the prefix / zero-mass: 0      */
+  float* g;            /* [W, m_max]; same                                        */
+  int32_t* depth;      /* [W] l_t in cycles                                       */
+  float* residual;     /* [W] max(row, col) L1 residual of the returned state     */
+  float* row_residual; /* [W] may be NULL                                          */
+  float* col_residual; /* [W] may be NULL                                          */
+  int32_t* status;     /* [W] ds_lane_status                                      */
+  int32_t* order;      /* [W] lane ids in completion order (depth, then lane id);
+                          may be NULL                                              */
+} ds_result;
+
+/* Host-side accounting of one solve (all counts exact). */
+typedef struct {
+  int64_t slots_update;       /* sum over cycles of lanes that ran both halves:
+                                 sum_t l_t (active), W * l_max (static, logical)  */
+  int64_t halfsteps_executed; /* lane-half-steps launched, incl. the discarded
+                                 f-half of each retired lane                       */
+  int64_t pair_evals;         /* valid (i, j) terms evaluated by the half-steps      */
+  int64_t check_pair_evals;   /* valid (i, j) terms evaluated by marginal checks     */
+  int64_t bytes_compacted;    /* bytes moved by survivor gathers                    */
+  int32_t l_max, cycles, audits, screen_positive, check_failures, compactions;
+  int32_t missed_ready;       /* DS_F_SHADOW only                                   */
+  int32_t update_launches;    /* DS_F_TIMING: number of timed (sampled) launches     */
+  double ms_total;            /* wall time of the call (host clock)                 */
+  double ms_update;           /* DS_F_TIMING: summed event time of the timed launches
+                                 (both launches of every 32nd cycle, and the final
+                                 audit), bracketed by HIP events on the stream     */
+  int64_t timed_pair_evals;   /* DS_F_TIMING: (i, j) terms evaluated by those launches */
+  double ms_check;            /* reserved (checks share the g-half launches)         */
+  double ms_compact;          /* DS_F_TIMING: compaction (scan + gather) launches     */
+  int32_t* width_trace;       /* optional HOST buffer: A_k for k = 1..             */
+  int32_t width_trace_len;    /* capacity in; entries written out                  */
+  size_t workspace_bytes;     /* bytes of workspace the call used                   */
+} ds_stats;
+
+/* Version of this header the library was built from (DS_API_VERSION). */
+int ds_api_version(void);
+
+/* Workspace bytes ds_solve needs for this problem shape and options. Only the
+ * scalar fields of `problem` are read (no pointer is dereferenced). */
+ds_err ds_workspace_bytes(const ds_problem* problem, const ds_options* options,
+                          size_t* bytes);
+
+/* Solve one window (the whole hot path: ingest, packed f/g updates, fused row
+ * screen, two-sided verifier, retirement and compaction, output emission).
+ * `workspace` is a device buffer of at least ds_workspace_bytes() bytes,
+ * 256-byte aligned, owned by the caller; its contents need no initialisation.
+ * `stream` is a hipStream_t (void* here so this header needs no HIP include).
+ * `stats` may be NULL. */
+ds_err ds_solve(const ds_problem* problem, const ds_options* options,
+                const ds_result* result, void* workspace, size_t workspace_bytes,
+                void* stream, ds_stats* stats);
+
+/* Static string for an error code. */
+const char* ds_error_string(ds_err err);
+
+/* Detail of the last non-OK return on this host thread ("" if none). */
+const char* ds_last_error_message(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DRAINSINKHORN_DS_H */

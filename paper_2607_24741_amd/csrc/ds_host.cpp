@@ -1,0 +1,538 @@
+// Host runtime of the C ABI declared in include/ds.h: argument validation,
+// workspace carve-up, the active-set control loop and the accounting.
+//
+// Control loop (Sec. 3, Fig. fig:active-loop). Cycle k is two launches:
+//   f-half (also the row screen of state k-1 when k-1 is on the audit grid:
+//           R_i/a_i = 2^(lse_new - lse_old), a full evaluation of the row
+//           marginal);
+//   g-half + column check of the screen-positive lanes of state k-1; the last
+//           block of each checked lane takes its decision on the device
+//           (verifier-gated: the screen alone never retires a lane) and a
+//           retired lane's work items stop running at once.
+// The host never waits per cycle: a snapshot of the control block is copied
+// back every few cycles, and when one shows retirements the host launches the
+// compaction (scan + gather into the other bank, with emission of the retired
+// lanes) so later launches run at the survivor width. The host runs at most a
+// bounded number of cycles ahead of the device.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <chrono>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "ds.h"
+#include "ds_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+ds_err fail(ds_err e, const std::string& msg) {
+  g_last_error = msg;
+  return e;
+}
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+bool uses_mfma(const ds_problem* pr, const ds_options* op);
+
+struct Carver {
+  char* base;
+  size_t off = 0;
+  template <typename T>
+  T* take(size_t count) {
+    off = align_up(off, 256);
+    T* p = reinterpret_cast<T*>(base ? base + off : nullptr);
+    off += count * sizeof(T);
+    return p;
+  }
+};
+
+ds::Layout plan(const ds_problem* pr, const ds_options* op, void* ws) {
+  ds::Layout L;
+  std::memset(&L, 0, sizeof(L));
+  L.W = pr->W;
+  L.n_max = pr->n_max;
+  L.m_max = pr->m_max;
+  L.d = pr->d;
+  L.dp = pr->d + (pr->d & 1);
+  L.dh = L.dp / 2;
+  L.pad[0] = (int)align_up((size_t)pr->n_max, ds::kPad);
+  L.pad[1] = (int)align_up((size_t)pr->m_max, ds::kPad);
+  L.rows = uses_mfma(pr, op) ? ds::kRowsMfma : ds::kRowsValu;
+  L.rbmax = std::max(L.pad[0], L.pad[1]) / L.rows;
+  const size_t W = (size_t)pr->W;
+  Carver c{reinterpret_cast<char*>(ws)};
+  for (int b = 0; b < 2; ++b) {
+    ds::Bank& B = L.bank[b];
+    for (int side = 0; side < 2; ++side) {
+      const size_t np = W * (size_t)L.pad[side];
+      B.rec[side] = c.take<float>(np * L.dp);
+      B.lm[side] = c.take<float>(np);
+      for (int par = 0; par < 2; ++par) {
+        B.lse[side][par] = c.take<float>(np);
+        B.gam[side][par] = c.take<float>(np);
+      }
+    }
+    B.slot = c.take<ds::SlotInfo>(W);
+    B.dec = c.take<ds::Decision>(W);
+  }
+  L.center = c.take<float>(W * (size_t)L.d);
+  for (int k = 0; k < 4; ++k) L.agg[k] = c.take<float4>(W * (size_t)L.rbmax);
+  L.vcnt = c.take<int>(W);
+  L.samp = c.take<unsigned long long>(ds::kMaxSamples);
+  L.audit = c.take<ds::Audit>(W);
+  L.off[0] = c.take<int>(W + 1);
+  L.off[1] = c.take<int>(W + 1);
+  L.ctrl = c.take<ds::Ctrl>(1);
+  L.bytes = align_up(c.off, 256);
+  return L;
+}
+
+bool uses_mfma(const ds_problem* pr, const ds_options* op) {
+  if (op->flags & DS_F_FORCE_MFMA) return true;
+  if (op->flags & DS_F_FORCE_VALU) return false;
+  return pr->d >= 8;
+}
+
+ds_err check_problem(const ds_problem* pr, const ds_options* op) {
+  if (!pr || !op) return fail(DS_E_INVALID, "problem and options must not be NULL");
+  if (pr->W < 1 || pr->n_max < 1 || pr->m_max < 1 || pr->d < 1)
+    return fail(DS_E_INVALID, "W, n_max, m_max and d must be >= 1");
+  if (pr->W > ds::kMaxW) return fail(DS_E_UNSUPPORTED, "W above 4096 is not supported");
+  if (pr->d > 512) return fail(DS_E_INVALID, "d must be <= 512");
+  if (pr->d > ds::kMaxDSmall)
+    return fail(DS_E_UNSUPPORTED, "d > 32 needs the large-dimension path, not built");
+  if (!(op->tol > 0.f) || !std::isfinite(op->tol)) return fail(DS_E_INVALID, "tol must be finite and > 0");
+  if (op->max_iter < 1) return fail(DS_E_INVALID, "max_iter must be >= 1");
+  if (op->audit_every < 1) return fail(DS_E_INVALID, "audit_every must be >= 1");
+  if (op->mode < DS_MODE_ACTIVE || op->mode > DS_MODE_LOGICAL) return fail(DS_E_INVALID, "unknown mode");
+  if ((op->flags & DS_F_FORCE_VALU) && (op->flags & DS_F_FORCE_MFMA))
+    return fail(DS_E_INVALID, "DS_F_FORCE_VALU and DS_F_FORCE_MFMA are exclusive");
+  if ((op->flags & DS_F_FORCE_VALU) && pr->d > 16)
+    return fail(DS_E_UNSUPPORTED, "the vector-ALU kernels support d <= 16");
+  // sizes that keep every 32-bit index in range
+  const double pts = (double)pr->W * (double)std::max(pr->n_max, pr->m_max);
+  if (pts > 2.0e9) return fail(DS_E_UNSUPPORTED, "W * max(n_max, m_max) too large");
+  return DS_OK;
+}
+
+#define HIP_TRY(expr)                                                              \
+  do {                                                                             \
+    hipError_t _e = (expr);                                                        \
+    if (_e != hipSuccess)                                                          \
+      return fail(DS_E_HIP, std::string(#expr) + ": " + hipGetErrorString(_e));  \
+  } while (0)
+
+// Per-device host resources kept for the life of the process: a pinned ring
+// for control snapshots and a pool of timing events.
+constexpr int kRing = 16;
+struct DeviceRes {
+  bool ready = false;
+  ds::HostSnap* snap = nullptr;      // pinned, device-written control mirror (host view)
+  ds::HostSnap* snap_dev = nullptr;  // the same memory as the device addresses it
+  hipEvent_t ring_ev[kRing];
+  std::vector<hipEvent_t> timing;
+};
+thread_local DeviceRes g_res[64];
+
+hipError_t device_res(DeviceRes** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  DeviceRes& r = g_res[dev];
+  if (!r.ready) {
+    e = hipHostMalloc(reinterpret_cast<void**>(&r.snap), sizeof(ds::HostSnap),
+                      hipHostMallocMapped | hipHostMallocCoherent);
+    if (e != hipSuccess) return e;
+    e = hipHostGetDevicePointer(reinterpret_cast<void**>(&r.snap_dev), r.snap, 0);
+    if (e != hipSuccess) return e;
+    for (int i = 0; i < kRing; ++i) {
+      e = hipEventCreateWithFlags(&r.ring_ev[i], hipEventDisableTiming);
+      if (e != hipSuccess) return e;
+    }
+    r.ready = true;
+  }
+  *out = &r;
+  return hipSuccess;
+}
+
+struct EventTimer {
+  bool on = false;
+  hipStream_t st = nullptr;
+  std::vector<hipEvent_t>* pool = nullptr;
+  size_t used = 0;
+  std::vector<std::pair<int, int>> spans[3];  // update kernel, compaction, other
+  int rec() {
+    if (used == pool->size()) {
+      hipEvent_t e;
+      if (hipEventCreate(&e) != hipSuccess) return -1;
+      pool->push_back(e);
+    }
+    hipEvent_t e = (*pool)[used];
+    if (hipEventRecord(e, st) != hipSuccess) return -1;
+    return (int)used++;
+  }
+  double total(int kind) {
+    double ms = 0;
+    for (auto& sp : spans[kind]) {
+      if (sp.first < 0 || sp.second < 0) continue;
+      float t = 0;
+      if (hipEventElapsedTime(&t, (*pool)[sp.first], (*pool)[sp.second]) == hipSuccess) ms += t;
+    }
+    return ms;
+  }
+};
+
+}  // namespace
+
+extern "C" {
+
+int ds_api_version(void) { return DS_API_VERSION; }
+
+const char* ds_error_string(ds_err e) {
+  switch (e) {
+    case DS_OK: return "ok";
+    case DS_E_INVALID: return "invalid argument";
+    case DS_E_WORKSPACE: return "workspace missing, misaligned or too small";
+    case DS_E_HIP: return "HIP runtime error";
+    case DS_E_UNSUPPORTED: return "unsupported configuration";
+    case DS_E_INTERNAL: return "internal error";
+  }
+  return "unknown error";
+}
+
+const char* ds_last_error_message(void) { return g_last_error.c_str(); }
+
+ds_err ds_workspace_bytes(const ds_problem* pr, const ds_options* op, size_t* bytes) {
+  g_last_error.clear();
+  if (!bytes) return fail(DS_E_INVALID, "bytes must not be NULL");
+  ds_err e = check_problem(pr, op);
+  if (e != DS_OK) return e;
+  *bytes = plan(pr, op, nullptr).bytes;
+  return DS_OK;
+}
+
+ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res, void* ws,
+                size_t ws_bytes, void* stream_v, ds_stats* stats) {
+  using namespace ds;
+  const auto t_start = std::chrono::steady_clock::now();
+  g_last_error.clear();
+  ds_err e = check_problem(pr, op);
+  if (e != DS_OK) return e;
+  if (!res) return fail(DS_E_INVALID, "result must not be NULL");
+  if (!pr->X || !pr->Y || !pr->a || !pr->b || !pr->eps)
+    return fail(DS_E_INVALID, "X, Y, a, b and eps must not be NULL");
+  if (!res->f || !res->g || !res->depth || !res->residual || !res->status)
+    return fail(DS_E_INVALID, "f, g, depth, residual and status must not be NULL");
+  Layout L = plan(pr, op, nullptr);
+  if (!ws) return fail(DS_E_WORKSPACE, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(ws) % 256) return fail(DS_E_WORKSPACE, "workspace must be 256-byte aligned");
+  if (ws_bytes < L.bytes)
+    return fail(DS_E_WORKSPACE, "workspace too small: need " + std::to_string(L.bytes) + " bytes");
+  L = plan(pr, op, ws);
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream_v);
+  DeviceRes* R = nullptr;
+  HIP_TRY(device_res(&R));
+
+  const int W = pr->W, d = pr->d;
+  const int mode = op->mode;
+  const bool active = (mode == DS_MODE_ACTIVE);
+  const bool shadow = (op->flags & DS_F_SHADOW) != 0;
+  const bool use_mfma = uses_mfma(pr, op);
+  const int maxpad = std::max(L.pad[0], L.pad[1]);
+
+  EventTimer tm;
+  tm.on = (op->flags & DS_F_TIMING) != 0;
+  tm.st = st;
+  tm.pool = &R->timing;
+
+  // ---------------------------------------------------------------- ingest
+  IngestArgs ia;
+  std::memset(&ia, 0, sizeof(ia));
+  ia.X = pr->X; ia.Y = pr->Y; ia.a = pr->a; ia.b = pr->b; ia.eps = pr->eps;
+  ia.n = pr->n; ia.m = pr->m;
+  ia.W = W; ia.n_max = pr->n_max; ia.m_max = pr->m_max; ia.d = d; ia.dp = L.dp; ia.dh = L.dh;
+  ia.pad[0] = L.pad[0]; ia.pad[1] = L.pad[1];
+  ia.bank = L.bank[0];
+  ia.center = L.center;
+  for (int k = 0; k < 4; ++k) ia.agg[k] = L.agg[k];
+  ia.vcnt = L.vcnt; ia.rbmax = L.rbmax;
+  ia.ctrl = L.ctrl;
+  HIP_TRY(launch_ingest(ia, maxpad, st));
+  HIP_TRY(launch_offsets(L.bank[0].slot, W, L.rows, L.off[0], L.off[1], L.ctrl, st));
+  Ctrl ctrl;
+  HIP_TRY(hipMemcpyAsync(&ctrl, L.ctrl, sizeof(Ctrl), hipMemcpyDeviceToHost, st));
+  std::vector<SlotInfo> lanes(W);
+  HIP_TRY(hipMemcpyAsync(lanes.data(), L.bank[0].slot, sizeof(SlotInfo) * W, hipMemcpyDeviceToHost, st));
+  HIP_TRY(hipStreamSynchronize(st));
+  if (ctrl.err_lane != 0x7fffffff) {
+    const char* what = ctrl.err_code == 1 ? "n out of range [1, n_max]"
+                     : ctrl.err_code == 2 ? "m out of range [1, m_max]"
+                                          : "eps not finite and > 0";
+    return fail(DS_E_INVALID, "lane " + std::to_string(ctrl.err_lane) + ": " + what);
+  }
+  // uniform lane shapes: work item -> slot is a division, no table lookup
+  bool uniform = true;
+  for (int t = 1; t < W; ++t)
+    uniform = uniform && lanes[t].n == lanes[0].n && lanes[t].m == lanes[0].m;
+  const int ipl[2] = {uniform ? row_blocks(lanes[0].n, L.rows) : 0,
+                      uniform ? row_blocks(lanes[0].m, L.rows) : 0};
+
+  int A = W, bank = 0;
+  int items[2] = {ctrl.items_f, ctrl.items_g};
+
+  auto make_pass = [&](int role, int kind, int par_in, int par_out, int col_par) {
+    Pass u;
+    std::memset(&u, 0, sizeof(u));
+    const Bank& B = L.bank[bank];
+    const int rs = role, cs = 1 - role;
+    u.rec_row = B.rec[rs]; u.rec_col = B.rec[cs];
+    u.lm_row = B.lm[rs];
+    u.lse_in = B.lse[rs][par_in];
+    u.lse_out = B.lse[rs][par_out];
+    u.gam_out = B.gam[rs][par_out];
+    u.gam_col = B.gam[cs][col_par];
+    u.w_row = role ? pr->b : pr->a;
+    u.w_ld = role ? pr->m_max : pr->n_max;
+    u.off = L.off[role];
+    if (kind == 0) {
+      u.agg_out = L.agg[role == 0 ? AGG_F : AGG_G];
+      u.agg_bound = L.agg[role == 0 ? AGG_G : AGG_F];
+    } else {
+      u.agg_out = L.agg[role == 0 ? AGG_ROW : AGG_COL];
+      u.agg_screen = L.agg[AGG_F];
+      u.agg_rowchk = L.agg[AGG_ROW];
+    }
+    u.A = A; u.ipl = ipl[role];
+    u.padr = L.pad[rs]; u.padc = L.pad[cs];
+    u.role = role; u.kind = kind;
+    return u;
+  };
+  auto make_launch = [&]() {
+    Launch l;
+    std::memset(&l, 0, sizeof(l));
+    l.dp = L.dp; l.rbmax = L.rbmax; l.mode = mode; l.rows = L.rows;
+    l.tau_screen = op->screen_tol > 0.f ? op->screen_tol : op->tol;
+    l.tol = op->tol;
+    l.slot = L.bank[bank].slot; l.dec = L.bank[bank].dec;
+    l.audit = L.audit; l.vcnt = L.vcnt; l.ctrl = L.ctrl;
+    l.hsnap = R->snap_dev; l.samp = nullptr;
+    return l;
+  };
+  // DS_F_TIMING: every kSampleEvery-th cycle's launches are bracketed by
+  // events and count their own (i, j) terms; the rest run untouched
+  constexpr int kSampleEvery = 32;
+  int nsamp = 0;
+  auto run = [&](Launch l, int blocks, bool sample) -> ds_err {
+    const bool timed = tm.on && sample && nsamp < kMaxSamples;
+    if (timed) l.samp = L.samp + nsamp;
+    const int e0 = timed ? tm.rec() : -1;
+    HIP_TRY(launch_update(l, d, use_mfma, blocks, st));
+    if (timed) {
+      tm.spans[0].push_back({e0, tm.rec()});
+      nsamp++;
+    }
+    return DS_OK;
+  };
+
+  // ------------------------------------------------------------ main loop
+  const int max_iter = op->max_iter, ae = op->audit_every;
+  const int kLag = 8;          // cycles the host may run ahead of the device
+  const int kEvery = 4;        // cycles between run-ahead events
+  volatile HostSnap* hs = R->snap;
+  hs->n_active = W; hs->n_retired = 0; hs->compacted = 0; hs->epoch = 0; hs->finished = 0;
+  hs->items_act_f = items[0]; hs->items_act_g = items[1];
+  if (tm.on) HIP_TRY(launch_zero_u64(L.samp, kMaxSamples, st));
+  struct Pending { int idx, cycle; };
+  std::vector<Pending> q;
+  int ring_next = 0, epoch = 0;
+  bool finished = false;
+  int launched = 0;
+  int compactions = 0;
+  int64_t bytes_compacted = 0;  // upper bound: survivors x per-lane state bytes
+  const int64_t lane_bytes = (int64_t)(L.pad[0] + L.pad[1]) * (L.dp + 5) * 4 +
+                             (int64_t)(sizeof(SlotInfo) + sizeof(Decision));
+  for (int k = 1; k <= max_iter; ++k) {
+    // bounded run-ahead: wait for the device only when too far behind
+    while (!q.empty() && q.front().cycle <= k - kLag) {
+      HIP_TRY(hipEventSynchronize(R->ring_ev[q.front().idx]));
+      q.erase(q.begin());
+    }
+    const int s_fin = hs->finished, s_ep = hs->epoch, s_ret = hs->n_retired;
+    const int s_cmp = hs->compacted, s_act = hs->n_active;
+    const int s_itf = hs->items_act_f, s_itg = hs->items_act_g;
+    if (s_fin) { finished = true; break; }
+    if (active && s_ep == epoch && s_ret > s_cmp) {
+      // physical compaction: survivors gathered into the other bank
+      epoch++;
+      ScanArgs sa;
+      std::memset(&sa, 0, sizeof(sa));
+      sa.slot = L.bank[bank].slot; sa.dec = L.bank[bank].dec;
+      sa.off_f = L.off[0]; sa.off_g = L.off[1]; sa.ctrl = L.ctrl; sa.hsnap = R->snap_dev;
+      sa.A = A; sa.W = W; sa.compact = 1; sa.rows = L.rows; sa.epoch = epoch;
+      const int e0 = tm.on ? tm.rec() : -1;
+      HIP_TRY(launch_scan(sa, st));
+      MoveArgs ma;
+      std::memset(&ma, 0, sizeof(ma));
+      ma.src = L.bank[bank]; ma.dst = L.bank[bank ^ 1]; ma.ctrl = L.ctrl;
+      ma.A = A; ma.dp = L.dp; ma.compact = 1; ma.emit_all = 0; ma.mode = mode;
+      ma.pad[0] = L.pad[0]; ma.pad[1] = L.pad[1];
+      ma.n_max = pr->n_max; ma.m_max = pr->m_max; ma.chunk = 1024;
+      ma.f = res->f; ma.g = res->g; ma.depth = res->depth; ma.residual = res->residual;
+      ma.row_res = res->row_residual; ma.col_res = res->col_residual; ma.status = res->status;
+      HIP_TRY(launch_move(ma, A, maxpad, st));
+      if (tm.on) tm.spans[1].push_back({e0, tm.rec()});
+      bank ^= 1;
+      bytes_compacted += (int64_t)s_act * lane_bytes;
+      A = std::min(A, s_act);              // upper bound on the survivors
+      items[0] = std::min(items[0], s_itf);
+      items[1] = std::min(items[1], s_itg);
+      compactions++;
+    }
+    if (A <= 0) { finished = true; break; }
+    const int pk = k & 1, pk1 = (k - 1) & 1;
+    const bool audit_prev = (k - 1 >= 1) && ((k - 1) % ae == 0);
+    const bool sample = (k % kSampleEvery) == 0;
+    // f-half of cycle k (+ row screen of state k-1)
+    Launch lf = make_launch();
+    lf.p[0] = make_pass(0, 0, pk1, pk, pk1);
+    lf.p[0].depth = k - 1;
+    lf.nb0 = items[0];
+    ds_err r = run(lf, items[0], sample);
+    if (r != DS_OK) return r;
+    // g-half of cycle k (+ column check and decision for state k-1)
+    // (the check blocks come first: most of them exit at once)
+    Launch lg = make_launch();
+    int blocks = items[1];
+    if (audit_prev) {
+      lg.p[0] = make_pass(1, 1, pk1, pk1, pk1);   // column marginal of state k-1
+      lg.p[0].decide = 1;
+      lg.p[0].verify_all = shadow ? 1 : 0;
+      lg.p[0].depth = k - 1;
+      lg.p[1] = make_pass(1, 0, pk1, pk, pk);     // g-half of cycle k
+      lg.nb0 = items[1];
+      blocks += items[1];
+    } else {
+      lg.p[0] = make_pass(1, 0, pk1, pk, pk);
+      lg.nb0 = items[1];
+    }
+    r = run(lg, blocks, sample);
+    if (r != DS_OK) return r;
+    launched = k;
+    if (k % kEvery == 0) {
+      const int idx = ring_next;
+      ring_next = (ring_next + 1) % kRing;
+      HIP_TRY(hipEventRecord(R->ring_ev[idx], st));
+      q.push_back({idx, k});
+    }
+  }
+  HIP_TRY(hipStreamSynchronize(st));
+  HIP_TRY(hipMemcpy(&ctrl, L.ctrl, sizeof(Ctrl), hipMemcpyDeviceToHost));
+  A = ctrl.A;
+
+  // ------------------------------------------------------- final audit
+  // max_iter reached with lanes still active (any mode), or static mode's
+  // common boundary: both marginals of the returned state, every lane.
+  const bool need_final = !ctrl.finished || mode == DS_MODE_STATIC;
+  if (need_final) {
+    const int K = ctrl.finished ? ctrl.final_cycle : launched;
+    const int pK = K & 1;
+    HIP_TRY(launch_zero_counters(L.vcnt, W, st));
+    Launch lv = make_launch();
+    lv.p[0] = make_pass(0, 1, pK, pK, pK);
+    lv.p[0].final_audit = 1; lv.p[0].depth = K; lv.p[0].verify_all = 1;
+    lv.nb0 = ctrl.items_f;
+    int saveA = A;
+    ds_err r = run(lv, ctrl.items_f, true);
+    if (r != DS_OK) return r;
+    Launch lw = make_launch();
+    lw.p[0] = make_pass(1, 1, pK, pK, pK);
+    lw.p[0].final_audit = 1; lw.p[0].decide = 1; lw.p[0].depth = K; lw.p[0].verify_all = 1;
+    lw.nb0 = ctrl.items_g;
+    r = run(lw, ctrl.items_g, true);
+    if (r != DS_OK) return r;
+    A = saveA;
+    HIP_TRY(hipStreamSynchronize(st));
+    HIP_TRY(hipMemcpy(&ctrl, L.ctrl, sizeof(Ctrl), hipMemcpyDeviceToHost));
+  }
+  // ------------------------------------------------------------ emission
+  {
+    MoveArgs ma;
+    std::memset(&ma, 0, sizeof(ma));
+    ma.src = L.bank[bank]; ma.dst = L.bank[bank ^ 1]; ma.ctrl = L.ctrl;
+    ma.A = A; ma.dp = L.dp; ma.compact = 0; ma.emit_all = (mode == DS_MODE_STATIC); ma.mode = mode;
+    ma.final_par = ctrl.final_cycle & 1;
+    ma.pad[0] = L.pad[0]; ma.pad[1] = L.pad[1];
+    ma.n_max = pr->n_max; ma.m_max = pr->m_max; ma.chunk = 1024;
+    ma.f = res->f; ma.g = res->g; ma.depth = res->depth; ma.residual = res->residual;
+    ma.row_res = res->row_residual; ma.col_res = res->col_residual; ma.status = res->status;
+    HIP_TRY(launch_move(ma, A, maxpad, st));
+    if (res->order) HIP_TRY(launch_order(res->depth, W, res->order, st));
+  }
+  std::vector<int32_t> depth(W), status(W);
+  HIP_TRY(hipMemcpyAsync(depth.data(), res->depth, sizeof(int32_t) * W, hipMemcpyDeviceToHost, st));
+  HIP_TRY(hipMemcpyAsync(status.data(), res->status, sizeof(int32_t) * W, hipMemcpyDeviceToHost, st));
+  HIP_TRY(hipStreamSynchronize(st));
+  HIP_TRY(hipGetLastError());
+  if (stats) {
+    ds_stats S;
+    std::memset(&S, 0, sizeof(S));
+    int lmax = 0;
+    int64_t sum_l = 0;
+    for (int t = 0; t < W; ++t) { lmax = std::max(lmax, depth[t]); sum_l += depth[t]; }
+    S.l_max = lmax;
+    S.slots_update = active ? sum_l : (int64_t)W * lmax;
+    S.pair_evals = (int64_t)ctrl.upd_pairs;
+    S.check_pair_evals = (int64_t)ctrl.chk_pairs;
+    S.halfsteps_executed = 0;
+    // every lane ran its l_t cycles; a lane retired at an ordinary audit also
+    // ran the cycle after it (its discarded f-half and the g-half that shared
+    // the launch with its check)
+    S.halfsteps_executed = active ? 2 * sum_l + 2 * (int64_t)ctrl.retire_events
+                                  : 2 * (int64_t)W * (lmax + (ctrl.finished ? 1 : 0));
+    S.cycles = launched;
+    S.audits = 0;
+    for (int k = 1; k <= launched; ++k) S.audits += (k % ae == 0) ? 1 : 0;
+    S.screen_positive = ctrl.screen_pos;
+    S.check_failures = ctrl.check_fail;
+    S.missed_ready = ctrl.missed_ready;
+    S.compactions = compactions;
+    S.update_launches = (int)tm.spans[0].size();   // timed (sampled) launches
+    S.workspace_bytes = L.bytes;
+    S.bytes_compacted = bytes_compacted;
+    if (stats->width_trace && stats->width_trace_len > 0) {
+      const int cap = stats->width_trace_len;
+      int n = 0;
+      for (int k = 1; k <= lmax && n < cap; ++k, ++n) {
+        int Ak = 0;
+        for (int t = 0; t < W; ++t) Ak += (active ? depth[t] >= k : 1);
+        stats->width_trace[n] = Ak;
+      }
+      S.width_trace_len = n;
+    }
+    S.width_trace = stats->width_trace;
+    if (tm.on && nsamp > 0) {
+      std::vector<unsigned long long> sp(nsamp);
+      HIP_TRY(hipMemcpy(sp.data(), L.samp, sizeof(unsigned long long) * nsamp, hipMemcpyDeviceToHost));
+      int64_t tp = 0;
+      for (auto v : sp) tp += (int64_t)v;
+      S.timed_pair_evals = tp;
+    }
+    if (tm.on) {
+      S.ms_update = tm.total(0);
+      S.ms_compact = tm.total(1);
+      S.ms_check = 0.0;
+    }
+    S.ms_total = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t_start).count();
+    *stats = S;
+  }
+  return DS_OK;
+}
+
+}  // extern "C"

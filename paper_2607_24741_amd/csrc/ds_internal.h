@@ -1,0 +1,225 @@
+// Internal layout shared by the host runtime (ds_host.cpp) and the gfx950
+// kernels (ds_kernels.hip). Not part of the public ABI.
+//
+// Representation. Per lane the points are centred (c = mean of the live source
+// points and target points, averaged) and scaled by sqrt(2 kappa), where
+// kappa = log2(e) / eps. With x~ = sqrt(2 kappa)(x - c) and likewise y~, every
+// exponent of the method is an affine function of the dot product x~ . y~ in
+// base-2 units:
+//     kappa (g_j - C_ij) + kappa |x_i - c|^2 = gam^y_j + x~_i . y~_j,
+//     gam^y_j = kappa (g_j - |y_j - c|^2),
+// and the f-half of eq:sinkhorn-cycle becomes
+//     lse^x_i = log2 sum_j 2^(gam^y_j + x~_i . y~_j),   gam^x_i = log2 a_i - lse^x_i,
+// with f_i = (gam^x_i + |x~_i|^2 / 2) / kappa. The g-half is the same with the
+// roles of the two sides swapped. Per point the state kept is lse (the row
+// role's log-sum, used as the anchor of the next update and for the screen) and
+// gam = log2 mass - lse (the column role's operand); both are stored by cycle
+// parity so the audited state k survives while cycle k+1 is computed.
+//
+// The row marginal ratio of the state (f^k, g^k) is exactly
+//     R_i / a_i = 2^(lse^x_i(k+1) - lse^x_i(k)),
+// so the f-update of cycle k+1 yields the row screen of state k with no extra
+// pass over (i, j) (eq:updated-marginal makes the column marginal the current
+// one; Sec. 3.1).
+#pragma once
+
+#include <stdint.h>
+
+#include <hip/hip_runtime.h>
+
+namespace ds {
+
+constexpr int kPad = 128;        // point padding of every lane-indexed array
+constexpr int kColTile = 32;     // columns per MFMA tile
+constexpr int kColGroups = 4;    // waves per work item, each sweeping one column quarter
+constexpr int kRowsMfma = 32;    // rows per work item, matrix-core kernel
+constexpr int kRowsValu = 64;    // rows per work item, vector-ALU kernel
+constexpr int kMaxW = 4096;
+constexpr int kMaxDSmall = 32;   // matrix-free kernels
+constexpr float kFastRange = 64.f;  // max spread of the bound (log2 units) for anchored sums
+constexpr int kMaxSamples = 4096;   // timed launches per solve (DS_F_TIMING)
+
+// Per physical slot lane descriptor; moved by compaction with the rest of the
+// lane-indexed state.
+struct SlotInfo {
+  int lane;        // caller lane id
+  int n, m;        // valid prefix sizes
+  int done;        // retired (active, logical) -- its work items no longer run
+  int passed;      // static mode: first passing audit seen (lane keeps updating)
+  float kappa;     // log2(e) / eps
+  // spread of the latest change of lse on each side (for the anchored sums):
+  // valid flag, min and max of (lse_new - lse_old) over live points
+  int bx_ok, by_ok;
+  float bx_min, bx_max, by_min, by_max;
+  int pad;
+};
+
+// Control block (device). Counters written by kernels, read by the host.
+struct Ctrl {
+  int err_lane;      // first lane failing validation (0x7fffffff none)
+  int err_code;      // 1 n out of range, 2 m out of range, 3 eps invalid
+  int n_active;      // lanes not yet retired (static: not yet passed)
+  int n_retired;     // lanes retired so far (active / logical)
+  int finished;      // every lane retired / passed: later work items exit
+  int final_cycle;   // audit cycle at which the last lane passed (static)
+  int A;             // slots in the current (compacted) layout
+  int items_f, items_g;            // work items of the current layout
+  int items_act_f, items_act_g;    // work items of the lanes still active
+  int screen_pos;    // screen-positive events
+  int check_fail;    // screen-positive lanes rejected by the two-sided check
+  int missed_ready;  // shadow mode: screen-negative lanes that would pass
+  int retire_events; // retirements at ordinary audits (each ran one extra cycle)
+  int compacted;     // retired lanes already removed by compaction
+  int A_prev;        // width before the latest compaction map
+  int pad2;
+  unsigned long long upd_pairs;  // valid (i, j) terms evaluated by update passes
+  unsigned long long chk_pairs;  // valid (i, j) terms evaluated by marginal checks
+};
+
+// Best-effort mirror of the control counters in pinned host memory, written
+// by the device with system-scope stores (no copy on the stream).
+struct HostSnap {
+  int n_active, n_retired, compacted, epoch, finished, items_act_f, items_act_g, pad;
+};
+
+// Per slot audit scratch (indexed by the slot at audit time).
+struct Audit {
+  float rhat;    // row residual (fused screen, or row check at the final audit)
+  float rcol;    // column residual from the check
+  int flag;      // screen-positive at the latest audit
+  int pad;
+};
+
+// Retirement record of a slot (written when the lane is decided).
+struct Decision {
+  int status;    // ds_lane_status
+  int depth;     // completion depth (cycles)
+  float res_row, res_col;
+  int new_slot;  // compaction map (scan output), -1 for emitted lanes
+  int pad[3];
+};
+
+// One bank of lane-indexed state (two banks ping-pong under compaction).
+struct Bank {
+  float* rec[2];     // side 0 (x), side 1 (y): [W][pad][dp] scaled, centred, de-interleaved
+  float* lm[2];      // log2 masses [W][pad]; -inf for dead points
+  float* lse[2][2];  // [side][parity] [W][pad]; +inf for dead points
+  float* gam[2][2];  // [side][parity] [W][pad]; -inf for dead points
+  SlotInfo* slot;    // [W]
+  Decision* dec;     // [W]
+};
+
+// Row-block aggregates, indexed by caller lane id (they never move):
+// {screen or residual partial sum, min and max of the lse change, non-finite
+// flag}. [0] f-half, [1] g-half, [2] row check, [3] column check.
+enum { AGG_F = 0, AGG_G = 1, AGG_ROW = 2, AGG_COL = 3 };
+
+struct Layout {
+  int W, n_max, m_max, d, dp, dh;
+  int pad[2];        // npad, mpad
+  int rbmax;         // max row blocks of either side
+  int rows;          // rows per work item (kernel dependent)
+  Bank bank[2];
+  float* center;     // [W][d] (ingest only)
+  float4* agg[4];    // [W][rbmax]
+  int* vcnt;         // [W] column-check arrival counters
+  unsigned long long* samp;  // [kMaxSamples] pair counts of timed launches
+  Audit* audit;      // [W]
+  int* off[2];       // work item offsets per role [W + 1]
+  Ctrl* ctrl;
+  size_t bytes;
+};
+
+// work items of one lane-side: one per block of `rows` rows (all columns)
+__host__ __device__ inline int row_blocks(int nrows, int rows) { return (nrows + rows - 1) / rows; }
+
+
+// ------------------------------------------------------ kernel arguments
+// One pass = one half-step (kind 0) or one marginal check (kind 1) over the
+// slots of the current bank. A launch runs one or two passes.
+struct Pass {
+  const float* rec_row;   // [W][padr][dp]
+  const float* rec_col;   // [W][padc][dp]
+  const float* lm_row;    // [W][padr] log2 masses of the row side
+  const float* lse_in;    // [W][padr] row lse of the input state
+  float* lse_out;         // [W][padr] (update kind)
+  float* gam_out;         // [W][padr] (update kind)
+  const float* gam_col;   // [W][padc] column operand
+  const float* w_row;     // caller masses of the row side, [W][w_ld] by lane id
+  const int* off;         // [A + 1] work item offsets (ipl == 0)
+  float4* agg_out;        // [W][rbmax] this pass's row-block aggregates
+  const float4* agg_bound;   // update: the column side's latest update aggregates
+  const float4* agg_screen;  // column check: the f-half aggregates (row screen)
+  const float4* agg_rowchk;  // final column check: the row-check aggregates
+  int A, ipl;             // slots; uniform items per lane (0: use off)
+  int padr, padc, w_ld;
+  int role;               // 0: rows are x (f-half), 1: rows are y (g-half)
+  int kind;               // 0: update, 1: check (marginal ratio of the input state)
+  int verify_all;         // check: every live lane, else screen-positive lanes only
+  int decide;             // role 1 check: take the retirement decision
+  int final_audit;        // the decision is the max_iter audit
+  int depth;              // depth of the audited state
+};
+
+struct Launch {
+  Pass p[2];
+  int nb0;                // blocks of pass 0; the rest belong to pass 1
+  int dp, rbmax, mode, rows;
+  float tau_screen, tol;
+  SlotInfo* slot;
+  Decision* dec;
+  Audit* audit;
+  int* vcnt;
+  Ctrl* ctrl;
+  HostSnap* hsnap;                // may be null
+  unsigned long long* samp;       // timed launch: its (i, j) term count (may be null)
+};
+
+struct ScanArgs {          // compaction map over the slots of the current bank
+  SlotInfo* slot;
+  Decision* dec;
+  int* off_f;             // [W + 1] rewritten for the new layout
+  int* off_g;
+  Ctrl* ctrl;
+  HostSnap* hsnap;
+  int A, W, compact, rows, epoch;
+};
+
+struct MoveArgs {
+  Bank src, dst;
+  const Ctrl* ctrl;       // compaction: iterate the slots of the width before the map
+  int A, dp, compact, emit_all, mode;
+  int pad[2];
+  int n_max, m_max;
+  int final_par;          // parity of the final state (static mode emission)
+  int chunk;              // points per block per side
+  const Audit* audit;     // static mode: residuals of the final state
+  // outputs (caller order)
+  float* f; float* g; int* depth; float* residual; float* row_res; float* col_res;
+  int* status;
+};
+
+struct IngestArgs {
+  const float* X; const float* Y; const float* a; const float* b; const float* eps;
+  const int* n; const int* m;
+  int W, n_max, m_max, d, dp, dh;
+  int pad[2];
+  Bank bank;
+  float* center;
+  float4* agg[4];
+  int* vcnt;
+  int rbmax;
+  Ctrl* ctrl;
+};
+
+hipError_t launch_update(const Launch& a, int d, bool use_mfma, int blocks, hipStream_t st);
+hipError_t launch_scan(const ScanArgs& a, hipStream_t st);
+hipError_t launch_offsets(SlotInfo* slot, int A, int rows, int* off_f, int* off_g, Ctrl* ctrl,
+                          hipStream_t st);
+hipError_t launch_move(const MoveArgs& a, int A, int maxpad, hipStream_t st);
+hipError_t launch_ingest(const IngestArgs& a, int maxpad, hipStream_t st);
+hipError_t launch_order(const int* depth, int W, int* order, hipStream_t st);
+hipError_t launch_zero_counters(int* vcnt, int W, hipStream_t st);
+hipError_t launch_zero_u64(unsigned long long* p, int n, hipStream_t st);
+
+}  // namespace ds

@@ -1,0 +1,87 @@
+"""C-ABI checks that need no GPU: the built library loads, exports every
+function include/ds.h declares, and rejects bad arguments on the host before
+any device work (no compute call is made here)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_24741_amd as ds
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ds.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[A-Za-z_][A-Za-z0-9_\s\*]*?\b(ds_[a-z_]+)\s*\(",
+                                 text, flags=re.M)))
+
+
+def test_library_exports_every_declared_function():
+    lib = ds.load_library()
+    names = _declared_functions()
+    assert set(names) == {"ds_api_version", "ds_workspace_bytes", "ds_solve", "ds_error_string",
+                          "ds_last_error_message"}
+    for nm in names:
+        assert hasattr(lib, nm), nm
+    assert lib.ds_api_version() == 1
+    for code in range(6):
+        assert lib.ds_error_string(code).decode()
+
+
+def _problem(**kw):
+    p = dict(W=4, n_max=100, m_max=90, d=3)
+    p.update(kw)
+    return ds._Problem(**p)
+
+
+def _bytes(pr, op):
+    lib = ds.load_library()
+    out = ctypes.c_size_t(0)
+    code = lib.ds_workspace_bytes(ctypes.byref(pr), ctypes.byref(op), ctypes.byref(out))
+    return code, out.value
+
+
+def test_workspace_query_and_validation():
+    op = ds._options(1e-3, None, 100, 1, "active", 0)
+    code, n = _bytes(_problem(), op)
+    assert code == 0 and n > 0 and n % 256 == 0
+    code2, n2 = _bytes(_problem(W=8), op)
+    assert code2 == 0 and n2 > n
+    for bad in (dict(W=0), dict(n_max=0), dict(m_max=-1), dict(d=0), dict(d=513)):
+        assert _bytes(_problem(**bad), op)[0] == 1, bad
+    assert _bytes(_problem(W=5000), op)[0] == 4
+    for tol, mi, ae, mode in ((0.0, 10, 1, 0), (1e-3, 0, 1, 0), (1e-3, 10, 0, 0), (1e-3, 10, 1, 7)):
+        o = ds._Options(tol=tol, screen_tol=0.0, max_iter=mi, audit_every=ae, mode=mode, flags=0)
+        assert _bytes(_problem(), o)[0] == 1
+    o = ds._Options(tol=1e-3, screen_tol=0.0, max_iter=10, audit_every=1, mode=0, flags=4 | 8)
+    assert _bytes(_problem(), o)[0] == 1
+    assert ds.load_library().ds_last_error_message().decode()
+
+
+def test_solve_rejects_bad_arguments_before_device_work():
+    lib = ds.load_library()
+    op = ds._options(1e-3, None, 100, 1, "active", 0)
+    res = ds._Result()
+    st = ds._Stats()
+    # NULL problem / NULL inputs / NULL outputs / missing workspace: all host-side
+    assert lib.ds_solve(None, ctypes.byref(op), ctypes.byref(res), None, 0, None, None) == 1
+    pr = _problem()
+    assert lib.ds_solve(ctypes.byref(pr), ctypes.byref(op), ctypes.byref(res), None, 0, None,
+                        ctypes.byref(st)) == 1
+    fake = ctypes.c_void_p(0x1000)
+    pr = _problem(X=fake, Y=fake, a=fake, b=fake, eps=fake)
+    assert lib.ds_solve(ctypes.byref(pr), ctypes.byref(op), ctypes.byref(res), None, 0, None,
+                        None) == 1
+    res = ds._Result(f=fake, g=fake, depth=fake, residual=fake, status=fake)
+    assert lib.ds_solve(ctypes.byref(pr), ctypes.byref(op), ctypes.byref(res), None, 0, None,
+                        None) == 2
+    assert lib.ds_solve(ctypes.byref(pr), ctypes.byref(op), ctypes.byref(res),
+                        ctypes.c_void_p(0x1001), 1 << 30, None, None) == 2
+    assert lib.ds_solve(ctypes.byref(pr), ctypes.byref(op), ctypes.byref(res),
+                        ctypes.c_void_p(0x1000), 16, None, None) == 2
+    assert "workspace" in lib.ds_last_error_message().decode()
