@@ -130,8 +130,11 @@ typedef struct {
                                  sum_t l_t (active), W * l_max (static, logical)  */
   int64_t halfsteps_executed; /* lane-half-steps launched, incl. the discarded
                                  f-half of each retired lane                       */
-  int64_t pair_evals;         /* valid (i, j) terms evaluated by the half-steps      */
-  int64_t check_pair_evals;   /* valid (i, j) terms evaluated by marginal checks     */
+  int64_t pair_evals;         /* (i, j) terms of the kept half-steps:
+                                 2 sum_t l_t n_t m_t (active), 2 l_max sum_t n_t m_t
+                                 (static, logical); speculative halves excluded    */
+  int64_t check_pair_evals;   /* (i, j) terms of the two-sided checks: one marginal
+                                 pass per ordinary check, two at the final audit  */
   int64_t bytes_compacted;    /* bytes moved by survivor gathers                    */
   int32_t l_max, cycles, audits, screen_positive, check_failures, compactions;
   int32_t missed_ready;       /* DS_F_SHADOW only                                   */
@@ -140,7 +143,9 @@ typedef struct {
   double ms_update;           /* DS_F_TIMING: summed event time of the timed launches
                                  (both launches of every 32nd cycle, and the final
                                  audit), bracketed by HIP events on the stream     */
-  int64_t timed_pair_evals;   /* DS_F_TIMING: (i, j) terms evaluated by those launches */
+  int64_t timed_pair_evals;   /* DS_F_TIMING: algorithmic (i, j) terms of those
+                                 launches (lanes running at that cycle; the checks
+                                 sharing a g-launch are not counted)               */
   double ms_check;            /* reserved (checks share the g-half launches)         */
   double ms_compact;          /* DS_F_TIMING: compaction (scan + gather) launches     */
   int32_t* width_trace;       /* optional HOST buffer: A_k for k = 1..             */

@@ -84,7 +84,7 @@ ds::Layout plan(const ds_problem* pr, const ds_options* op, void* ws) {
   L.center = c.take<float>(W * (size_t)L.d);
   for (int k = 0; k < 4; ++k) L.agg[k] = c.take<float4>(W * (size_t)L.rbmax);
   L.vcnt = c.take<int>(W);
-  L.samp = c.take<unsigned long long>(ds::kMaxSamples);
+  L.nchk = c.take<int>(W);
   L.audit = c.take<ds::Audit>(W);
   L.off[0] = c.take<int>(W + 1);
   L.off[1] = c.take<int>(W + 1);
@@ -262,7 +262,7 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
   ia.bank = L.bank[0];
   ia.center = L.center;
   for (int k = 0; k < 4; ++k) ia.agg[k] = L.agg[k];
-  ia.vcnt = L.vcnt; ia.rbmax = L.rbmax;
+  ia.vcnt = L.vcnt; ia.nchk = L.nchk; ia.rbmax = L.rbmax;
   ia.ctrl = L.ctrl;
   HIP_TRY(launch_ingest(ia, maxpad, st));
   HIP_TRY(launch_offsets(L.bank[0].slot, W, L.rows, L.off[0], L.off[1], L.ctrl, st));
@@ -322,21 +322,24 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
     l.tol = op->tol;
     l.slot = L.bank[bank].slot; l.dec = L.bank[bank].dec;
     l.audit = L.audit; l.vcnt = L.vcnt; l.ctrl = L.ctrl;
-    l.hsnap = R->snap_dev; l.samp = nullptr;
+    l.hsnap = R->snap_dev; l.nchk = L.nchk;
     return l;
   };
-  // DS_F_TIMING: every kSampleEvery-th cycle's launches are bracketed by
-  // events and count their own (i, j) terms; the rest run untouched
+  // DS_F_TIMING: both launches of every kSampleEvery-th cycle (and the final
+  // audit) are bracketed by events; the rest run untouched. Each timed launch
+  // remembers its cycle so its algorithmic (i, j) terms can be counted from the
+  // completion depths afterwards (kind 0: update halves of cycle k, kind 1:
+  // one marginal pass of the final audit).
   constexpr int kSampleEvery = 32;
-  int nsamp = 0;
-  auto run = [&](Launch l, int blocks, bool sample) -> ds_err {
-    const bool timed = tm.on && sample && nsamp < kMaxSamples;
-    if (timed) l.samp = L.samp + nsamp;
+  struct Timed { int cycle, kind; };
+  std::vector<Timed> timed_launches;
+  auto run = [&](Launch l, int blocks, bool sample, int cycle, int kind) -> ds_err {
+    const bool timed = tm.on && sample && (int)timed_launches.size() < kMaxTimed;
     const int e0 = timed ? tm.rec() : -1;
     HIP_TRY(launch_update(l, d, use_mfma, blocks, st));
     if (timed) {
       tm.spans[0].push_back({e0, tm.rec()});
-      nsamp++;
+      timed_launches.push_back({cycle, kind});
     }
     return DS_OK;
   };
@@ -348,7 +351,6 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
   volatile HostSnap* hs = R->snap;
   hs->n_active = W; hs->n_retired = 0; hs->compacted = 0; hs->epoch = 0; hs->finished = 0;
   hs->items_act_f = items[0]; hs->items_act_g = items[1];
-  if (tm.on) HIP_TRY(launch_zero_u64(L.samp, kMaxSamples, st));
   struct Pending { int idx, cycle; };
   std::vector<Pending> q;
   int ring_next = 0, epoch = 0;
@@ -404,7 +406,7 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
     lf.p[0] = make_pass(0, 0, pk1, pk, pk1);
     lf.p[0].depth = k - 1;
     lf.nb0 = items[0];
-    ds_err r = run(lf, items[0], sample);
+    ds_err r = run(lf, items[0], sample, k, 0);
     if (r != DS_OK) return r;
     // g-half of cycle k (+ column check and decision for state k-1)
     // (the check blocks come first: most of them exit at once)
@@ -422,7 +424,7 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
       lg.p[0] = make_pass(1, 0, pk1, pk, pk);
       lg.nb0 = items[1];
     }
-    r = run(lg, blocks, sample);
+    r = run(lg, blocks, sample, k, 0);
     if (r != DS_OK) return r;
     launched = k;
     if (k % kEvery == 0) {
@@ -449,13 +451,13 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
     lv.p[0].final_audit = 1; lv.p[0].depth = K; lv.p[0].verify_all = 1;
     lv.nb0 = ctrl.items_f;
     int saveA = A;
-    ds_err r = run(lv, ctrl.items_f, true);
+    ds_err r = run(lv, ctrl.items_f, true, K, 1);
     if (r != DS_OK) return r;
     Launch lw = make_launch();
     lw.p[0] = make_pass(1, 1, pK, pK, pK);
     lw.p[0].final_audit = 1; lw.p[0].decide = 1; lw.p[0].depth = K; lw.p[0].verify_all = 1;
     lw.nb0 = ctrl.items_g;
-    r = run(lw, ctrl.items_g, true);
+    r = run(lw, ctrl.items_g, true, K, 1);
     if (r != DS_OK) return r;
     A = saveA;
     HIP_TRY(hipStreamSynchronize(st));
@@ -488,8 +490,20 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
     for (int t = 0; t < W; ++t) { lmax = std::max(lmax, depth[t]); sum_l += depth[t]; }
     S.l_max = lmax;
     S.slots_update = active ? sum_l : (int64_t)W * lmax;
-    S.pair_evals = (int64_t)ctrl.upd_pairs;
-    S.check_pair_evals = (int64_t)ctrl.chk_pairs;
+    // (i, j) term counts from the completion depths: a lane runs both halves
+    // of every cycle up to its depth (active) or up to l_max (static, logical);
+    // speculative halves are not algorithmic work and are not counted here
+    std::vector<int64_t> nm(W);
+    for (int t = 0; t < W; ++t) nm[t] = (int64_t)lanes[t].n * (int64_t)lanes[t].m;
+    std::vector<int32_t> nchk(W);
+    HIP_TRY(hipMemcpy(nchk.data(), L.nchk, sizeof(int32_t) * W, hipMemcpyDeviceToHost));
+    int64_t upd = 0, chk = 0;
+    for (int t = 0; t < W; ++t) {
+      upd += 2 * (int64_t)(active ? depth[t] : lmax) * nm[t];
+      chk += (int64_t)nchk[t] * nm[t];
+    }
+    S.pair_evals = upd;
+    S.check_pair_evals = chk;
     S.halfsteps_executed = 0;
     // every lane ran its l_t cycles; a lane retired at an ordinary audit also
     // ran the cycle after it (its discarded f-half and the g-half that shared
@@ -517,11 +531,17 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
       S.width_trace_len = n;
     }
     S.width_trace = stats->width_trace;
-    if (tm.on && nsamp > 0) {
-      std::vector<unsigned long long> sp(nsamp);
-      HIP_TRY(hipMemcpy(sp.data(), L.samp, sizeof(unsigned long long) * nsamp, hipMemcpyDeviceToHost));
+    if (tm.on) {
+      // algorithmic terms of the timed launches: one half-step over the lanes
+      // still running at that cycle, or one marginal pass of the final audit
       int64_t tp = 0;
-      for (auto v : sp) tp += (int64_t)v;
+      for (const Timed& q : timed_launches) {
+        for (int t = 0; t < W; ++t) {
+          const bool in = q.kind == 0 ? (active ? depth[t] >= q.cycle : q.cycle <= lmax)
+                                      : (mode == DS_MODE_STATIC || depth[t] == q.cycle);
+          if (in) tp += nm[t];
+        }
+      }
       S.timed_pair_evals = tp;
     }
     if (tm.on) {

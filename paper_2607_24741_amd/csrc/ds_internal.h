@@ -37,7 +37,7 @@ constexpr int kRowsValu = 64;    // rows per work item, vector-ALU kernel
 constexpr int kMaxW = 4096;
 constexpr int kMaxDSmall = 32;   // matrix-free kernels
 constexpr float kFastRange = 64.f;  // max spread of the bound (log2 units) for anchored sums
-constexpr int kMaxSamples = 4096;   // timed launches per solve (DS_F_TIMING)
+constexpr int kMaxTimed = 4096;     // timed launches per solve (DS_F_TIMING)
 
 // Per physical slot lane descriptor; moved by compaction with the rest of the
 // lane-indexed state.
@@ -72,8 +72,6 @@ struct Ctrl {
   int compacted;     // retired lanes already removed by compaction
   int A_prev;        // width before the latest compaction map
   int pad2;
-  unsigned long long upd_pairs;  // valid (i, j) terms evaluated by update passes
-  unsigned long long chk_pairs;  // valid (i, j) terms evaluated by marginal checks
 };
 
 // Best-effort mirror of the control counters in pinned host memory, written
@@ -123,7 +121,7 @@ struct Layout {
   float* center;     // [W][d] (ingest only)
   float4* agg[4];    // [W][rbmax]
   int* vcnt;         // [W] column-check arrival counters
-  unsigned long long* samp;  // [kMaxSamples] pair counts of timed launches
+  int* nchk;         // [W] marginal evaluation passes spent on checks, per caller lane
   Audit* audit;      // [W]
   int* off[2];       // work item offsets per role [W + 1]
   Ctrl* ctrl;
@@ -172,7 +170,7 @@ struct Launch {
   int* vcnt;
   Ctrl* ctrl;
   HostSnap* hsnap;                // may be null
-  unsigned long long* samp;       // timed launch: its (i, j) term count (may be null)
+  int* nchk;                      // [W] check passes per caller lane
 };
 
 struct ScanArgs {          // compaction map over the slots of the current bank
@@ -208,6 +206,7 @@ struct IngestArgs {
   float* center;
   float4* agg[4];
   int* vcnt;
+  int* nchk;
   int rbmax;
   Ctrl* ctrl;
 };
@@ -220,6 +219,5 @@ hipError_t launch_move(const MoveArgs& a, int A, int maxpad, hipStream_t st);
 hipError_t launch_ingest(const IngestArgs& a, int maxpad, hipStream_t st);
 hipError_t launch_order(const int* depth, int W, int* order, hipStream_t st);
 hipError_t launch_zero_counters(int* vcnt, int W, hipStream_t st);
-hipError_t launch_zero_u64(unsigned long long* p, int n, hipStream_t st);
 
 }  // namespace ds

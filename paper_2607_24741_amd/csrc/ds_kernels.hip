@@ -174,32 +174,30 @@ __device__ __forceinline__ LaneAgg lane_aggregate(const float4* agg, int lane_id
   return g;
 }
 
-// Per work item lane facts, computed once per block and broadcast via LDS:
-// anchored-sum bound for updates, the row screen for column checks.
-struct LaneFacts {
-  int run;      // check passes: this lane is checked
-  int fast;     // update: anchored (max-free) sums are safe
-  float M;      // update: max change of the column operand
-  float rhat;   // column check: row residual of the audited state (screen)
-};
-// Every wave reduces the aggregates itself (same bits in every wave), so no
-// LDS broadcast or barrier sits between the block's loads and its sweep.
-__device__ LaneFacts lane_facts(const Launch& L, const Pass& P, const SlotInfo& si) {
-  LaneFacts f;
-  f.run = 1; f.fast = 0; f.M = 0.f; f.rhat = NAN;
+// Lane facts every wave reduces itself (same bits in every wave), so no LDS
+// broadcast or barrier sits between the block's loads and its sweep.
+//
+// Update: lse_new - lse_old lies in [min_j dgam_j, max_j dgam_j], dgam being
+// the latest change of the column operand (= -(change of the column lse)), so
+// anchored (max-free) sums are safe when that spread is small; M = -min dgam.
+__device__ __forceinline__ void update_facts(const Launch& L, const Pass& P, const SlotInfo& si,
+                                             bool& fast, float& M) {
   const int ncols = P.role ? si.n : si.m;
-  if (P.kind == KIND_UPDATE) {
-    // lse_new - lse_old lies in [min_j dgam_j, max_j dgam_j], dgam being the
-    // latest change of the column operand (= -(change of the column lse))
-    const LaneAgg g = lane_aggregate(P.agg_bound, si.lane, L.rbmax, row_blocks(ncols, L.rows), false);
-    f.fast = !g.bad && g.dmin <= g.dmax && (g.dmax - g.dmin) <= kFastRange;
-    f.M = -g.dmin;
-  } else if (P.role == 1 && !P.final_audit) {
+  const LaneAgg g = lane_aggregate(P.agg_bound, si.lane, L.rbmax, row_blocks(ncols, L.rows), false);
+  fast = !g.bad && g.dmin <= g.dmax && (g.dmax - g.dmin) <= kFastRange;
+  M = -g.dmin;
+}
+// Check: whether this lane is checked at all (screen-positive, non-finite
+// screen, or every lane), and the row screen of the audited state.
+__device__ __forceinline__ bool check_facts(const Launch& L, const Pass& P, const SlotInfo& si,
+                                            float& rhat) {
+  rhat = NAN;
+  if (P.role == 1 && !P.final_audit) {
     const LaneAgg g = lane_aggregate(P.agg_screen, si.lane, L.rbmax, row_blocks(si.n, L.rows), false);
-    f.rhat = g.sum;
-    f.run = P.verify_all || !isfinite(g.sum) || g.sum <= L.tau_screen;
+    rhat = g.sum;
+    return P.verify_all || !isfinite(g.sum) || g.sum <= L.tau_screen;
   }
-  return f;
+  return true;
 }
 
 // -------------------------------------------------------- block epilogue
@@ -211,7 +209,7 @@ __device__ LaneFacts lane_facts(const Launch& L, const Pass& P, const SlotInfo& 
 template <int NWAVES>
 __device__ void finish_block(const Launch& L, const Pass& P, int s, const SlotInfo& si, int rb,
                              int i, bool owner, bool live, bool fast, float anchor, float lse_old,
-                             float lm, float w, float M, float sum, float rhat, int rows_here) {
+                             float lm, float w, float M, float sum, float rhat) {
   __shared__ float sh_red[4][NWAVES];
   __shared__ int sh_last;
   const bool frozen = (L.mode == MODE_LOGICAL) && si.done;
@@ -254,7 +252,6 @@ __device__ void finish_block(const Launch& L, const Pass& P, int s, const SlotIn
     sh_red[3][wave] = (float)r3;
   }
   __syncthreads();
-  const int ncols = P.role ? si.n : si.m;
   if (threadIdx.x == 0) {
     float4 a = make_float4(0.f, INFINITY, -INFINITY, 0.f);
     for (int w = 0; w < NWAVES; ++w) {
@@ -264,14 +261,10 @@ __device__ void finish_block(const Launch& L, const Pass& P, int s, const SlotIn
       a.w = fmaxf(a.w, sh_red[3][w]);
     }
     float4* dst = P.agg_out + (size_t)si.lane * L.rbmax + rb;
-    const unsigned long long pairs = (unsigned long long)rows_here * (unsigned long long)ncols;
-    if (L.samp) atomicAdd(L.samp, pairs);
     if (P.kind == KIND_UPDATE) {
       *dst = a;
-      atomicAdd(&L.ctrl->upd_pairs, pairs);
       sh_last = 0;
     } else {
-      atomicAdd(&L.ctrl->chk_pairs, pairs);
       if (P.role == 0 || !P.decide) {
         *dst = a;
         sh_last = 0;
@@ -295,6 +288,9 @@ __device__ void finish_block(const Launch& L, const Pass& P, int s, const SlotIn
     rrow = gr.sum;
   }
   if (threadIdx.x != 0) return;
+  // marginal evaluations spent on this lane's check (the final audit
+  // evaluates both marginals)
+  atomicAdd(&L.nchk[si.lane], P.final_audit ? 2 : 1);
   const float rcol = gc.sum;
   L.audit[s].rhat = rrow;
   L.audit[s].rcol = rcol;
@@ -322,18 +318,33 @@ __device__ void finish_block(const Launch& L, const Pass& P, int s, const SlotIn
   }
 }
 
-// Decide what a block does. Returns false when the block has no work.
-__device__ __forceinline__ bool locate_item(const Launch& L, const Pass& P, int item, int& s,
+// XCD-aware item order. Consecutive workgroups are dispatched to the 8 XCDs
+// in turn, so block b (x = b mod 8) takes item x*q + min(x, r) + b/8 of the
+// N = 8q + r items: every XCD works through one contiguous range of items --
+// whole lanes -- and its L2 holds only those lanes' column operands. The map
+// is a bijection of [0, N), so it changes which block runs an item, never
+// what the item computes.
+__device__ __forceinline__ int xcd_item(int b, int N) {
+  const int q = N >> 3, r = N & 7, x = b & 7;
+  return x * q + min(x, r) + (b >> 3);
+}
+
+// Decide what block b of a pass does. Returns false when it has no work.
+__device__ __forceinline__ bool locate_item(const Launch& L, const Pass& P, int b, int& s,
                                             int& rb, SlotInfo& si) {
   const Ctrl* c = L.ctrl;
   if (!P.final_audit && c->finished) return false;
   const int A = min(P.A, c->A);
   if (P.ipl > 0) {
+    const int N = P.ipl * A;
+    if (b >= N) return false;
+    const int item = xcd_item(b, N);
     s = item / P.ipl;
     rb = item - s * P.ipl;
-    if (s >= A) return false;
   } else {
-    if (item >= P.off[A]) return false;
+    const int N = P.off[A];
+    if (b >= N) return false;
+    const int item = xcd_item(b, N);
     s = find_slot(P.off, A, item);
     rb = item - P.off[s];
   }
@@ -359,12 +370,12 @@ __global__ __launch_bounds__(256, (DH <= 7 ? 8 : (DH <= 12 ? 6 : 4))) void k_upd
   const int b = blockIdx.x;
   const int pi = b >= L.nb0;
   const Pass P = pi ? L.p[1] : L.p[0];
-  const int item = pi ? b - L.nb0 : b;
   int s, rb;
   SlotInfo si;
-  if (!locate_item(L, P, item, s, rb, si)) return;
-  const LaneFacts lf = lane_facts(L, P, si);
-  if (!lf.run) return;
+  if (!locate_item(L, P, pi ? b - L.nb0 : b, s, rb, si)) return;
+  const bool upd = P.kind == KIND_UPDATE;
+  float rhat = NAN;
+  if (!upd && !check_facts(L, P, si, rhat)) return;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform (SGPR)
   const int h = lane >> 5;
@@ -374,23 +385,17 @@ __global__ __launch_bounds__(256, (DH <= 7 ? 8 : (DH <= 12 ? 6 : 4))) void k_upd
   const int i = rb * kRowsMfma + r;
   constexpr int DP = 2 * DH;
 
+  // Every load of the item (row data, first column tile) is issued before the
+  // update facts are reduced, so their latencies overlap.
   const size_t ridx = (size_t)s * P.padr + i;
   const float lse_old = P.lse_in[ridx];
   const float lm = P.lm_row[ridx];
   const bool in_prefix = i < nrows;
   const float w = in_prefix ? P.w_row[(size_t)si.lane * P.w_ld + i] : 0.f;
-  const bool live = in_prefix && (lse_old != INFINITY);
-  const bool fast = lf.fast;
-  float anchor = 0.f, bias = 0.f;
-  if (live) {
-    if (P.kind == KIND_VERIFY) bias = -lse_old;
-    else if (fast) { anchor = lse_old + lf.M; bias = -anchor; }
-  }
   float bv[DH + 1];
   const float* rrow = P.rec_row + ridx * DP + h * DH;
 #pragma unroll
   for (int k = 0; k < DH; ++k) bv[k] = rrow[k];
-  bv[DH] = h ? bias : 1.f;
 
   const int ct = (ncols + kColTile - 1) / kColTile;
   const int tpg = (ct + kColGroups - 1) / kColGroups;
@@ -398,16 +403,27 @@ __global__ __launch_bounds__(256, (DH <= 7 ? 8 : (DH <= 12 ? 6 : 4))) void k_upd
   const int t1 = min(ct, t0 + tpg);
   const float* ccol = P.rec_col + (size_t)s * P.padc * DP + h * DH + (size_t)r * DP;
   const float* gcol = P.gam_col + (size_t)s * P.padc + r;
-
-  float mrun = fast ? 0.f : -INFINITY, srun = 0.f;
-  // operand ping-pong: tile t+1 is in flight while tile t is reduced; the
-  // prefetch index is clamped so every load stays in range
   auto load = [&](int t, float* a) {
     const float* c = ccol + (size_t)t * kColTile * DP;
 #pragma unroll
     for (int k = 0; k < DH; ++k) a[k] = c[k];
     a[DH] = gcol[(size_t)t * kColTile];
   };
+  float A0[DH + 1], A1[DH + 1];
+  if (t0 < t1) load(t0, A0);
+
+  bool fast = false;
+  float M = 0.f;
+  if (upd) update_facts(L, P, si, fast, M);
+  const bool live = in_prefix && (lse_old != INFINITY);
+  float anchor = 0.f, bias = 0.f;
+  if (live) {
+    if (!upd) bias = -lse_old;
+    else if (fast) { anchor = lse_old + M; bias = -anchor; }
+  }
+  bv[DH] = h ? bias : 1.f;
+
+  float mrun = fast ? 0.f : -INFINITY, srun = 0.f;
   auto tile = [&](const float* a, bool anchored) {
     f32x16 acc = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -438,10 +454,10 @@ __global__ __launch_bounds__(256, (DH <= 7 ? 8 : (DH <= 12 ? 6 : 4))) void k_upd
       mrun = mn;
     }
   };
+  // operand ping-pong: tile t+1 is in flight while tile t is reduced; the
+  // prefetch index is clamped so every load stays in range
   auto sweep = [&](bool anchored) {
     if (t0 >= t1) return;
-    float A0[DH + 1], A1[DH + 1];
-    load(t0, A0);
     int t = t0;
     for (; t + 1 < t1; t += 2) {
       load(t + 1, A1);
@@ -474,9 +490,7 @@ __global__ __launch_bounds__(256, (DH <= 7 ? 8 : (DH <= 12 ? 6 : 4))) void k_upd
 #pragma unroll
     for (int g = 0; g < kColGroups; ++g) St += sh_part[g][r].y * ex2(sh_part[g][r].x - Mt);
   }
-  const int rows_here = min(kRowsMfma, nrows - rb * kRowsMfma);
-  finish_block<4>(L, P, s, si, rb, i, owner, live, fast, anchor, lse_old, lm, w, Mt, St, lf.rhat,
-                  rows_here);
+  finish_block<4>(L, P, s, si, rb, i, owner, live, fast, anchor, lse_old, lm, w, Mt, St, rhat);
 }
 
 // --------------------------------------------------------- VALU half-step
@@ -491,34 +505,37 @@ __global__ __launch_bounds__(256, 8) void k_update_valu(Launch L) {
   const int b = blockIdx.x;
   const int pi = b >= L.nb0;
   const Pass P = pi ? L.p[1] : L.p[0];
-  const int item = pi ? b - L.nb0 : b;
   int s, rb;
   SlotInfo si;
-  if (!locate_item(L, P, item, s, rb, si)) return;
-  const LaneFacts lf = lane_facts(L, P, si);
-  if (!lf.run) return;
+  if (!locate_item(L, P, pi ? b - L.nb0 : b, s, rb, si)) return;
+  const bool upd = P.kind == KIND_UPDATE;
+  float rhat = NAN;
+  if (!upd && !check_facts(L, P, si, rhat)) return;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform (SGPR)
   const int nrows = P.role ? si.m : si.n;
   const int ncols = P.role ? si.n : si.m;
   const int i = rb * kRowsValu + lane;
   constexpr int DP = 2 * DH;
+  // row loads are issued before the update facts are reduced
   const size_t ridx = (size_t)s * P.padr + i;
   const float lse_old = P.lse_in[ridx];
   const float lm = P.lm_row[ridx];
   const bool in_prefix = i < nrows;
   const float w = in_prefix ? P.w_row[(size_t)si.lane * P.w_ld + i] : 0.f;
-  const bool live = in_prefix && (lse_old != INFINITY);
-  const bool fast = lf.fast;
-  float anchor = 0.f, bias = 0.f;
-  if (live) {
-    if (P.kind == KIND_VERIFY) bias = -lse_old;
-    else if (fast) { anchor = lse_old + lf.M; bias = -anchor; }
-  }
   float xr[D];
   const float* rrow = P.rec_row + ridx * DP;
 #pragma unroll
   for (int k = 0; k < D; ++k) xr[k] = rrow[k];
+  bool fast = false;
+  float M = 0.f;
+  if (upd) update_facts(L, P, si, fast, M);
+  const bool live = in_prefix && (lse_old != INFINITY);
+  float anchor = 0.f, bias = 0.f;
+  if (live) {
+    if (!upd) bias = -lse_old;
+    else if (fast) { anchor = lse_old + M; bias = -anchor; }
+  }
 
   const int ct = (ncols + kColTile - 1) / kColTile;
   const int tpg = (ct + kColGroups - 1) / kColGroups;
@@ -578,9 +595,7 @@ __global__ __launch_bounds__(256, 8) void k_update_valu(Launch L) {
 #pragma unroll
     for (int g = 0; g < kColGroups; ++g) St += sh_part[g][lane].y * ex2(sh_part[g][lane].x - Mt);
   }
-  const int rows_here = min(kRowsValu, nrows - rb * kRowsValu);
-  finish_block<4>(L, P, s, si, rb, i, owner, live, fast, anchor, lse_old, lm, w, Mt, St, lf.rhat,
-                  rows_here);
+  finish_block<4>(L, P, s, si, rb, i, owner, live, fast, anchor, lse_old, lm, w, Mt, St, rhat);
 }
 
 // ------------------------------------------------------------- block scan
@@ -840,6 +855,7 @@ __global__ __launch_bounds__(256) void k_ingest_lanes(IngestArgs p) {
     d.pad[0] = d.pad[1] = d.pad[2] = 0;
     p.bank.dec[t] = d;
     p.vcnt[t] = 0;
+    p.nchk[t] = 0;
   }
   // no previous half-step: the first update of each side runs unanchored
   const float4 none = make_float4(0.f, INFINITY, -INFINITY, 1.f);
@@ -906,11 +922,6 @@ __global__ void k_zero_counters(int* vcnt, int W) {
   if (t < W) vcnt[t] = 0;
 }
 
-__global__ void k_zero_u64(unsigned long long* p, int n) {
-  const int t = blockIdx.x * blockDim.x + threadIdx.x;
-  if (t < n) p[t] = 0ull;
-}
-
 __global__ void k_ctrl_init(Ctrl* c, int W) {
   if (threadIdx.x == 0) {
     Ctrl z;
@@ -918,7 +929,6 @@ __global__ void k_ctrl_init(Ctrl* c, int W) {
     z.final_cycle = 0; z.A = W; z.items_f = 0; z.items_g = 0; z.items_act_f = 0;
     z.items_act_g = 0; z.screen_pos = 0; z.check_fail = 0; z.missed_ready = 0;
     z.retire_events = 0; z.compacted = 0; z.A_prev = W; z.pad2 = 0;
-    z.upd_pairs = 0ull; z.chk_pairs = 0ull;
     *c = z;
   }
 }
@@ -1009,10 +1019,6 @@ hipError_t launch_ingest(const IngestArgs& a, int maxpad, hipStream_t st) {
 }
 hipError_t launch_zero_counters(int* vcnt, int W, hipStream_t st) {
   hipLaunchKernelGGL(k_zero_counters, dim3((W + 255) / 256), dim3(256), 0, st, vcnt, W);
-  return hipGetLastError();
-}
-hipError_t launch_zero_u64(unsigned long long* p, int n, hipStream_t st) {
-  hipLaunchKernelGGL(k_zero_u64, dim3((n + 255) / 256), dim3(256), 0, st, p, n);
   return hipGetLastError();
 }
 hipError_t launch_order(const int* depth, int W, int* order, hipStream_t st) {
