@@ -333,10 +333,22 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
   constexpr int kSampleEvery = 32;
   struct Timed { int cycle, kind; };
   std::vector<Timed> timed_launches;
-  auto run = [&](Launch l, int blocks, bool sample, int cycle, int kind) -> ds_err {
+  // Kernel variant by the width bound of the launch: few items -> more waves
+  // per item (shorter sweeps); many items -> more rows per wave (fewer column
+  // re-reads). Every variant computes the same bits.
+  auto pick = [&](int items) -> int {
+    if (use_mfma && uniform && items >= kWideItems) return VAR_WIDE;
+    return items >= (use_mfma ? kMediumItemsMfma : kMediumItemsValu) ? VAR_MEDIUM : VAR_NARROW;
+  };
+  auto blocks_of = [&](int variant, int role, int items) -> int {
+    if (variant != VAR_WIDE || items <= 0) return std::max(items, 0);
+    const int lanes_ub = (items + ipl[role] - 1) / ipl[role];
+    return lanes_ub * ((ipl[role] + 1) / 2);
+  };
+  auto run = [&](Launch l, int variant, int blocks, bool sample, int cycle, int kind) -> ds_err {
     const bool timed = tm.on && sample && (int)timed_launches.size() < kMaxTimed;
     const int e0 = timed ? tm.rec() : -1;
-    HIP_TRY(launch_update(l, d, use_mfma, blocks, st));
+    HIP_TRY(launch_update(l, d, use_mfma, variant, blocks, st));
     if (timed) {
       tm.spans[0].push_back({e0, tm.rec()});
       timed_launches.push_back({cycle, kind});
@@ -405,26 +417,29 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
     Launch lf = make_launch();
     lf.p[0] = make_pass(0, 0, pk1, pk, pk1);
     lf.p[0].depth = k - 1;
-    lf.nb0 = items[0];
-    ds_err r = run(lf, items[0], sample, k, 0);
+    const int vf = pick(items[0]);
+    lf.nb0 = blocks_of(vf, 0, items[0]);
+    ds_err r = run(lf, vf, lf.nb0, sample, k, 0);
     if (r != DS_OK) return r;
     // g-half of cycle k (+ column check and decision for state k-1)
     // (the check blocks come first: most of them exit at once)
     Launch lg = make_launch();
-    int blocks = items[1];
+    const int vg = pick(items[1]);
+    const int nbg = blocks_of(vg, 1, items[1]);
+    int blocks = nbg;
     if (audit_prev) {
       lg.p[0] = make_pass(1, 1, pk1, pk1, pk1);   // column marginal of state k-1
       lg.p[0].decide = 1;
       lg.p[0].verify_all = shadow ? 1 : 0;
       lg.p[0].depth = k - 1;
       lg.p[1] = make_pass(1, 0, pk1, pk, pk);     // g-half of cycle k
-      lg.nb0 = items[1];
-      blocks += items[1];
+      lg.nb0 = nbg;
+      blocks += nbg;
     } else {
       lg.p[0] = make_pass(1, 0, pk1, pk, pk);
-      lg.nb0 = items[1];
+      lg.nb0 = nbg;
     }
-    r = run(lg, blocks, sample, k, 0);
+    r = run(lg, vg, blocks, sample, k, 0);
     if (r != DS_OK) return r;
     launched = k;
     if (k % kEvery == 0) {
@@ -449,15 +464,17 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
     Launch lv = make_launch();
     lv.p[0] = make_pass(0, 1, pK, pK, pK);
     lv.p[0].final_audit = 1; lv.p[0].depth = K; lv.p[0].verify_all = 1;
-    lv.nb0 = ctrl.items_f;
+    const int vv = pick(ctrl.items_f);
+    lv.nb0 = blocks_of(vv, 0, ctrl.items_f);
     int saveA = A;
-    ds_err r = run(lv, ctrl.items_f, true, K, 1);
+    ds_err r = run(lv, vv, lv.nb0, true, K, 1);
     if (r != DS_OK) return r;
     Launch lw = make_launch();
     lw.p[0] = make_pass(1, 1, pK, pK, pK);
     lw.p[0].final_audit = 1; lw.p[0].decide = 1; lw.p[0].depth = K; lw.p[0].verify_all = 1;
-    lw.nb0 = ctrl.items_g;
-    r = run(lw, ctrl.items_g, true, K, 1);
+    const int vw = pick(ctrl.items_g);
+    lw.nb0 = blocks_of(vw, 1, ctrl.items_g);
+    r = run(lw, vw, lw.nb0, true, K, 1);
     if (r != DS_OK) return r;
     A = saveA;
     HIP_TRY(hipStreamSynchronize(st));

@@ -31,13 +31,17 @@ namespace ds {
 
 constexpr int kPad = 128;        // point padding of every lane-indexed array
 constexpr int kColTile = 32;     // columns per MFMA tile
-constexpr int kColGroups = 4;    // waves per work item, each sweeping one column quarter
+constexpr int kGroups = 8;       // fixed column groups of a lane (whole tiles each)
 constexpr int kRowsMfma = 32;    // rows per work item, matrix-core kernel
 constexpr int kRowsValu = 64;    // rows per work item, vector-ALU kernel
 constexpr int kMaxW = 4096;
 constexpr int kMaxDSmall = 32;   // matrix-free kernels
 constexpr float kFastRange = 64.f;  // max spread of the bound (log2 units) for anchored sums
 constexpr int kMaxTimed = 4096;     // timed launches per solve (DS_F_TIMING)
+// launch-variant thresholds (work items of the launch, see launch_update)
+constexpr int kWideItems = 1536;
+constexpr int kMediumItemsMfma = 512;
+constexpr int kMediumItemsValu = 256;
 
 // Per physical slot lane descriptor; moved by compaction with the rest of the
 // lane-indexed state.
@@ -211,7 +215,13 @@ struct IngestArgs {
   Ctrl* ctrl;
 };
 
-hipError_t launch_update(const Launch& a, int d, bool use_mfma, int blocks, hipStream_t st);
+// Update kernel variants: how a launch spreads (row tile, column group) work
+// over waves. All variants compute identical bits; the host picks one by width.
+enum { VAR_NARROW = 0,   // 32-row items, one group per wave (8 waves)
+       VAR_MEDIUM = 1,   // 32-row items, two groups per wave (4 waves)
+       VAR_WIDE = 2 };   // 64-row items (uniform lane shapes only), two groups per wave
+hipError_t launch_update(const Launch& a, int d, bool use_mfma, int variant, int blocks,
+                         hipStream_t st);
 hipError_t launch_scan(const ScanArgs& a, hipStream_t st);
 hipError_t launch_offsets(SlotInfo* slot, int A, int rows, int* off_f, int* off_g, Ctrl* ctrl,
                           hipStream_t st);

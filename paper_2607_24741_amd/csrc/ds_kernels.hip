@@ -81,27 +81,38 @@ __device__ __forceinline__ int find_slot(const int* off, int A, int b) {
 }
 
 // ---------------------------------------------------------- wave reductions
-// Fixed butterfly over the 64 lanes: identical result in every lane, and the
-// order of operations never depends on data or timing.
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+// Fixed trees with the same bits in every lane: inside each row of 16 lanes by
+// DPP (neighbour pairs, quad pairs, mirrored halves of 8, mirrored halves of
+// 16), then across the rows through lane reads, in the order (r0, r1), (r2, r3).
+// Every step combines two lanes that already hold equal values on both sides
+// of a commutative operation, so no lane can end up with different bits.
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float rdlane(float v, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+struct OpAdd { __device__ float operator()(float a, float b) const { return a + b; } };
+struct OpMin { __device__ float operator()(float a, float b) const { return fminf(a, b); } };
+struct OpMax { __device__ float operator()(float a, float b) const { return fmaxf(a, b); } };
+template <class Op>
+__device__ __forceinline__ float row16(float v, Op op) {
+  v = op(v, dpp<0xB1>(v));   // lane ^ 1
+  v = op(v, dpp<0x4E>(v));   // lane ^ 2
+  v = op(v, dpp<0x141>(v));  // the other quad of the 8
+  v = op(v, dpp<0x140>(v));  // the other 8 of the row
   return v;
 }
-__device__ __forceinline__ float wave_min(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fminf(v, __shfl_xor(v, o, 64));
-  return v;
+// result of rows (2u, 2u+1), i.e. of lanes [32u, 32u + 32)
+template <class Op>
+__device__ __forceinline__ float half32(float v16, int u, Op op) {
+  return op(rdlane(v16, 32 * u), rdlane(v16, 32 * u + 16));
 }
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
-}
-__device__ __forceinline__ int wave_or(int v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v |= __shfl_xor(v, o, 64);
-  return v;
+template <class Op>
+__device__ __forceinline__ float wave64(float v, Op op) {
+  const float r = row16(v, op);
+  return op(half32(r, 0, op), half32(r, 1, op));
 }
 
 __device__ __forceinline__ void st_dev4(float4* p, float4 v) {
@@ -157,20 +168,19 @@ struct LaneAgg {
 __device__ __forceinline__ LaneAgg lane_aggregate(const float4* agg, int lane_id, int rbmax,
                                                   int nrb, bool coherent) {
   LaneAgg g;
-  float t0 = 0.f, t1 = INFINITY, t2 = -INFINITY;
-  int t3 = 0;
+  float t0 = 0.f, t1 = INFINITY, t2 = -INFINITY, t3 = 0.f;
   const float4* base = agg + (size_t)lane_id * rbmax;
   for (int q = (int)(threadIdx.x & 63); q < nrb; q += 64) {
     const float4 v = coherent ? ld_dev4(base + q) : base[q];
     t0 += v.x;
     t1 = fminf(t1, v.y);
     t2 = fmaxf(t2, v.z);
-    t3 |= (v.w != 0.f);
+    t3 = fmaxf(t3, v.w != 0.f ? 1.f : 0.f);
   }
-  g.sum = wave_sum(t0);
-  g.dmin = wave_min(t1);
-  g.dmax = wave_max(t2);
-  g.bad = wave_or(t3);
+  g.sum = wave64(t0, OpAdd());
+  g.dmin = wave64(t1, OpMin());
+  g.dmax = wave64(t2, OpMax());
+  g.bad = wave64(t3, OpMax()) != 0.f;
   return g;
 }
 
@@ -200,94 +210,94 @@ __device__ __forceinline__ bool check_facts(const Launch& L, const Pass& P, cons
   return true;
 }
 
-// -------------------------------------------------------- block epilogue
-// Finish of one work item after the column groups were merged. `owner`
-// threads hold one row each (merged (M, sum)). Writes the new lse / gam
-// (update), the row-block aggregate, and -- for the column check -- takes
-// the lane's retirement decision in the last arriving block of the lane.
-// Every thread of the block must call it.
-template <int NWAVES>
-__device__ void finish_block(const Launch& L, const Pass& P, int s, const SlotInfo& si, int rb,
-                             int i, bool owner, bool live, bool fast, float anchor, float lse_old,
-                             float lm, float w, float M, float sum, float rhat) {
-  __shared__ float sh_red[4][NWAVES];
-  __shared__ int sh_last;
+// ----------------------------------------------------------- item epilogue
+// Finish of one work item by wave 0 alone, after the column groups were merged.
+// Lane l owns row rb0 * UNIT + l when `owner` (merged (Mt, St) of that row).
+// Writes the new lse / gam (update kind), one aggregate per UNIT-row block
+// (NU of them), and -- for the deciding column check -- takes the lane's
+// retirement decision in the last arriving item of the lane.
+template <int UNIT, int NU>
+__device__ void finish_rows(const Launch& L, const Pass& P, int s, const SlotInfo& si, int rb0,
+                            bool owner, bool live, bool fast, float M, float lse_old, float lm,
+                            float w, float Mt, float St, float rhat) {
+  static_assert(UNIT * NU <= 64, "one wave owns the rows of an item");
+  const int lane = threadIdx.x & 63;
+  const int nrows = P.role ? si.m : si.n;
+  const int nrb = row_blocks(nrows, UNIT);
   const bool frozen = (L.mode == MODE_LOGICAL) && si.done;
-  float rho = 0.f, dmin = INFINITY, dmax = -INFINITY;
-  int bad = 0;
+  float rho = 0.f, dmin = INFINITY, dmax = -INFINITY, bad = 0.f;
+  float lse_new = INFINITY, gam_new = -INFINITY;
   if (owner) {
-    const size_t idx = (size_t)s * P.padr + i;
     if (P.kind == KIND_UPDATE) {
-      float lse_new, gam_new;
       if (live) {
-        lse_new = (fast ? anchor : 0.f) + (M + lg2(sum));
+        const float anchor = fast ? lse_old + M : 0.f;   // the sweep's row anchor
+        lse_new = anchor + (Mt + lg2(St));
         gam_new = lm - lse_new;
-        float dl = lse_new - lse_old;
-        if (isfinite(dl)) { dmin = dl; dmax = dl; } else { bad = 1; }
+        const float dl = lse_new - lse_old;
+        if (isfinite(dl)) { dmin = dl; dmax = dl; } else { bad = 1.f; }
         if (P.role == 0) {
           // R_i / a_i of the input state = 2^(lse_new - lse_old), formed so the
           // large terms cancel exactly before rounding
-          float ratio = fast ? sum * ex2(anchor - lse_old) : sum * ex2(M - lse_old);
+          const float ratio = fast ? St * ex2(anchor - lse_old) : St * ex2(Mt - lse_old);
           rho = w * fabsf(ratio - 1.f);
         }
-      } else {
-        lse_new = INFINITY;
-        gam_new = -INFINITY;
-      }
-      if (!frozen) {
-        P.lse_out[idx] = lse_new;
-        P.gam_out[idx] = gam_new;
       }
     } else if (live) {
-      // check: terms were pi_ij / 2^lm_i, so sum * 2^M = R_i / a_i
-      float ratio = sum * ex2(M);
+      // check: terms were pi_ij / 2^lm_i, so St * 2^Mt = R_i / a_i
+      const float ratio = St * ex2(Mt);
       rho = w * fabsf(ratio - 1.f);
     }
   }
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform (SGPR)
-  float r0 = wave_sum(rho), r1 = wave_min(dmin), r2 = wave_max(dmax);
-  int r3 = wave_or(bad);
-  if ((threadIdx.x & 63) == 0) {
-    sh_red[0][wave] = r0; sh_red[1][wave] = r1; sh_red[2][wave] = r2;
-    sh_red[3][wave] = (float)r3;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    float4 a = make_float4(0.f, INFINITY, -INFINITY, 0.f);
-    for (int w = 0; w < NWAVES; ++w) {
-      a.x += sh_red[0][w];
-      a.y = fminf(a.y, sh_red[1][w]);
-      a.z = fmaxf(a.z, sh_red[2][w]);
-      a.w = fmaxf(a.w, sh_red[3][w]);
-    }
-    float4* dst = P.agg_out + (size_t)si.lane * L.rbmax + rb;
-    if (P.kind == KIND_UPDATE) {
-      *dst = a;
-      sh_last = 0;
+  // one aggregate per UNIT-row block: {sum rho, min, max of the lse change, bad}
+  const float r0 = row16(rho, OpAdd()), r1 = row16(dmin, OpMin());
+  const float r2 = row16(dmax, OpMax()), r3 = row16(bad, OpMax());
+  float4 ag[NU];
+#pragma unroll
+  for (int u = 0; u < NU; ++u) {
+    if (UNIT == 32) {
+      ag[u] = make_float4(half32(r0, u, OpAdd()), half32(r1, u, OpMin()),
+                          half32(r2, u, OpMax()), half32(r3, u, OpMax()));
     } else {
-      if (P.role == 0 || !P.decide) {
-        *dst = a;
-        sh_last = 0;
-      } else {
-        st_dev4(dst, a);
-        wait_mem();
-        const int nrb = row_blocks(si.m, L.rows);
-        const int prev = atomicAdd(&L.vcnt[si.lane], 1);
-        sh_last = (prev == nrb - 1);
-        if (sh_last) atomicExch(&L.vcnt[si.lane], 0);
-      }
+      ag[u] = make_float4(OpAdd()(half32(r0, 0, OpAdd()), half32(r0, 1, OpAdd())),
+                          OpMin()(half32(r1, 0, OpMin()), half32(r1, 1, OpMin())),
+                          OpMax()(half32(r2, 0, OpMax()), half32(r2, 1, OpMax())),
+                          OpMax()(half32(r3, 0, OpMax()), half32(r3, 1, OpMax())));
     }
   }
-  __syncthreads();
-  if (!sh_last || threadIdx.x >= 64) return;
-  // last block of a checked lane: column residual and the decision
-  const LaneAgg gc = lane_aggregate(P.agg_out, si.lane, L.rbmax, row_blocks(si.m, L.rows), true);
+  const int nu = min(NU, nrb - rb0);
+  float4* dst = P.agg_out + (size_t)si.lane * L.rbmax + rb0;
+  const bool deciding = P.kind == KIND_VERIFY && P.role == 1 && P.decide;
+  if (!deciding) {
+    if (lane == 0)
+      for (int u = 0; u < nu; ++u) dst[u] = ag[u];
+    // the new state goes out last: nothing after it reuses its registers, so
+    // the wave ends without waiting for the stores
+    if (owner && P.kind == KIND_UPDATE && !frozen) {
+      const size_t idx = (size_t)s * P.padr + rb0 * UNIT + lane;
+      P.lse_out[idx] = lse_new;
+      P.gam_out[idx] = gam_new;
+    }
+    return;
+  }
+  // publish the column-check partials, then count this item's blocks in
+  int last = 0;
+  if (lane == 0) {
+    for (int u = 0; u < nu; ++u) st_dev4(dst + u, ag[u]);
+    wait_mem();
+    const int prev = atomicAdd(&L.vcnt[si.lane], nu);
+    last = (prev + nu == nrb);
+    if (last) atomicExch(&L.vcnt[si.lane], 0);
+  }
+  last = __builtin_amdgcn_readfirstlane(last);
+  if (!last) return;
+  // last item of a checked lane: column residual and the decision
+  const LaneAgg gc = lane_aggregate(P.agg_out, si.lane, L.rbmax, nrb, true);
   float rrow = rhat;
   if (P.final_audit) {
-    const LaneAgg gr = lane_aggregate(P.agg_rowchk, si.lane, L.rbmax, row_blocks(si.n, L.rows), false);
+    const LaneAgg gr = lane_aggregate(P.agg_rowchk, si.lane, L.rbmax, row_blocks(si.n, UNIT), false);
     rrow = gr.sum;
   }
-  if (threadIdx.x != 0) return;
+  if (lane != 0) return;
   // marginal evaluations spent on this lane's check (the final audit
   // evaluates both marginals)
   atomicAdd(&L.nchk[si.lane], P.final_audit ? 2 : 1);
@@ -329,24 +339,28 @@ __device__ __forceinline__ int xcd_item(int b, int N) {
   return x * q + min(x, r) + (b >> 3);
 }
 
-// Decide what block b of a pass does. Returns false when it has no work.
+// Decide what block b of a pass does: the slot s and the first row block rb0
+// of its item (RPI row blocks per item; RPI > 1 only for uniform lane shapes).
+// Returns false when the block has no work.
+template <int RPI>
 __device__ __forceinline__ bool locate_item(const Launch& L, const Pass& P, int b, int& s,
-                                            int& rb, SlotInfo& si) {
+                                            int& rb0, SlotInfo& si) {
   const Ctrl* c = L.ctrl;
   if (!P.final_audit && c->finished) return false;
   const int A = min(P.A, c->A);
   if (P.ipl > 0) {
-    const int N = P.ipl * A;
+    const int ipi = (P.ipl + RPI - 1) / RPI;   // items per lane
+    const int N = ipi * A;
     if (b >= N) return false;
     const int item = xcd_item(b, N);
-    s = item / P.ipl;
-    rb = item - s * P.ipl;
+    s = item / ipi;
+    rb0 = (item - s * ipi) * RPI;
   } else {
     const int N = P.off[A];
     if (b >= N) return false;
     const int item = xcd_item(b, N);
     s = find_slot(P.off, A, item);
-    rb = item - P.off[s];
+    rb0 = item - P.off[s];
   }
   si = L.slot[s];
   if (P.kind == KIND_UPDATE) return !(si.done && L.mode == MODE_ACTIVE);
@@ -356,23 +370,41 @@ __device__ __forceinline__ bool locate_item(const Launch& L, const Pass& P, int 
 }
 
 // --------------------------------------------------------- MFMA half-step
-// Work item = 32 rows of one lane against all its columns; wave w of the 4
-// sweeps column quarter w. In every 32x32 tile the matrix core forms
-// D[j][i] = sum_k A[j][k] B[k][i] over the augmented vectors
-// A_j = (y~_j, gam_j, 1), B_i = (x~_i, 1, -anchor_i) (K = 2*DH + 2): D is the
-// base-2 exponent of the (i, j) term minus the row anchor. Lane l holds row
-// i = l % 32 for 16 columns, so the streaming sum over j stays inside the
-// lane; half-waves and then the four column quarters are merged (LDS) in a
-// fixed order. The next tile's operands load while the current tile reduces.
-template <int DH>
-__global__ __launch_bounds__(256, (DH <= 7 ? 8 : (DH <= 12 ? 6 : 4))) void k_update_mfma(Launch L) {
-  __shared__ float2 sh_part[kColGroups][kRowsMfma];
+// The columns of a lane are cut into kGroups fixed groups of whole 32-column
+// tiles (tpg = ceil(tiles / kGroups) tiles each). Every group is swept in tile
+// order from its own start, per half-wave; the partials are then merged per row
+// in a fixed order (half-wave 0, half-wave 1, then groups 0..kGroups-1). How a
+// launch spreads (row tile, group) pairs over waves -- RT 32-row tiles and GW
+// consecutive groups per wave, kGroups / GW waves per block -- changes which
+// wave does the work, never the arithmetic, so a lane's bits do not depend on
+// the variant the host picks for the current width.
+//
+// In every 32x32 tile the matrix core forms D[j][i] = sum_k A[j][k] B[k][i] over
+// the augmented vectors A_j = (y~_j, gam_j, 1), B_i = (x~_i, 1, -anchor_i)
+// (K = 2*DH + 2): D is the base-2 exponent of the (i, j) term minus the row
+// anchor. Lane l holds row i = l % 32 for 16 columns, so the streaming sum over
+// j stays inside the lane. The next tile's operands load while the current
+// tile is reduced.
+template <int DH, int RT, int GW>
+constexpr int mfma_min_blocks() {
+  return (kGroups / GW) == 8 ? (DH <= 7 ? 4 : 2)
+                             : (RT == 1 ? (DH <= 7 ? 8 : (DH <= 12 ? 6 : 4))
+                                        : (DH <= 8 ? 4 : 2));
+}
+
+template <int DH, int RT, int GW>
+__global__ __launch_bounds__(64 * (kGroups / GW), (mfma_min_blocks<DH, RT, GW>()))
+void k_update_mfma(Launch L) {
+  constexpr int NW = kGroups / GW;
+  constexpr int ROWS = 32 * RT;
+  constexpr int DP = 2 * DH;
+  __shared__ float2 sh_part[kGroups][2][ROWS];
   const int b = blockIdx.x;
   const int pi = b >= L.nb0;
   const Pass P = pi ? L.p[1] : L.p[0];
-  int s, rb;
+  int s, rb0;
   SlotInfo si;
-  if (!locate_item(L, P, pi ? b - L.nb0 : b, s, rb, si)) return;
+  if (!locate_item<RT>(L, P, pi ? b - L.nb0 : b, s, rb0, si)) return;
   const bool upd = P.kind == KIND_UPDATE;
   float rhat = NAN;
   if (!upd && !check_facts(L, P, si, rhat)) return;
@@ -382,25 +414,32 @@ __global__ __launch_bounds__(256, (DH <= 7 ? 8 : (DH <= 12 ? 6 : 4))) void k_upd
   const int r = lane & 31;
   const int nrows = P.role ? si.m : si.n;
   const int ncols = P.role ? si.n : si.m;
-  const int i = rb * kRowsMfma + r;
-  constexpr int DP = 2 * DH;
 
   // Every load of the item (row data, first column tile) is issued before the
   // update facts are reduced, so their latencies overlap.
-  const size_t ridx = (size_t)s * P.padr + i;
-  const float lse_old = P.lse_in[ridx];
-  const float lm = P.lm_row[ridx];
-  const bool in_prefix = i < nrows;
-  const float w = in_prefix ? P.w_row[(size_t)si.lane * P.w_ld + i] : 0.f;
-  float bv[DH + 1];
-  const float* rrow = P.rec_row + ridx * DP + h * DH;
+  float lse_t[RT], bv[RT][DH + 1];
 #pragma unroll
-  for (int k = 0; k < DH; ++k) bv[k] = rrow[k];
+  for (int q = 0; q < RT; ++q) {
+    const size_t ridx = (size_t)s * P.padr + (rb0 + q) * 32 + r;
+    lse_t[q] = P.lse_in[ridx];
+    const float* rrow = P.rec_row + ridx * DP + h * DH;
+#pragma unroll
+    for (int k = 0; k < DH; ++k) bv[q][k] = rrow[k];
+  }
+  // wave 0 lane l owns row rb0 * 32 + l (tile l / 32, row l % 32)
+  const int orow = rb0 * 32 + lane;
+  const bool owner = wave == 0 && lane < ROWS && orow < nrows;
+  float own_lm = 0.f, own_w = 0.f;
+  if (owner) {
+    own_lm = P.lm_row[(size_t)s * P.padr + orow];
+    own_w = P.w_row[(size_t)si.lane * P.w_ld + orow];
+  }
 
   const int ct = (ncols + kColTile - 1) / kColTile;
-  const int tpg = (ct + kColGroups - 1) / kColGroups;
-  const int t0 = wave * tpg;
-  const int t1 = min(ct, t0 + tpg);
+  const int tpg = (ct + kGroups - 1) / kGroups;
+  const int g0 = wave * GW;
+  const int ta = min(ct, g0 * tpg);
+  const int tb = min(ct, (g0 + GW) * tpg);
   const float* ccol = P.rec_col + (size_t)s * P.padc * DP + h * DH + (size_t)r * DP;
   const float* gcol = P.gam_col + (size_t)s * P.padc + r;
   auto load = [&](int t, float* a) {
@@ -410,104 +449,138 @@ __global__ __launch_bounds__(256, (DH <= 7 ? 8 : (DH <= 12 ? 6 : 4))) void k_upd
     a[DH] = gcol[(size_t)t * kColTile];
   };
   float A0[DH + 1], A1[DH + 1];
-  if (t0 < t1) load(t0, A0);
+  if (ta < tb) load(ta, A0);
 
   bool fast = false;
   float M = 0.f;
   if (upd) update_facts(L, P, si, fast, M);
-  const bool live = in_prefix && (lse_old != INFINITY);
-  float anchor = 0.f, bias = 0.f;
-  if (live) {
-    if (!upd) bias = -lse_old;
-    else if (fast) { anchor = lse_old + M; bias = -anchor; }
+#pragma unroll
+  for (int q = 0; q < RT; ++q) {
+    const bool live_q = (rb0 + q) * 32 + r < nrows && lse_t[q] != INFINITY;
+    float bias = 0.f;
+    if (live_q) {
+      if (!upd) bias = -lse_t[q];
+      else if (fast) bias = -(lse_t[q] + M);
+    }
+    bv[q][DH] = h ? bias : 1.f;
   }
-  bv[DH] = h ? bias : 1.f;
 
-  float mrun = fast ? 0.f : -INFINITY, srun = 0.f;
+  float mrun[RT], srun[RT];
+  auto reset = [&]() {
+#pragma unroll
+    for (int q = 0; q < RT; ++q) { mrun[q] = fast ? 0.f : -INFINITY; srun[q] = 0.f; }
+  };
   auto tile = [&](const float* a, bool anchored) {
-    f32x16 acc = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    f32x16 acc[RT];
 #pragma unroll
-    for (int k = 0; k < DH; ++k) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[k], bv[k], acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(h ? 1.f : a[DH], bv[DH], acc, 0, 0, 0);
-    float e[16];
-    if (anchored) {
+    for (int q = 0; q < RT; ++q)
+      acc[q] = f32x16{0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int v = 0; v < 16; ++v) e[v] = ex2(acc[v]);
+    for (int k = 0; k < DH; ++k)
 #pragma unroll
-      for (int w = 8; w > 0; w >>= 1)
+      for (int q = 0; q < RT; ++q)
+        acc[q] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[k], bv[q][k], acc[q], 0, 0, 0);
 #pragma unroll
-        for (int v = 0; v < w; ++v) e[v] += e[v + w];
-      srun += e[0];
-    } else {
-      float tm = acc[0];
+    for (int q = 0; q < RT; ++q)
+      acc[q] = __builtin_amdgcn_mfma_f32_32x32x2f32(h ? 1.f : a[DH], bv[q][DH], acc[q], 0, 0, 0);
 #pragma unroll
-      for (int v = 1; v < 16; ++v) tm = fmaxf(tm, acc[v]);
-      const float mn = fmaxf(mrun, tm);
-      const float mref = (mn == -INFINITY) ? 0.f : mn;
+    for (int q = 0; q < RT; ++q) {
+      float e[16];
+      if (anchored) {
 #pragma unroll
-      for (int v = 0; v < 16; ++v) e[v] = ex2(acc[v] - mref);
+        for (int v = 0; v < 16; ++v) e[v] = ex2(acc[q][v]);
 #pragma unroll
-      for (int w = 8; w > 0; w >>= 1)
+        for (int w = 8; w > 0; w >>= 1)
 #pragma unroll
-        for (int v = 0; v < w; ++v) e[v] += e[v + w];
-      srun = srun * ex2(mrun - mref) + e[0];
-      mrun = mn;
+          for (int v = 0; v < w; ++v) e[v] += e[v + w];
+        srun[q] += e[0];
+      } else {
+        float tm = acc[q][0];
+#pragma unroll
+        for (int v = 1; v < 16; ++v) tm = fmaxf(tm, acc[q][v]);
+        const float mn = fmaxf(mrun[q], tm);
+        const float mref = (mn == -INFINITY) ? 0.f : mn;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) e[v] = ex2(acc[q][v] - mref);
+#pragma unroll
+        for (int w = 8; w > 0; w >>= 1)
+#pragma unroll
+          for (int v = 0; v < w; ++v) e[v] += e[v + w];
+        srun[q] = srun[q] * ex2(mrun[q] - mref) + e[0];
+        mrun[q] = mn;
+      }
     }
   };
-  // operand ping-pong: tile t+1 is in flight while tile t is reduced; the
-  // prefetch index is clamped so every load stays in range
+  // The wave's groups are consecutive tile ranges: the last prefetch of one
+  // group may already be the first tile of the next (`have`). No prefetch
+  // goes past the wave's last tile, so every load stays in bounds and none is
+  // left in flight when the sweep ends.
   auto sweep = [&](bool anchored) {
-    if (t0 >= t1) return;
-    int t = t0;
-    for (; t + 1 < t1; t += 2) {
-      load(t + 1, A1);
-      tile(A0, anchored);
-      load(min(t + 2, t1 - 1), A0);
-      tile(A1, anchored);
+    bool have = ta < tb;
+    int t = ta;
+#pragma unroll
+    for (int u = 0; u < GW; ++u) {
+      const int t1 = min(ct, (g0 + u + 1) * tpg);
+      reset();
+      if (t < t1) {
+        if (!have) load(t, A0);
+        for (; t + 1 < t1; t += 2) {
+          load(t + 1, A1);
+          tile(A0, anchored);
+          if (t + 2 < tb) load(t + 2, A0);   // no load past the wave's last tile
+          tile(A1, anchored);
+        }
+        if (t < t1) { tile(A0, anchored); ++t; have = false; }
+        else have = t < tb;
+      }
+#pragma unroll
+      for (int q = 0; q < RT; ++q) sh_part[g0 + u][h][32 * q + r] = make_float2(mrun[q], srun[q]);
     }
-    if (t < t1) tile(A0, anchored);
   };
   if (fast) sweep(true); else sweep(false);
-  // merge the two half-waves (same rows, different columns) in a canonical
-  // order so both halves hold identical bits
-  const float mo = __shfl_xor(mrun, 32, 64);
-  const float so_ = __shfl_xor(srun, 32, 64);
-  const float mA = h ? mo : mrun, sA = h ? so_ : srun;
-  const float mB = h ? mrun : mo, sB = h ? srun : so_;
-  const float Mw = fmaxf(mA, mB);              // -inf only if both halves are empty
-  const float mref = (Mw == -INFINITY) ? 0.f : Mw;
-  const float Sw = sA * ex2(mA - mref) + sB * ex2(mB - mref);
-  if (h == 0) sh_part[wave][r] = make_float2(Mw, Sw);
   __syncthreads();
-  // merge the column quarters in order (wave 0 owns the rows)
-  const bool owner = (wave == 0) && (h == 0);
+  if (wave != 0) return;
+  // merge per row: half-waves, then groups, in order
   float Mt = 0.f, St = 0.f;
   if (owner) {
+    float Mg[kGroups], Sg[kGroups];
     float mx = -INFINITY;
 #pragma unroll
-    for (int g = 0; g < kColGroups; ++g) mx = fmaxf(mx, sh_part[g][r].x);
+    for (int g = 0; g < kGroups; ++g) {
+      const float2 pa = sh_part[g][0][lane], pb = sh_part[g][1][lane];
+      const float mw = fmaxf(pa.x, pb.x);              // -inf only if both are empty
+      const float mref = (mw == -INFINITY) ? 0.f : mw;
+      Sg[g] = pa.y * ex2(pa.x - mref) + pb.y * ex2(pb.x - mref);
+      Mg[g] = mw;
+      mx = fmaxf(mx, mw);
+    }
     Mt = (mx == -INFINITY) ? 0.f : mx;
 #pragma unroll
-    for (int g = 0; g < kColGroups; ++g) St += sh_part[g][r].y * ex2(sh_part[g][r].x - Mt);
+    for (int g = 0; g < kGroups; ++g) St += Sg[g] * ex2(Mg[g] - Mt);
   }
-  finish_block<4>(L, P, s, si, rb, i, owner, live, fast, anchor, lse_old, lm, w, Mt, St, rhat);
+  // lane l < 32 RT owns tile l / 32 row l % 32, whose input lse it holds as lse_t[l / 32]
+  const float own_lse = (RT == 2 && h) ? lse_t[RT - 1] : lse_t[0];
+  const bool live = owner && own_lse != INFINITY;
+  finish_rows<32, RT>(L, P, s, si, rb0, owner, live, fast, M, own_lse, own_lm, own_w, Mt, St, rhat);
 }
 
 // --------------------------------------------------------- VALU half-step
-// Work item = 64 rows (one per lane) of one lane against all its columns;
-// wave w sweeps column quarter w. The column data of a tile is the same for
-// every lane (wave-uniform), so it is read through the scalar path and used
-// as SGPR operands: per (i, j) term one subtract, D fused multiply-adds, one
-// v_exp_f32 and one add. Column quarters are merged in LDS in a fixed order.
-template <int D, int DH>
-__global__ __launch_bounds__(256, 8) void k_update_valu(Launch L) {
-  __shared__ float2 sh_part[kColGroups][kRowsValu];
+// Work item = 64 rows (one per lane) of one lane against all its columns, with
+// the same fixed column groups as the matrix-core kernel; each wave sweeps GW
+// consecutive groups. The column data of a tile is the same for every lane
+// (wave-uniform), so it is read through the scalar path and used as SGPR
+// operands: per (i, j) term D fused multiply-adds, one v_exp_f32 and one add.
+// Groups are merged in LDS in a fixed order.
+template <int D, int DH, int GW>
+__global__ __launch_bounds__(64 * (kGroups / GW), (kGroups / GW == 8 ? 4 : 8))
+void k_update_valu(Launch L) {
+  __shared__ float2 sh_part[kGroups][kRowsValu];
   const int b = blockIdx.x;
   const int pi = b >= L.nb0;
   const Pass P = pi ? L.p[1] : L.p[0];
   int s, rb;
   SlotInfo si;
-  if (!locate_item(L, P, pi ? b - L.nb0 : b, s, rb, si)) return;
+  if (!locate_item<1>(L, P, pi ? b - L.nb0 : b, s, rb, si)) return;
   const bool upd = P.kind == KIND_UPDATE;
   float rhat = NAN;
   if (!upd && !check_facts(L, P, si, rhat)) return;
@@ -520,9 +593,13 @@ __global__ __launch_bounds__(256, 8) void k_update_valu(Launch L) {
   // row loads are issued before the update facts are reduced
   const size_t ridx = (size_t)s * P.padr + i;
   const float lse_old = P.lse_in[ridx];
-  const float lm = P.lm_row[ridx];
   const bool in_prefix = i < nrows;
-  const float w = in_prefix ? P.w_row[(size_t)si.lane * P.w_ld + i] : 0.f;
+  const bool owner = wave == 0 && in_prefix;
+  float lm = 0.f, w = 0.f;
+  if (owner) {
+    lm = P.lm_row[ridx];
+    w = P.w_row[(size_t)si.lane * P.w_ld + i];
+  }
   float xr[D];
   const float* rrow = P.rec_row + ridx * DP;
 #pragma unroll
@@ -531,71 +608,75 @@ __global__ __launch_bounds__(256, 8) void k_update_valu(Launch L) {
   float M = 0.f;
   if (upd) update_facts(L, P, si, fast, M);
   const bool live = in_prefix && (lse_old != INFINITY);
-  float anchor = 0.f, bias = 0.f;
+  float bias = 0.f;
   if (live) {
     if (!upd) bias = -lse_old;
-    else if (fast) { anchor = lse_old + M; bias = -anchor; }
+    else if (fast) bias = -(lse_old + M);
   }
 
   const int ct = (ncols + kColTile - 1) / kColTile;
-  const int tpg = (ct + kColGroups - 1) / kColGroups;
-  const int j0 = min(ct, wave * tpg) * kColTile;
-  const int j1 = min(ct, wave * tpg + tpg) * kColTile;
+  const int tpg = (ct + kGroups - 1) / kGroups;
   const float* __restrict__ ccol = P.rec_col + (size_t)s * P.padc * DP;
   const float* __restrict__ gcol = P.gam_col + (size_t)s * P.padc;
-
-  float mrun = -INFINITY, srun = 0.f;
-  if (fast) {
-    float sacc[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int j = j0; j < j1; j += 4) {
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const float* cj = ccol + (size_t)(j + u) * DP;
-        float z = gcol[j + u] + bias;
+  for (int u = 0; u < GW; ++u) {
+    const int g = wave * GW + u;
+    const int j0 = min(ct, g * tpg) * kColTile;
+    const int j1 = min(ct, g * tpg + tpg) * kColTile;
+    float mrun = -INFINITY, srun = 0.f;
+    if (fast) {
+      float sacc[4] = {0.f, 0.f, 0.f, 0.f};
+      for (int j = j0; j < j1; j += 4) {
 #pragma unroll
-        for (int k = 0; k < D; ++k) z = fmaf(xr[k], cj[k], z);
-        sacc[u] += ex2(z);
+        for (int v = 0; v < 4; ++v) {
+          const float* cj = ccol + (size_t)(j + v) * DP;
+          float z = gcol[j + v] + bias;
+#pragma unroll
+          for (int k = 0; k < D; ++k) z = fmaf(xr[k], cj[k], z);
+          sacc[v] += ex2(z);
+        }
+      }
+      srun = (sacc[0] + sacc[1]) + (sacc[2] + sacc[3]);
+      mrun = 0.f;
+    } else {
+      for (int j = j0; j < j1; j += 8) {
+        float z[8];
+#pragma unroll
+        for (int v = 0; v < 8; ++v) {
+          const float* cj = ccol + (size_t)(j + v) * DP;
+          float zz = gcol[j + v] + bias;
+#pragma unroll
+          for (int k = 0; k < D; ++k) zz = fmaf(xr[k], cj[k], zz);
+          z[v] = zz;
+        }
+        float tm = z[0];
+#pragma unroll
+        for (int v = 1; v < 8; ++v) tm = fmaxf(tm, z[v]);
+        const float mn = fmaxf(mrun, tm);
+        const float mref = (mn == -INFINITY) ? 0.f : mn;
+        float e[8];
+#pragma unroll
+        for (int v = 0; v < 8; ++v) e[v] = ex2(z[v] - mref);
+        const float ts = ((e[0] + e[1]) + (e[2] + e[3])) + ((e[4] + e[5]) + (e[6] + e[7]));
+        srun = srun * ex2(mrun - mref) + ts;
+        mrun = mn;
       }
     }
-    srun = (sacc[0] + sacc[1]) + (sacc[2] + sacc[3]);
-    mrun = 0.f;
-  } else {
-    for (int j = j0; j < j1; j += 8) {
-      float z[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const float* cj = ccol + (size_t)(j + u) * DP;
-        float zz = gcol[j + u] + bias;
-#pragma unroll
-        for (int k = 0; k < D; ++k) zz = fmaf(xr[k], cj[k], zz);
-        z[u] = zz;
-      }
-      float tm = z[0];
-#pragma unroll
-      for (int u = 1; u < 8; ++u) tm = fmaxf(tm, z[u]);
-      const float mn = fmaxf(mrun, tm);
-      const float mref = (mn == -INFINITY) ? 0.f : mn;
-      float e[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) e[u] = ex2(z[u] - mref);
-      const float ts = ((e[0] + e[1]) + (e[2] + e[3])) + ((e[4] + e[5]) + (e[6] + e[7]));
-      srun = srun * ex2(mrun - mref) + ts;
-      mrun = mn;
-    }
+    sh_part[g][lane] = make_float2(mrun, srun);   // (-inf, 0) for an empty group
   }
-  sh_part[wave][lane] = make_float2(mrun, srun);   // (-inf, 0) for an empty quarter
   __syncthreads();
-  const bool owner = (wave == 0);
+  if (wave != 0) return;
   float Mt = 0.f, St = 0.f;
   if (owner) {
     float mx = -INFINITY;
 #pragma unroll
-    for (int g = 0; g < kColGroups; ++g) mx = fmaxf(mx, sh_part[g][lane].x);
+    for (int g = 0; g < kGroups; ++g) mx = fmaxf(mx, sh_part[g][lane].x);
     Mt = (mx == -INFINITY) ? 0.f : mx;
 #pragma unroll
-    for (int g = 0; g < kColGroups; ++g) St += sh_part[g][lane].y * ex2(sh_part[g][lane].x - Mt);
+    for (int g = 0; g < kGroups; ++g) St += sh_part[g][lane].y * ex2(sh_part[g][lane].x - Mt);
   }
-  finish_block<4>(L, P, s, si, rb, i, owner, live, fast, anchor, lse_old, lm, w, Mt, St, rhat);
+  finish_rows<kRowsValu, 1>(L, P, s, si, rb, owner, live && owner, fast, M, lse_old, lm, w, Mt,
+                            St, rhat);
 }
 
 // ------------------------------------------------------------- block scan
@@ -935,13 +1016,20 @@ __global__ void k_ctrl_init(Ctrl* c, int W) {
 
 // ------------------------------------------------------- host-side launchers
 template <int DH>
-static hipError_t launch_mfma_dh(const Launch& a, int blocks, hipStream_t st) {
-  hipLaunchKernelGGL(k_update_mfma<DH>, dim3(blocks), dim3(256), 0, st, a);
+static hipError_t launch_mfma_dh(const Launch& a, int variant, int blocks, hipStream_t st) {
+  switch (variant) {
+    case VAR_NARROW: hipLaunchKernelGGL((k_update_mfma<DH, 1, 1>), dim3(blocks), dim3(512), 0, st, a); break;
+    case VAR_MEDIUM: hipLaunchKernelGGL((k_update_mfma<DH, 1, 2>), dim3(blocks), dim3(256), 0, st, a); break;
+    default: hipLaunchKernelGGL((k_update_mfma<DH, 2, 2>), dim3(blocks), dim3(256), 0, st, a); break;
+  }
   return hipGetLastError();
 }
 template <int D>
-static hipError_t launch_valu_d(const Launch& a, int blocks, hipStream_t st) {
-  hipLaunchKernelGGL((k_update_valu<D, (D + 1) / 2>), dim3(blocks), dim3(256), 0, st, a);
+static hipError_t launch_valu_d(const Launch& a, int variant, int blocks, hipStream_t st) {
+  if (variant == VAR_NARROW)
+    hipLaunchKernelGGL((k_update_valu<D, (D + 1) / 2, 1>), dim3(blocks), dim3(512), 0, st, a);
+  else
+    hipLaunchKernelGGL((k_update_valu<D, (D + 1) / 2, 2>), dim3(blocks), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
@@ -949,47 +1037,48 @@ static hipError_t launch_valu_d(const Launch& a, int blocks, hipStream_t st) {
 
 // Entry points used by the host runtime (C++ linkage, same library).
 namespace ds {
-hipError_t launch_update(const Launch& a, int d, bool use_mfma, int blocks, hipStream_t st) {
+hipError_t launch_update(const Launch& a, int d, bool use_mfma, int variant, int blocks,
+                         hipStream_t st) {
   if (blocks <= 0) return hipSuccess;
   const int dh = (d + 1) / 2;
   if (use_mfma) {
     switch (dh) {
-      case 1: return launch_mfma_dh<1>(a, blocks, st);
-      case 2: return launch_mfma_dh<2>(a, blocks, st);
-      case 3: return launch_mfma_dh<3>(a, blocks, st);
-      case 4: return launch_mfma_dh<4>(a, blocks, st);
-      case 5: return launch_mfma_dh<5>(a, blocks, st);
-      case 6: return launch_mfma_dh<6>(a, blocks, st);
-      case 7: return launch_mfma_dh<7>(a, blocks, st);
-      case 8: return launch_mfma_dh<8>(a, blocks, st);
-      case 9: return launch_mfma_dh<9>(a, blocks, st);
-      case 10: return launch_mfma_dh<10>(a, blocks, st);
-      case 11: return launch_mfma_dh<11>(a, blocks, st);
-      case 12: return launch_mfma_dh<12>(a, blocks, st);
-      case 13: return launch_mfma_dh<13>(a, blocks, st);
-      case 14: return launch_mfma_dh<14>(a, blocks, st);
-      case 15: return launch_mfma_dh<15>(a, blocks, st);
-      case 16: return launch_mfma_dh<16>(a, blocks, st);
+      case 1: return launch_mfma_dh<1>(a, variant, blocks, st);
+      case 2: return launch_mfma_dh<2>(a, variant, blocks, st);
+      case 3: return launch_mfma_dh<3>(a, variant, blocks, st);
+      case 4: return launch_mfma_dh<4>(a, variant, blocks, st);
+      case 5: return launch_mfma_dh<5>(a, variant, blocks, st);
+      case 6: return launch_mfma_dh<6>(a, variant, blocks, st);
+      case 7: return launch_mfma_dh<7>(a, variant, blocks, st);
+      case 8: return launch_mfma_dh<8>(a, variant, blocks, st);
+      case 9: return launch_mfma_dh<9>(a, variant, blocks, st);
+      case 10: return launch_mfma_dh<10>(a, variant, blocks, st);
+      case 11: return launch_mfma_dh<11>(a, variant, blocks, st);
+      case 12: return launch_mfma_dh<12>(a, variant, blocks, st);
+      case 13: return launch_mfma_dh<13>(a, variant, blocks, st);
+      case 14: return launch_mfma_dh<14>(a, variant, blocks, st);
+      case 15: return launch_mfma_dh<15>(a, variant, blocks, st);
+      case 16: return launch_mfma_dh<16>(a, variant, blocks, st);
       default: return hipErrorInvalidValue;
     }
   }
   switch (d) {
-    case 1: return launch_valu_d<1>(a, blocks, st);
-    case 2: return launch_valu_d<2>(a, blocks, st);
-    case 3: return launch_valu_d<3>(a, blocks, st);
-    case 4: return launch_valu_d<4>(a, blocks, st);
-    case 5: return launch_valu_d<5>(a, blocks, st);
-    case 6: return launch_valu_d<6>(a, blocks, st);
-    case 7: return launch_valu_d<7>(a, blocks, st);
-    case 8: return launch_valu_d<8>(a, blocks, st);
-    case 9: return launch_valu_d<9>(a, blocks, st);
-    case 10: return launch_valu_d<10>(a, blocks, st);
-    case 11: return launch_valu_d<11>(a, blocks, st);
-    case 12: return launch_valu_d<12>(a, blocks, st);
-    case 13: return launch_valu_d<13>(a, blocks, st);
-    case 14: return launch_valu_d<14>(a, blocks, st);
-    case 15: return launch_valu_d<15>(a, blocks, st);
-    case 16: return launch_valu_d<16>(a, blocks, st);
+    case 1: return launch_valu_d<1>(a, variant, blocks, st);
+    case 2: return launch_valu_d<2>(a, variant, blocks, st);
+    case 3: return launch_valu_d<3>(a, variant, blocks, st);
+    case 4: return launch_valu_d<4>(a, variant, blocks, st);
+    case 5: return launch_valu_d<5>(a, variant, blocks, st);
+    case 6: return launch_valu_d<6>(a, variant, blocks, st);
+    case 7: return launch_valu_d<7>(a, variant, blocks, st);
+    case 8: return launch_valu_d<8>(a, variant, blocks, st);
+    case 9: return launch_valu_d<9>(a, variant, blocks, st);
+    case 10: return launch_valu_d<10>(a, variant, blocks, st);
+    case 11: return launch_valu_d<11>(a, variant, blocks, st);
+    case 12: return launch_valu_d<12>(a, variant, blocks, st);
+    case 13: return launch_valu_d<13>(a, variant, blocks, st);
+    case 14: return launch_valu_d<14>(a, variant, blocks, st);
+    case 15: return launch_valu_d<15>(a, variant, blocks, st);
+    case 16: return launch_valu_d<16>(a, variant, blocks, st);
     default: return hipErrorInvalidValue;
   }
 }

@@ -148,6 +148,24 @@ def test_bitwise_lane_independence_and_determinism():
     assert solo["depth"][0] == g["depth"][3]
 
 
+@pytest.mark.parametrize("flags", [0, F_FORCE_VALU], ids=["mfma", "valu"])
+def test_launch_layouts_are_bitwise_identical(flags):
+    """The host picks the update kernel's work layout (row tiles and column
+    groups per wave) from each launch's width; a lane's bits must not depend
+    on it. Fixed work on full c2 lanes: the whole window (widest layout),
+    twenty lanes (middle layout) and four lanes (narrowest layout)."""
+    w = wl.make("c2")
+    log(f"[case] layouts flags={flags}: W=64 fixed work 12 cycles")
+    g = run_gpu(w, 1e-9, max_iter=12, flags=flags)
+    for lanes in (list(range(20)), [5, 17, 33, 60]):
+        log(f"[case] layouts flags={flags}: lanes {lanes[:4]}... ({len(lanes)})")
+        gs = run_gpu(wl.make("c2", lanes=lanes), 1e-9, max_iter=12, flags=flags)
+        for q, t in enumerate(lanes):
+            assert np.array_equal(gs["f"][q], g["f"][t]), (t, "f")
+            assert np.array_equal(gs["g"][q], g["g"][t]), (t, "g")
+            assert gs["residual"][q] == g["residual"][t], t
+
+
 def test_padding_isolation():
     log("[case] NaN vs zero padding")
     wn = wl.make("c5", W=6, n=300, m=300, hetero=(30, 300), pad_value=np.nan)
