@@ -64,6 +64,7 @@ ds::Layout plan(const ds_problem* pr, const ds_options* op, void* ws) {
   L.pad[0] = (int)align_up((size_t)pr->n_max, ds::kPad);
   L.pad[1] = (int)align_up((size_t)pr->m_max, ds::kPad);
   L.rows = uses_mfma(pr, op) ? ds::kRowsMfma : ds::kRowsValu;
+  L.es = (op->flags & DS_F_PRECISE) ? 2 : 1;
   L.rbmax = std::max(L.pad[0], L.pad[1]) / L.rows;
   const size_t W = (size_t)pr->W;
   Carver c{reinterpret_cast<char*>(ws)};
@@ -71,11 +72,11 @@ ds::Layout plan(const ds_problem* pr, const ds_options* op, void* ws) {
     ds::Bank& B = L.bank[b];
     for (int side = 0; side < 2; ++side) {
       const size_t np = W * (size_t)L.pad[side];
-      B.rec[side] = c.take<float>(np * L.dp);
-      B.lm[side] = c.take<float>(np);
+      B.rec[side] = c.take<float>(np * L.dp * L.es);
+      B.lm[side] = c.take<float>(np * L.es);
       for (int par = 0; par < 2; ++par) {
-        B.lse[side][par] = c.take<float>(np);
-        B.gam[side][par] = c.take<float>(np);
+        B.lse[side][par] = c.take<float>(np * L.es);
+        B.gam[side][par] = c.take<float>(np * L.es);
       }
     }
     B.slot = c.take<ds::SlotInfo>(W);
@@ -94,6 +95,7 @@ ds::Layout plan(const ds_problem* pr, const ds_options* op, void* ws) {
 }
 
 bool uses_mfma(const ds_problem* pr, const ds_options* op) {
+  if (op->flags & DS_F_PRECISE) return false;
   if (op->flags & DS_F_FORCE_MFMA) return true;
   if (op->flags & DS_F_FORCE_VALU) return false;
   return pr->d >= 8;
@@ -115,6 +117,10 @@ ds_err check_problem(const ds_problem* pr, const ds_options* op) {
     return fail(DS_E_INVALID, "DS_F_FORCE_VALU and DS_F_FORCE_MFMA are exclusive");
   if ((op->flags & DS_F_FORCE_VALU) && pr->d > 16)
     return fail(DS_E_UNSUPPORTED, "the vector-ALU kernels support d <= 16");
+  if ((op->flags & DS_F_PRECISE) && (op->flags & DS_F_FORCE_MFMA))
+    return fail(DS_E_INVALID, "DS_F_PRECISE runs on the vector ALU: DS_F_FORCE_MFMA is exclusive");
+  if ((op->flags & DS_F_PRECISE) && pr->d > 16)
+    return fail(DS_E_UNSUPPORTED, "the float64 state supports d <= 16");
   // sizes that keep every 32-bit index in range
   const double pts = (double)pr->W * (double)std::max(pr->n_max, pr->m_max);
   if (pts > 2.0e9) return fail(DS_E_UNSUPPORTED, "W * max(n_max, m_max) too large");
@@ -245,6 +251,7 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
   const bool active = (mode == DS_MODE_ACTIVE);
   const bool shadow = (op->flags & DS_F_SHADOW) != 0;
   const bool use_mfma = uses_mfma(pr, op);
+  const bool precise = (op->flags & DS_F_PRECISE) != 0;
   const int maxpad = std::max(L.pad[0], L.pad[1]);
 
   EventTimer tm;
@@ -263,6 +270,7 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
   ia.center = L.center;
   for (int k = 0; k < 4; ++k) ia.agg[k] = L.agg[k];
   ia.vcnt = L.vcnt; ia.nchk = L.nchk; ia.rbmax = L.rbmax;
+  ia.precise = precise ? 1 : 0;
   ia.ctrl = L.ctrl;
   HIP_TRY(launch_ingest(ia, maxpad, st));
   HIP_TRY(launch_offsets(L.bank[0].slot, W, L.rows, L.off[0], L.off[1], L.ctrl, st));
@@ -348,7 +356,8 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
   auto run = [&](Launch l, int variant, int blocks, bool sample, int cycle, int kind) -> ds_err {
     const bool timed = tm.on && sample && (int)timed_launches.size() < kMaxTimed;
     const int e0 = timed ? tm.rec() : -1;
-    HIP_TRY(launch_update(l, d, use_mfma, variant, blocks, st));
+    if (precise) HIP_TRY(launch_update_f64(l, d, variant, blocks, st));
+    else HIP_TRY(launch_update(l, d, use_mfma, variant, blocks, st));
     if (timed) {
       tm.spans[0].push_back({e0, tm.rec()});
       timed_launches.push_back({cycle, kind});
@@ -370,7 +379,7 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
   int launched = 0;
   int compactions = 0;
   int64_t bytes_compacted = 0;  // upper bound: survivors x per-lane state bytes
-  const int64_t lane_bytes = (int64_t)(L.pad[0] + L.pad[1]) * (L.dp + 5) * 4 +
+  const int64_t lane_bytes = (int64_t)(L.pad[0] + L.pad[1]) * (L.dp + 5) * 4 * L.es +
                              (int64_t)(sizeof(SlotInfo) + sizeof(Decision));
   for (int k = 1; k <= max_iter; ++k) {
     // bounded run-ahead: wait for the device only when too far behind
@@ -397,7 +406,7 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
       ma.src = L.bank[bank]; ma.dst = L.bank[bank ^ 1]; ma.ctrl = L.ctrl;
       ma.A = A; ma.dp = L.dp; ma.compact = 1; ma.emit_all = 0; ma.mode = mode;
       ma.pad[0] = L.pad[0]; ma.pad[1] = L.pad[1];
-      ma.n_max = pr->n_max; ma.m_max = pr->m_max; ma.chunk = 1024;
+      ma.n_max = pr->n_max; ma.m_max = pr->m_max; ma.chunk = 1024; ma.es = L.es;
       ma.f = res->f; ma.g = res->g; ma.depth = res->depth; ma.residual = res->residual;
       ma.row_res = res->row_residual; ma.col_res = res->col_residual; ma.status = res->status;
       HIP_TRY(launch_move(ma, A, maxpad, st));
@@ -488,7 +497,7 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
     ma.A = A; ma.dp = L.dp; ma.compact = 0; ma.emit_all = (mode == DS_MODE_STATIC); ma.mode = mode;
     ma.final_par = ctrl.final_cycle & 1;
     ma.pad[0] = L.pad[0]; ma.pad[1] = L.pad[1];
-    ma.n_max = pr->n_max; ma.m_max = pr->m_max; ma.chunk = 1024;
+    ma.n_max = pr->n_max; ma.m_max = pr->m_max; ma.chunk = 1024; ma.es = L.es;
     ma.f = res->f; ma.g = res->g; ma.depth = res->depth; ma.residual = res->residual;
     ma.row_res = res->row_residual; ma.col_res = res->col_residual; ma.status = res->status;
     HIP_TRY(launch_move(ma, A, maxpad, st));

@@ -37,6 +37,7 @@ constexpr int kRowsValu = 64;    // rows per work item, vector-ALU kernel
 constexpr int kMaxW = 4096;
 constexpr int kMaxDSmall = 32;   // matrix-free kernels
 constexpr float kFastRange = 64.f;  // max spread of the bound (log2 units) for anchored sums
+constexpr float kFastRangePrecise = 1.f;  // the same for the float64 state
 constexpr int kMaxTimed = 4096;     // timed launches per solve (DS_F_TIMING)
 // launch-variant thresholds (work items of the launch, see launch_update)
 constexpr int kWideItems = 1536;
@@ -51,11 +52,8 @@ struct SlotInfo {
   int done;        // retired (active, logical) -- its work items no longer run
   int passed;      // static mode: first passing audit seen (lane keeps updating)
   float kappa;     // log2(e) / eps
-  // spread of the latest change of lse on each side (for the anchored sums):
-  // valid flag, min and max of (lse_new - lse_old) over live points
-  int bx_ok, by_ok;
-  float bx_min, bx_max, by_min, by_max;
-  int pad;
+  double kappa64;  // the same in float64 (precise state)
+  int pad[2];
 };
 
 // Control block (device). Counters written by kernels, read by the host.
@@ -102,6 +100,9 @@ struct Decision {
 };
 
 // One bank of lane-indexed state (two banks ping-pong under compaction).
+// With the float64 (precise) state every array below holds doubles in the same
+// shape (the float pointers are reinterpreted) and records are not
+// de-interleaved.
 struct Bank {
   float* rec[2];     // side 0 (x), side 1 (y): [W][pad][dp] scaled, centred, de-interleaved
   float* lm[2];      // log2 masses [W][pad]; -inf for dead points
@@ -118,6 +119,7 @@ enum { AGG_F = 0, AGG_G = 1, AGG_ROW = 2, AGG_COL = 3 };
 
 struct Layout {
   int W, n_max, m_max, d, dp, dh;
+  int es;            // state element size in floats: 1 float32, 2 float64 (precise)
   int pad[2];        // npad, mpad
   int rbmax;         // max row blocks of either side
   int rows;          // rows per work item (kernel dependent)
@@ -192,6 +194,7 @@ struct MoveArgs {
   const Ctrl* ctrl;       // compaction: iterate the slots of the width before the map
   int A, dp, compact, emit_all, mode;
   int pad[2];
+  int es;                 // state element size in floats (1 or 2)
   int n_max, m_max;
   int final_par;          // parity of the final state (static mode emission)
   int chunk;              // points per block per side
@@ -206,6 +209,7 @@ struct IngestArgs {
   const int* n; const int* m;
   int W, n_max, m_max, d, dp, dh;
   int pad[2];
+  int precise;            // float64 state
   Bank bank;
   float* center;
   float4* agg[4];
@@ -222,6 +226,7 @@ enum { VAR_NARROW = 0,   // 32-row items, one group per wave (8 waves)
        VAR_WIDE = 2 };   // 64-row items (uniform lane shapes only), two groups per wave
 hipError_t launch_update(const Launch& a, int d, bool use_mfma, int variant, int blocks,
                          hipStream_t st);
+hipError_t launch_update_f64(const Launch& a, int d, int variant, int blocks, hipStream_t st);
 hipError_t launch_scan(const ScanArgs& a, hipStream_t st);
 hipError_t launch_offsets(SlotInfo* slot, int A, int rows, int* off_f, int* off_g, Ctrl* ctrl,
                           hipStream_t st);

@@ -191,10 +191,10 @@ __device__ __forceinline__ LaneAgg lane_aggregate(const float4* agg, int lane_id
 // the latest change of the column operand (= -(change of the column lse)), so
 // anchored (max-free) sums are safe when that spread is small; M = -min dgam.
 __device__ __forceinline__ void update_facts(const Launch& L, const Pass& P, const SlotInfo& si,
-                                             bool& fast, float& M) {
+                                             bool& fast, float& M, float range = kFastRange) {
   const int ncols = P.role ? si.n : si.m;
   const LaneAgg g = lane_aggregate(P.agg_bound, si.lane, L.rbmax, row_blocks(ncols, L.rows), false);
-  fast = !g.bad && g.dmin <= g.dmax && (g.dmax - g.dmin) <= kFastRange;
+  fast = !g.bad && g.dmin <= g.dmax && (g.dmax - g.dmin) <= range;
   M = -g.dmin;
 }
 // Check: whether this lane is checked at all (screen-positive, non-finite
@@ -216,36 +216,42 @@ __device__ __forceinline__ bool check_facts(const Launch& L, const Pass& P, cons
 // Writes the new lse / gam (update kind), one aggregate per UNIT-row block
 // (NU of them), and -- for the deciding column check -- takes the lane's
 // retirement decision in the last arriving item of the lane.
-template <int UNIT, int NU>
+__device__ __forceinline__ float log2_t(float x) { return lg2(x); }
+__device__ __forceinline__ double log2_t(double x) { return log2(x); }
+__device__ __forceinline__ float exp2_t(float x) { return ex2(x); }
+__device__ __forceinline__ double exp2_t(double x) { return exp2(x); }
+
+template <int UNIT, int NU, typename T>
 __device__ void finish_rows(const Launch& L, const Pass& P, int s, const SlotInfo& si, int rb0,
-                            bool owner, bool live, bool fast, float M, float lse_old, float lm,
-                            float w, float Mt, float St, float rhat) {
+                            bool owner, bool live, bool fast, float Mf, T lse_old, T lm,
+                            float w, T Mt, T St, float rhat) {
   static_assert(UNIT * NU <= 64, "one wave owns the rows of an item");
   const int lane = threadIdx.x & 63;
   const int nrows = P.role ? si.m : si.n;
   const int nrb = row_blocks(nrows, UNIT);
   const bool frozen = (L.mode == MODE_LOGICAL) && si.done;
+  const T M = (T)Mf;
   float rho = 0.f, dmin = INFINITY, dmax = -INFINITY, bad = 0.f;
-  float lse_new = INFINITY, gam_new = -INFINITY;
+  T lse_new = (T)INFINITY, gam_new = -(T)INFINITY;
   if (owner) {
     if (P.kind == KIND_UPDATE) {
       if (live) {
-        const float anchor = fast ? lse_old + M : 0.f;   // the sweep's row anchor
-        lse_new = anchor + (Mt + lg2(St));
+        const T anchor = fast ? lse_old + M : (T)0;   // the sweep's row anchor
+        lse_new = anchor + (Mt + log2_t(St));
         gam_new = lm - lse_new;
-        const float dl = lse_new - lse_old;
+        const float dl = (float)(lse_new - lse_old);
         if (isfinite(dl)) { dmin = dl; dmax = dl; } else { bad = 1.f; }
         if (P.role == 0) {
           // R_i / a_i of the input state = 2^(lse_new - lse_old), formed so the
           // large terms cancel exactly before rounding
-          const float ratio = fast ? St * ex2(anchor - lse_old) : St * ex2(Mt - lse_old);
-          rho = w * fabsf(ratio - 1.f);
+          const T ratio = fast ? St * exp2_t(anchor - lse_old) : St * exp2_t(Mt - lse_old);
+          rho = w * fabsf((float)(ratio - (T)1));
         }
       }
     } else if (live) {
       // check: terms were pi_ij / 2^lm_i, so St * 2^Mt = R_i / a_i
-      const float ratio = St * ex2(Mt);
-      rho = w * fabsf(ratio - 1.f);
+      const T ratio = St * exp2_t(Mt);
+      rho = w * fabsf((float)(ratio - (T)1));
     }
   }
   // one aggregate per UNIT-row block: {sum rho, min, max of the lse change, bad}
@@ -274,8 +280,8 @@ __device__ void finish_rows(const Launch& L, const Pass& P, int s, const SlotInf
     // the wave ends without waiting for the stores
     if (owner && P.kind == KIND_UPDATE && !frozen) {
       const size_t idx = (size_t)s * P.padr + rb0 * UNIT + lane;
-      P.lse_out[idx] = lse_new;
-      P.gam_out[idx] = gam_new;
+      reinterpret_cast<T*>(P.lse_out)[idx] = lse_new;
+      reinterpret_cast<T*>(P.gam_out)[idx] = gam_new;
     }
     return;
   }
@@ -561,7 +567,8 @@ void k_update_mfma(Launch L) {
   // lane l < 32 RT owns tile l / 32 row l % 32, whose input lse it holds as lse_t[l / 32]
   const float own_lse = (RT == 2 && h) ? lse_t[RT - 1] : lse_t[0];
   const bool live = owner && own_lse != INFINITY;
-  finish_rows<32, RT>(L, P, s, si, rb0, owner, live, fast, M, own_lse, own_lm, own_w, Mt, St, rhat);
+  finish_rows<32, RT, float>(L, P, s, si, rb0, owner, live, fast, M, own_lse, own_lm, own_w, Mt, St,
+                             rhat);
 }
 
 // --------------------------------------------------------- VALU half-step
@@ -675,8 +682,125 @@ void k_update_valu(Launch L) {
 #pragma unroll
     for (int g = 0; g < kGroups; ++g) St += sh_part[g][lane].y * ex2(sh_part[g][lane].x - Mt);
   }
-  finish_rows<kRowsValu, 1>(L, P, s, si, rb, owner, live && owner, fast, M, lse_old, lm, w, Mt,
-                            St, rhat);
+  finish_rows<kRowsValu, 1, float>(L, P, s, si, rb, owner, live && owner, fast, M, lse_old, lm, w,
+                                   Mt, St, rhat);
+}
+
+// ------------------------------------------------- float64 (precise) half-step
+// The vector-ALU half-step with the state (records, log masses, lse, gam) in
+// float64 and every exponent formed in float64; only the final, anchored
+// exponent (|z| small for the terms that matter) is rounded to float32 for
+// v_exp_f32, and the sums run in float64. Anchored sums are used only when
+// the bound's spread is at most kFastRangePrecise.
+template <int D, int GW>
+__global__ __launch_bounds__(64 * (kGroups / GW), (kGroups / GW == 8 ? 2 : 4))
+void k_update_f64(Launch L) {
+  __shared__ double2 sh_part[kGroups][kRowsValu];
+  const int b = blockIdx.x;
+  const int pi = b >= L.nb0;
+  const Pass P = pi ? L.p[1] : L.p[0];
+  int s, rb;
+  SlotInfo si;
+  if (!locate_item<1>(L, P, pi ? b - L.nb0 : b, s, rb, si)) return;
+  const bool upd = P.kind == KIND_UPDATE;
+  float rhat = NAN;
+  if (!upd && !check_facts(L, P, si, rhat)) return;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform (SGPR)
+  const int nrows = P.role ? si.m : si.n;
+  const int ncols = P.role ? si.n : si.m;
+  const int i = rb * kRowsValu + lane;
+  constexpr int DP = D + (D & 1);
+  const size_t ridx = (size_t)s * P.padr + i;
+  const double lse_old = reinterpret_cast<const double*>(P.lse_in)[ridx];
+  const bool in_prefix = i < nrows;
+  const bool owner = wave == 0 && in_prefix;
+  double lm = 0.0;
+  float w = 0.f;
+  if (owner) {
+    lm = reinterpret_cast<const double*>(P.lm_row)[ridx];
+    w = P.w_row[(size_t)si.lane * P.w_ld + i];
+  }
+  double xr[D];
+  const double* rrow = reinterpret_cast<const double*>(P.rec_row) + ridx * DP;
+#pragma unroll
+  for (int k = 0; k < D; ++k) xr[k] = rrow[k];
+  bool fast = false;
+  float M = 0.f;
+  if (upd) update_facts(L, P, si, fast, M, kFastRangePrecise);
+  const bool live = in_prefix && (lse_old != (double)INFINITY);
+  double bias = 0.0;
+  if (live) {
+    if (!upd) bias = -lse_old;
+    else if (fast) bias = -(lse_old + (double)M);
+  }
+
+  const int ct = (ncols + kColTile - 1) / kColTile;
+  const int tpg = (ct + kGroups - 1) / kGroups;
+  // Column data is the same for every lane. In float64 one column is up to
+  // 2 (d + 1) dwords, too many for scalar registers, so it is read through the
+  // vector path as a broadcast: the offset below is zero in every lane but is
+  // not provably uniform, which keeps the reads off the scalar path.
+  const int zero = (int)__builtin_amdgcn_mbcnt_lo(0u, 0u);
+  const double* __restrict__ ccol =
+      reinterpret_cast<const double*>(P.rec_col) + (size_t)s * P.padc * DP + zero;
+  const double* __restrict__ gcol =
+      reinterpret_cast<const double*>(P.gam_col) + (size_t)s * P.padc + zero;
+#pragma unroll
+  for (int u = 0; u < GW; ++u) {
+    const int g = wave * GW + u;
+    const int j0 = min(ct, g * tpg) * kColTile;
+    const int j1 = min(ct, g * tpg + tpg) * kColTile;
+    double mrun = -(double)INFINITY, srun = 0.0;
+    if (fast) {
+      double sacc[2] = {0.0, 0.0};
+      for (int j = j0; j < j1; j += 2) {
+#pragma unroll
+        for (int v = 0; v < 2; ++v) {
+          const double* cj = ccol + (size_t)(j + v) * DP;
+          double z = gcol[j + v] + bias;
+#pragma unroll
+          for (int k = 0; k < D; ++k) z = fma(xr[k], cj[k], z);
+          sacc[v] += (double)ex2((float)z);
+        }
+      }
+      srun = sacc[0] + sacc[1];
+      mrun = 0.0;
+    } else {
+      for (int j = j0; j < j1; j += 4) {
+        double z[4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const double* cj = ccol + (size_t)(j + v) * DP;
+          double zz = gcol[j + v] + bias;
+#pragma unroll
+          for (int k = 0; k < D; ++k) zz = fma(xr[k], cj[k], zz);
+          z[v] = zz;
+        }
+        const double tm = fmax(fmax(z[0], z[1]), fmax(z[2], z[3]));
+        const double mn = fmax(mrun, tm);
+        const double mref = (mn == -(double)INFINITY) ? 0.0 : mn;
+        const double ts = ((double)ex2((float)(z[0] - mref)) + (double)ex2((float)(z[1] - mref))) +
+                          ((double)ex2((float)(z[2] - mref)) + (double)ex2((float)(z[3] - mref)));
+        srun = srun * (double)ex2((float)(mrun - mref)) + ts;
+        mrun = mn;
+      }
+    }
+    sh_part[g][lane] = make_double2(mrun, srun);   // (-inf, 0) for an empty group
+  }
+  __syncthreads();
+  if (wave != 0) return;
+  double Mt = 0.0, St = 0.0;
+  if (owner) {
+    double mx = -(double)INFINITY;
+#pragma unroll
+    for (int g = 0; g < kGroups; ++g) mx = fmax(mx, sh_part[g][lane].x);
+    Mt = (mx == -(double)INFINITY) ? 0.0 : mx;
+#pragma unroll
+    for (int g = 0; g < kGroups; ++g) St += sh_part[g][lane].y * (double)ex2((float)(sh_part[g][lane].x - Mt));
+  }
+  finish_rows<kRowsValu, 1, double>(L, P, s, si, rb, owner, live && owner, fast, M, lse_old, lm, w,
+                                    Mt, St, rhat);
 }
 
 // ------------------------------------------------------------- block scan
@@ -807,23 +931,35 @@ __global__ __launch_bounds__(256) void k_move(MoveArgs p) {
   if (!emit && !copy) return;
   const int c0 = blockIdx.x * p.chunk;
   if (emit) {
+    // f_i = (gam_i + |x~_i|^2 / 2) / kappa, in the precision of the state
     const float inv_k = 1.f / si.kappa;
+    const double inv_k64 = 1.0 / si.kappa64;
     const int par = p.emit_all ? p.final_par : (d.depth & 1);
     for (int side = 0; side < 2; ++side) {
       const int lim = side ? p.m_max : p.n_max;
       const int cnt = side ? si.m : si.n;
       const int padn = p.pad[side];
       float* out = side ? p.g : p.f;
-      const float* gam = p.src.gam[side][par] + (size_t)s * padn;
-      const float* rec = p.src.rec[side] + (size_t)s * padn * p.dp;
       for (int q = c0 + threadIdx.x; q < min(lim, c0 + p.chunk); q += blockDim.x) {
         float v = 0.f;
         if (q < cnt) {
-          const float gq = gam[q];
-          if (gq != -INFINITY) {
-            float nrm = 0.f;
-            for (int k = 0; k < p.dp; ++k) { float x = rec[(size_t)q * p.dp + k]; nrm = fmaf(x, x, nrm); }
-            v = (gq + 0.5f * nrm) * inv_k;
+          const size_t e = (size_t)s * padn + q;
+          if (p.es == 2) {
+            const double gq = reinterpret_cast<const double*>(p.src.gam[side][par])[e];
+            if (gq != -(double)INFINITY) {
+              const double* rec = reinterpret_cast<const double*>(p.src.rec[side]) + e * p.dp;
+              double nrm = 0.0;
+              for (int k = 0; k < p.dp; ++k) nrm = fma(rec[k], rec[k], nrm);
+              v = (float)((gq + 0.5 * nrm) * inv_k64);
+            }
+          } else {
+            const float gq = p.src.gam[side][par][e];
+            if (gq != -INFINITY) {
+              const float* rec = p.src.rec[side] + e * p.dp;
+              float nrm = 0.f;
+              for (int k = 0; k < p.dp; ++k) nrm = fmaf(rec[k], rec[k], nrm);
+              v = (gq + 0.5f * nrm) * inv_k;
+            }
           }
         }
         out[(size_t)si.lane * lim + q] = v;
@@ -839,22 +975,24 @@ __global__ __launch_bounds__(256) void k_move(MoveArgs p) {
     }
   }
   if (copy) {
+    // every per-point array moves as raw floats (es of them per element)
     const int ns = d.new_slot;
+    const int es = p.es;
     for (int side = 0; side < 2; ++side) {
       const int padn = p.pad[side];
       const int lim = min(padn, c0 + p.chunk);
-      const size_t so = (size_t)s * padn, dn = (size_t)ns * padn;
-      for (int q = c0 + threadIdx.x; q < lim; q += blockDim.x) {
+      const size_t so = (size_t)s * padn * es, dn = (size_t)ns * padn * es;
+      for (int q = c0 * es + threadIdx.x; q < lim * es; q += blockDim.x) {
         p.dst.lm[side][dn + q] = p.src.lm[side][so + q];
         for (int par = 0; par < 2; ++par) {
           p.dst.lse[side][par][dn + q] = p.src.lse[side][par][so + q];
           p.dst.gam[side][par][dn + q] = p.src.gam[side][par][so + q];
         }
       }
-      // records: contiguous [pad][dp] floats per slot
+      // records: contiguous [pad][dp] elements per slot
       const float4* rs = reinterpret_cast<const float4*>(p.src.rec[side] + so * p.dp);
       float4* rd = reinterpret_cast<float4*>(p.dst.rec[side] + dn * p.dp);
-      const int q0 = c0 * p.dp / 4, q1 = lim * p.dp / 4;
+      const int q0 = c0 * p.dp * es / 4, q1 = lim * p.dp * es / 4;
       for (int q = q0 + threadIdx.x; q < q1; q += blockDim.x) rd[q] = rs[q];
     }
     if (blockIdx.x == 0 && threadIdx.x == 0) {
@@ -926,10 +1064,9 @@ __global__ __launch_bounds__(256) void k_ingest_lanes(IngestArgs p) {
   if (threadIdx.x == 0) {
     SlotInfo si;
     si.lane = t; si.n = nt; si.m = mt; si.done = 0; si.passed = 0;
-    si.kappa = (float)(1.4426950408889634 / (double)e);
-    si.bx_ok = 0; si.by_ok = 0;
-    si.bx_min = si.bx_max = si.by_min = si.by_max = 0.f;
-    si.pad = 0;
+    si.kappa64 = 1.4426950408889634 / (double)e;
+    si.kappa = (float)si.kappa64;
+    si.pad[0] = si.pad[1] = 0;
     p.bank.slot[t] = si;
     Decision d;
     d.status = 1; d.depth = 0; d.res_row = NAN; d.res_col = NAN; d.new_slot = -1;
@@ -949,7 +1086,7 @@ __global__ __launch_bounds__(256) void k_ingest_points(IngestArgs p, int chunk) 
   const int t = blockIdx.y;
   if (p.ctrl->err_lane != 0x7fffffff) return;
   const SlotInfo si = p.bank.slot[t];
-  const double sigma = sqrt(2.0 * (double)si.kappa);
+  const double sigma = sqrt(2.0 * si.kappa64);
   const float* c = p.center + (size_t)t * p.d;
   for (int side = 0; side < 2; ++side) {
     const int padn = p.pad[side];
@@ -960,9 +1097,38 @@ __global__ __launch_bounds__(256) void k_ingest_points(IngestArgs p, int chunk) 
     const int c0 = blockIdx.x * chunk;
     for (int q = c0 + threadIdx.x; q < min(padn, c0 + chunk); q += blockDim.x) {
       const size_t idx = (size_t)t * padn + q;
-      float* rec = p.bank.rec[side] + idx * p.dp;
       const float mass = (q < cnt) ? w[(size_t)t * ld + q] : 0.f;
       const bool live = (q < cnt) && (mass != 0.f);
+      const double lm = live ? log2((double)mass) : -(double)INFINITY;
+      if (p.precise) {
+        // float64 state: records in natural component order
+        double* rec = reinterpret_cast<double*>(p.bank.rec[side]) + idx * p.dp;
+        double nrm = 0.0;
+        for (int k = 0; k < p.dp; ++k) {
+          const double v = (live && k < p.d)
+                               ? sigma * ((double)P[((size_t)t * ld + q) * p.d + k] - (double)c[k])
+                               : 0.0;
+          rec[k] = v;
+          nrm = fma(v, v, nrm);
+        }
+        reinterpret_cast<double*>(p.bank.lm[side])[idx] = lm;
+        for (int par = 0; par < 2; ++par) {
+          double* lse = reinterpret_cast<double*>(p.bank.lse[side][par]);
+          double* gam = reinterpret_cast<double*>(p.bank.gam[side][par]);
+          if (!live) {
+            lse[idx] = (double)INFINITY;
+            gam[idx] = -(double)INFINITY;
+          } else if (side == 0) {
+            lse[idx] = (double)NAN;   // no f^0: the first f-half runs unanchored
+            gam[idx] = (double)NAN;
+          } else {
+            gam[idx] = -0.5 * nrm;    // cold start g^0 = 0
+            lse[idx] = lm + 0.5 * nrm;
+          }
+        }
+        continue;
+      }
+      float* rec = p.bank.rec[side] + idx * p.dp;
       float nrm = 0.f;
       if (live) {
         for (int k = 0; k < p.d; ++k) {
@@ -977,8 +1143,7 @@ __global__ __launch_bounds__(256) void k_ingest_points(IngestArgs p, int chunk) 
       } else {
         for (int k = 0; k < p.dp; ++k) rec[k] = 0.f;
       }
-      const float lm = live ? (float)log2((double)mass) : -INFINITY;
-      p.bank.lm[side][idx] = lm;
+      p.bank.lm[side][idx] = (float)lm;
       for (int par = 0; par < 2; ++par) {
         if (!live) {
           p.bank.lse[side][par][idx] = INFINITY;
@@ -991,7 +1156,7 @@ __global__ __launch_bounds__(256) void k_ingest_points(IngestArgs p, int chunk) 
           // cold start g^0 = 0  =>  gam^y = -kappa |y - c|^2 = -|y~|^2 / 2
           const float gam0 = -0.5f * nrm;
           p.bank.gam[1][par][idx] = gam0;
-          p.bank.lse[1][par][idx] = lm - gam0;
+          p.bank.lse[1][par][idx] = (float)lm - gam0;
         }
       }
     }
@@ -1030,6 +1195,15 @@ static hipError_t launch_valu_d(const Launch& a, int variant, int blocks, hipStr
     hipLaunchKernelGGL((k_update_valu<D, (D + 1) / 2, 1>), dim3(blocks), dim3(512), 0, st, a);
   else
     hipLaunchKernelGGL((k_update_valu<D, (D + 1) / 2, 2>), dim3(blocks), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+template <int D>
+static hipError_t launch_f64_d(const Launch& a, int variant, int blocks, hipStream_t st) {
+  if (variant == VAR_NARROW)
+    hipLaunchKernelGGL((k_update_f64<D, 1>), dim3(blocks), dim3(512), 0, st, a);
+  else
+    hipLaunchKernelGGL((k_update_f64<D, 2>), dim3(blocks), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
@@ -1079,6 +1253,29 @@ hipError_t launch_update(const Launch& a, int d, bool use_mfma, int variant, int
     case 14: return launch_valu_d<14>(a, variant, blocks, st);
     case 15: return launch_valu_d<15>(a, variant, blocks, st);
     case 16: return launch_valu_d<16>(a, variant, blocks, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_update_f64(const Launch& a, int d, int variant, int blocks, hipStream_t st) {
+  if (blocks <= 0) return hipSuccess;
+  switch (d) {
+    case 1: return launch_f64_d<1>(a, variant, blocks, st);
+    case 2: return launch_f64_d<2>(a, variant, blocks, st);
+    case 3: return launch_f64_d<3>(a, variant, blocks, st);
+    case 4: return launch_f64_d<4>(a, variant, blocks, st);
+    case 5: return launch_f64_d<5>(a, variant, blocks, st);
+    case 6: return launch_f64_d<6>(a, variant, blocks, st);
+    case 7: return launch_f64_d<7>(a, variant, blocks, st);
+    case 8: return launch_f64_d<8>(a, variant, blocks, st);
+    case 9: return launch_f64_d<9>(a, variant, blocks, st);
+    case 10: return launch_f64_d<10>(a, variant, blocks, st);
+    case 11: return launch_f64_d<11>(a, variant, blocks, st);
+    case 12: return launch_f64_d<12>(a, variant, blocks, st);
+    case 13: return launch_f64_d<13>(a, variant, blocks, st);
+    case 14: return launch_f64_d<14>(a, variant, blocks, st);
+    case 15: return launch_f64_d<15>(a, variant, blocks, st);
+    case 16: return launch_f64_d<16>(a, variant, blocks, st);
     default: return hipErrorInvalidValue;
   }
 }

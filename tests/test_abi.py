@@ -63,6 +63,19 @@ def test_workspace_query_and_validation():
     assert ds.load_library().ds_last_error_message().decode()
 
 
+def test_precise_state_validation_and_size():
+    """The float64 state runs on the vector-ALU kernels only (d <= 16) and
+    doubles the per-point state of the workspace."""
+    op = ds._options(1e-3, None, 100, 1, "active", 0)
+    opp = ds._options(1e-3, None, 100, 1, "active", ds.F_PRECISE)
+    code, n32 = _bytes(_problem(W=4, d=8), op)
+    code2, n64 = _bytes(_problem(W=4, d=8), opp)
+    assert code == 0 and code2 == 0 and n64 > 1.5 * n32
+    bad = ds._options(1e-3, None, 100, 1, "active", ds.F_PRECISE | ds.F_FORCE_MFMA)
+    assert _bytes(_problem(d=8), bad)[0] == 1
+    assert _bytes(_problem(d=17), opp)[0] == 4
+
+
 def test_solve_rejects_bad_arguments_before_device_work():
     lib = ds.load_library()
     op = ds._options(1e-3, None, 100, 1, "active", 0)
