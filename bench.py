@@ -38,7 +38,24 @@ def _cores():
         return os.cpu_count() or 1
 
 
-def cpu_baseline(w, tol, cycles=60, lanes=None):
+def measured_traffic():
+    """HBM bytes per update launch from the committed FETCH_SIZE / WRITE_SIZE
+    summary, or None once the kernel source has changed since it was taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "k_update_mfma_c2_traffic.md")
+    src = os.path.join(ROOT, "paper_2607_24741_amd", "csrc", "ds_kernels.hip")
+    try:
+        fields = dict(line.split(": ", 1) for line in open(path).read().splitlines()
+                      if line.startswith(("kernel_source_sha256: ", "traffic_bytes_per_launch: ")))
+        cur = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    except OSError:
+        return None
+    if fields.get("kernel_source_sha256") != cur:
+        return None
+    return float(fields["traffic_bytes_per_launch"])
+
+
+def cpu_baseline(w, tol, cycles=600, lanes=None):
     """Oracle as it stands (test infrastructure, float64, not tuned) on a
     bounded sample: the first `lanes` lanes of the window, each run for a fixed
     `cycles` cycles with the two-sided audit after every cycle (the same work
@@ -137,7 +154,7 @@ def main():
         "timed_update_launches_per_step": launches // args.steps,
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": MFMA_FP32_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / MFMA_FP32_PEAK_TFLOPS,
-                     "traffic": None,
+                     "traffic": measured_traffic(),
                      "kernel": "k_update_mfma (f- and g-half-steps)",
                      "avg_launch_us": 1e3 * ms_upd / max(1, launches),
                      "algorithmic": "2*d flops per valid (i,j) term evaluated by the timed launches",

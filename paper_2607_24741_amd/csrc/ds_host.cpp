@@ -174,15 +174,18 @@ struct EventTimer {
   std::vector<hipEvent_t>* pool = nullptr;
   size_t used = 0;
   std::vector<std::pair<int, int>> spans[3];  // update kernel, compaction, other
-  int rec() {
+  int take() {  // an event of the pool, not yet recorded
     if (used == pool->size()) {
       hipEvent_t e;
       if (hipEventCreate(&e) != hipSuccess) return -1;
       pool->push_back(e);
     }
-    hipEvent_t e = (*pool)[used];
-    if (hipEventRecord(e, st) != hipSuccess) return -1;
     return (int)used++;
+  }
+  int rec() {
+    const int i = take();
+    if (i < 0 || hipEventRecord((*pool)[i], st) != hipSuccess) return -1;
+    return i;
   }
   double total(int kind) {
     double ms = 0;
@@ -355,11 +358,14 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
   };
   auto run = [&](Launch l, int variant, int blocks, bool sample, int cycle, int kind) -> ds_err {
     const bool timed = tm.on && sample && (int)timed_launches.size() < kMaxTimed;
-    const int e0 = timed ? tm.rec() : -1;
-    if (precise) HIP_TRY(launch_update_f64(l, d, variant, blocks, st));
-    else HIP_TRY(launch_update(l, d, use_mfma, variant, blocks, st));
+    // the events are part of the kernel's own dispatch: they time the kernel,
+    // not the queue around it
+    const int e0 = timed ? tm.take() : -1, e1 = timed ? tm.take() : -1;
+    hipEvent_t h0 = e0 >= 0 ? (*tm.pool)[e0] : nullptr, h1 = e1 >= 0 ? (*tm.pool)[e1] : nullptr;
+    if (precise) HIP_TRY(launch_update_f64(l, d, variant, blocks, st, h0, h1));
+    else HIP_TRY(launch_update(l, d, use_mfma, variant, blocks, st, h0, h1));
     if (timed) {
-      tm.spans[0].push_back({e0, tm.rec()});
+      tm.spans[0].push_back({e0, e1});
       timed_launches.push_back({cycle, kind});
     }
     return DS_OK;

@@ -224,9 +224,11 @@ struct IngestArgs {
 enum { VAR_NARROW = 0,   // 32-row items, one group per wave (8 waves)
        VAR_MEDIUM = 1,   // 32-row items, two groups per wave (4 waves)
        VAR_WIDE = 2 };   // 64-row items (uniform lane shapes only), two groups per wave
+// e0 / e1 (may be null): events that record the kernel's own start and end
 hipError_t launch_update(const Launch& a, int d, bool use_mfma, int variant, int blocks,
-                         hipStream_t st);
-hipError_t launch_update_f64(const Launch& a, int d, int variant, int blocks, hipStream_t st);
+                         hipStream_t st, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
+hipError_t launch_update_f64(const Launch& a, int d, int variant, int blocks, hipStream_t st,
+                             hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 hipError_t launch_scan(const ScanArgs& a, hipStream_t st);
 hipError_t launch_offsets(SlotInfo* slot, int A, int rows, int* off_f, int* off_g, Ctrl* ctrl,
                           hipStream_t st);

@@ -17,6 +17,7 @@
 // Determinism: every reduction runs in a fixed order (no float atomics); the
 // split count and tile order of a lane depend only on its (n, m), so a lane's
 // bits do not depend on the batch width, its slot or its co-lanes.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -1181,29 +1182,32 @@ __global__ void k_ctrl_init(Ctrl* c, int W) {
 
 // ------------------------------------------------------- host-side launchers
 template <int DH>
-static hipError_t launch_mfma_dh(const Launch& a, int variant, int blocks, hipStream_t st) {
+static hipError_t launch_mfma_dh(const Launch& a, int variant, int blocks, hipStream_t st,
+                                 hipEvent_t e0, hipEvent_t e1) {
   switch (variant) {
-    case VAR_NARROW: hipLaunchKernelGGL((k_update_mfma<DH, 1, 1>), dim3(blocks), dim3(512), 0, st, a); break;
-    case VAR_MEDIUM: hipLaunchKernelGGL((k_update_mfma<DH, 1, 2>), dim3(blocks), dim3(256), 0, st, a); break;
-    default: hipLaunchKernelGGL((k_update_mfma<DH, 2, 2>), dim3(blocks), dim3(256), 0, st, a); break;
+    case VAR_NARROW: hipExtLaunchKernelGGL((k_update_mfma<DH, 1, 1>), dim3(blocks), dim3(512), 0, st, e0, e1, 0, a); break;
+    case VAR_MEDIUM: hipExtLaunchKernelGGL((k_update_mfma<DH, 1, 2>), dim3(blocks), dim3(256), 0, st, e0, e1, 0, a); break;
+    default: hipExtLaunchKernelGGL((k_update_mfma<DH, 2, 2>), dim3(blocks), dim3(256), 0, st, e0, e1, 0, a); break;
   }
   return hipGetLastError();
 }
 template <int D>
-static hipError_t launch_valu_d(const Launch& a, int variant, int blocks, hipStream_t st) {
+static hipError_t launch_valu_d(const Launch& a, int variant, int blocks, hipStream_t st,
+                                hipEvent_t e0, hipEvent_t e1) {
   if (variant == VAR_NARROW)
-    hipLaunchKernelGGL((k_update_valu<D, (D + 1) / 2, 1>), dim3(blocks), dim3(512), 0, st, a);
+    hipExtLaunchKernelGGL((k_update_valu<D, (D + 1) / 2, 1>), dim3(blocks), dim3(512), 0, st, e0, e1, 0, a);
   else
-    hipLaunchKernelGGL((k_update_valu<D, (D + 1) / 2, 2>), dim3(blocks), dim3(256), 0, st, a);
+    hipExtLaunchKernelGGL((k_update_valu<D, (D + 1) / 2, 2>), dim3(blocks), dim3(256), 0, st, e0, e1, 0, a);
   return hipGetLastError();
 }
 
 template <int D>
-static hipError_t launch_f64_d(const Launch& a, int variant, int blocks, hipStream_t st) {
+static hipError_t launch_f64_d(const Launch& a, int variant, int blocks, hipStream_t st,
+                               hipEvent_t e0, hipEvent_t e1) {
   if (variant == VAR_NARROW)
-    hipLaunchKernelGGL((k_update_f64<D, 1>), dim3(blocks), dim3(512), 0, st, a);
+    hipExtLaunchKernelGGL((k_update_f64<D, 1>), dim3(blocks), dim3(512), 0, st, e0, e1, 0, a);
   else
-    hipLaunchKernelGGL((k_update_f64<D, 2>), dim3(blocks), dim3(256), 0, st, a);
+    hipExtLaunchKernelGGL((k_update_f64<D, 2>), dim3(blocks), dim3(256), 0, st, e0, e1, 0, a);
   return hipGetLastError();
 }
 
@@ -1212,70 +1216,71 @@ static hipError_t launch_f64_d(const Launch& a, int variant, int blocks, hipStre
 // Entry points used by the host runtime (C++ linkage, same library).
 namespace ds {
 hipError_t launch_update(const Launch& a, int d, bool use_mfma, int variant, int blocks,
-                         hipStream_t st) {
+                         hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
   if (blocks <= 0) return hipSuccess;
   const int dh = (d + 1) / 2;
   if (use_mfma) {
     switch (dh) {
-      case 1: return launch_mfma_dh<1>(a, variant, blocks, st);
-      case 2: return launch_mfma_dh<2>(a, variant, blocks, st);
-      case 3: return launch_mfma_dh<3>(a, variant, blocks, st);
-      case 4: return launch_mfma_dh<4>(a, variant, blocks, st);
-      case 5: return launch_mfma_dh<5>(a, variant, blocks, st);
-      case 6: return launch_mfma_dh<6>(a, variant, blocks, st);
-      case 7: return launch_mfma_dh<7>(a, variant, blocks, st);
-      case 8: return launch_mfma_dh<8>(a, variant, blocks, st);
-      case 9: return launch_mfma_dh<9>(a, variant, blocks, st);
-      case 10: return launch_mfma_dh<10>(a, variant, blocks, st);
-      case 11: return launch_mfma_dh<11>(a, variant, blocks, st);
-      case 12: return launch_mfma_dh<12>(a, variant, blocks, st);
-      case 13: return launch_mfma_dh<13>(a, variant, blocks, st);
-      case 14: return launch_mfma_dh<14>(a, variant, blocks, st);
-      case 15: return launch_mfma_dh<15>(a, variant, blocks, st);
-      case 16: return launch_mfma_dh<16>(a, variant, blocks, st);
+      case 1: return launch_mfma_dh<1>(a, variant, blocks, st, e0, e1);
+      case 2: return launch_mfma_dh<2>(a, variant, blocks, st, e0, e1);
+      case 3: return launch_mfma_dh<3>(a, variant, blocks, st, e0, e1);
+      case 4: return launch_mfma_dh<4>(a, variant, blocks, st, e0, e1);
+      case 5: return launch_mfma_dh<5>(a, variant, blocks, st, e0, e1);
+      case 6: return launch_mfma_dh<6>(a, variant, blocks, st, e0, e1);
+      case 7: return launch_mfma_dh<7>(a, variant, blocks, st, e0, e1);
+      case 8: return launch_mfma_dh<8>(a, variant, blocks, st, e0, e1);
+      case 9: return launch_mfma_dh<9>(a, variant, blocks, st, e0, e1);
+      case 10: return launch_mfma_dh<10>(a, variant, blocks, st, e0, e1);
+      case 11: return launch_mfma_dh<11>(a, variant, blocks, st, e0, e1);
+      case 12: return launch_mfma_dh<12>(a, variant, blocks, st, e0, e1);
+      case 13: return launch_mfma_dh<13>(a, variant, blocks, st, e0, e1);
+      case 14: return launch_mfma_dh<14>(a, variant, blocks, st, e0, e1);
+      case 15: return launch_mfma_dh<15>(a, variant, blocks, st, e0, e1);
+      case 16: return launch_mfma_dh<16>(a, variant, blocks, st, e0, e1);
       default: return hipErrorInvalidValue;
     }
   }
   switch (d) {
-    case 1: return launch_valu_d<1>(a, variant, blocks, st);
-    case 2: return launch_valu_d<2>(a, variant, blocks, st);
-    case 3: return launch_valu_d<3>(a, variant, blocks, st);
-    case 4: return launch_valu_d<4>(a, variant, blocks, st);
-    case 5: return launch_valu_d<5>(a, variant, blocks, st);
-    case 6: return launch_valu_d<6>(a, variant, blocks, st);
-    case 7: return launch_valu_d<7>(a, variant, blocks, st);
-    case 8: return launch_valu_d<8>(a, variant, blocks, st);
-    case 9: return launch_valu_d<9>(a, variant, blocks, st);
-    case 10: return launch_valu_d<10>(a, variant, blocks, st);
-    case 11: return launch_valu_d<11>(a, variant, blocks, st);
-    case 12: return launch_valu_d<12>(a, variant, blocks, st);
-    case 13: return launch_valu_d<13>(a, variant, blocks, st);
-    case 14: return launch_valu_d<14>(a, variant, blocks, st);
-    case 15: return launch_valu_d<15>(a, variant, blocks, st);
-    case 16: return launch_valu_d<16>(a, variant, blocks, st);
+    case 1: return launch_valu_d<1>(a, variant, blocks, st, e0, e1);
+    case 2: return launch_valu_d<2>(a, variant, blocks, st, e0, e1);
+    case 3: return launch_valu_d<3>(a, variant, blocks, st, e0, e1);
+    case 4: return launch_valu_d<4>(a, variant, blocks, st, e0, e1);
+    case 5: return launch_valu_d<5>(a, variant, blocks, st, e0, e1);
+    case 6: return launch_valu_d<6>(a, variant, blocks, st, e0, e1);
+    case 7: return launch_valu_d<7>(a, variant, blocks, st, e0, e1);
+    case 8: return launch_valu_d<8>(a, variant, blocks, st, e0, e1);
+    case 9: return launch_valu_d<9>(a, variant, blocks, st, e0, e1);
+    case 10: return launch_valu_d<10>(a, variant, blocks, st, e0, e1);
+    case 11: return launch_valu_d<11>(a, variant, blocks, st, e0, e1);
+    case 12: return launch_valu_d<12>(a, variant, blocks, st, e0, e1);
+    case 13: return launch_valu_d<13>(a, variant, blocks, st, e0, e1);
+    case 14: return launch_valu_d<14>(a, variant, blocks, st, e0, e1);
+    case 15: return launch_valu_d<15>(a, variant, blocks, st, e0, e1);
+    case 16: return launch_valu_d<16>(a, variant, blocks, st, e0, e1);
     default: return hipErrorInvalidValue;
   }
 }
 
-hipError_t launch_update_f64(const Launch& a, int d, int variant, int blocks, hipStream_t st) {
+hipError_t launch_update_f64(const Launch& a, int d, int variant, int blocks, hipStream_t st,
+                             hipEvent_t e0, hipEvent_t e1) {
   if (blocks <= 0) return hipSuccess;
   switch (d) {
-    case 1: return launch_f64_d<1>(a, variant, blocks, st);
-    case 2: return launch_f64_d<2>(a, variant, blocks, st);
-    case 3: return launch_f64_d<3>(a, variant, blocks, st);
-    case 4: return launch_f64_d<4>(a, variant, blocks, st);
-    case 5: return launch_f64_d<5>(a, variant, blocks, st);
-    case 6: return launch_f64_d<6>(a, variant, blocks, st);
-    case 7: return launch_f64_d<7>(a, variant, blocks, st);
-    case 8: return launch_f64_d<8>(a, variant, blocks, st);
-    case 9: return launch_f64_d<9>(a, variant, blocks, st);
-    case 10: return launch_f64_d<10>(a, variant, blocks, st);
-    case 11: return launch_f64_d<11>(a, variant, blocks, st);
-    case 12: return launch_f64_d<12>(a, variant, blocks, st);
-    case 13: return launch_f64_d<13>(a, variant, blocks, st);
-    case 14: return launch_f64_d<14>(a, variant, blocks, st);
-    case 15: return launch_f64_d<15>(a, variant, blocks, st);
-    case 16: return launch_f64_d<16>(a, variant, blocks, st);
+    case 1: return launch_f64_d<1>(a, variant, blocks, st, e0, e1);
+    case 2: return launch_f64_d<2>(a, variant, blocks, st, e0, e1);
+    case 3: return launch_f64_d<3>(a, variant, blocks, st, e0, e1);
+    case 4: return launch_f64_d<4>(a, variant, blocks, st, e0, e1);
+    case 5: return launch_f64_d<5>(a, variant, blocks, st, e0, e1);
+    case 6: return launch_f64_d<6>(a, variant, blocks, st, e0, e1);
+    case 7: return launch_f64_d<7>(a, variant, blocks, st, e0, e1);
+    case 8: return launch_f64_d<8>(a, variant, blocks, st, e0, e1);
+    case 9: return launch_f64_d<9>(a, variant, blocks, st, e0, e1);
+    case 10: return launch_f64_d<10>(a, variant, blocks, st, e0, e1);
+    case 11: return launch_f64_d<11>(a, variant, blocks, st, e0, e1);
+    case 12: return launch_f64_d<12>(a, variant, blocks, st, e0, e1);
+    case 13: return launch_f64_d<13>(a, variant, blocks, st, e0, e1);
+    case 14: return launch_f64_d<14>(a, variant, blocks, st, e0, e1);
+    case 15: return launch_f64_d<15>(a, variant, blocks, st, e0, e1);
+    case 16: return launch_f64_d<16>(a, variant, blocks, st, e0, e1);
     default: return hipErrorInvalidValue;
   }
 }
