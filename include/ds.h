@@ -83,11 +83,14 @@ enum {
   DS_F_TIMING = 2u,     /* time every update launch with HIP events (ds_stats)  */
   DS_F_FORCE_VALU = 4u, /* use the vector-ALU update kernels for any d <= 32     */
   DS_F_FORCE_MFMA = 8u, /* use the matrix-core update kernels for any d <= 32    */
-  DS_F_PRECISE = 16u    /* float64 state and exponent arguments (vector-ALU
+  DS_F_PRECISE = 16u,   /* float64 state and exponent arguments (vector-ALU
                            kernels, d <= 16, exclusive with DS_F_FORCE_MFMA):
                            for small eps, where float32 rounding of exponents of
                            size C/eps reaches the tolerance bands; the outputs
                            stay float32                                         */
+  DS_F_MATERIALIZE = 32u /* build the cost C (base-2 units, float32) once per call
+                           in the workspace and stream it from HBM in every
+                           half-step; always on for d > 32 (n_max, m_max <= 8192) */
 };
 
 /* One window of W lanes. Device pointers. */

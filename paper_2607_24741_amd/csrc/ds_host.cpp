@@ -39,6 +39,9 @@ ds_err fail(ds_err e, const std::string& msg) {
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 bool uses_mfma(const ds_problem* pr, const ds_options* op);
+bool uses_mat(const ds_problem* pr, const ds_options* op) {
+  return pr->d > ds::kMaxDSmall || (op->flags & DS_F_MATERIALIZE) != 0;
+}
 
 struct Carver {
   char* base;
@@ -63,8 +66,10 @@ ds::Layout plan(const ds_problem* pr, const ds_options* op, void* ws) {
   L.dh = L.dp / 2;
   L.pad[0] = (int)align_up((size_t)pr->n_max, ds::kPad);
   L.pad[1] = (int)align_up((size_t)pr->m_max, ds::kPad);
-  L.rows = uses_mfma(pr, op) ? ds::kRowsMfma : ds::kRowsValu;
+  L.mat = uses_mat(pr, op) ? 1 : 0;
+  L.rows = (!L.mat && uses_mfma(pr, op)) ? ds::kRowsMfma : ds::kRowsValu;
   L.es = (op->flags & DS_F_PRECISE) ? 2 : 1;
+  if (L.mat) L.dp = 0;   // no point records: the cost is materialised
   L.rbmax = std::max(L.pad[0], L.pad[1]) / L.rows;
   const size_t W = (size_t)pr->W;
   Carver c{reinterpret_cast<char*>(ws)};
@@ -90,6 +95,7 @@ ds::Layout plan(const ds_problem* pr, const ds_options* op, void* ws) {
   L.off[0] = c.take<int>(W + 1);
   L.off[1] = c.take<int>(W + 1);
   L.ctrl = c.take<ds::Ctrl>(1);
+  L.Q = L.mat ? c.take<float>(W * (size_t)L.pad[0] * (size_t)L.pad[1]) : nullptr;
   L.bytes = align_up(c.off, 256);
   return L;
 }
@@ -107,8 +113,13 @@ ds_err check_problem(const ds_problem* pr, const ds_options* op) {
     return fail(DS_E_INVALID, "W, n_max, m_max and d must be >= 1");
   if (pr->W > ds::kMaxW) return fail(DS_E_UNSUPPORTED, "W above 4096 is not supported");
   if (pr->d > 512) return fail(DS_E_INVALID, "d must be <= 512");
-  if (pr->d > ds::kMaxDSmall)
-    return fail(DS_E_UNSUPPORTED, "d > 32 needs the large-dimension path, not built");
+  if (uses_mat(pr, op)) {
+    if (op->flags & (DS_F_PRECISE | DS_F_FORCE_VALU | DS_F_FORCE_MFMA))
+      return fail(DS_E_UNSUPPORTED, "the materialised cost (d > 32 or DS_F_MATERIALIZE) runs "
+                                    "in float32 with its own kernels: no PRECISE / FORCE flags");
+    if (pr->n_max > ds::kMatMaxPts || pr->m_max > ds::kMatMaxPts)
+      return fail(DS_E_UNSUPPORTED, "the materialised cost supports at most 8192 points per side");
+  }
   if (!(op->tol > 0.f) || !std::isfinite(op->tol)) return fail(DS_E_INVALID, "tol must be finite and > 0");
   if (op->max_iter < 1) return fail(DS_E_INVALID, "max_iter must be >= 1");
   if (op->audit_every < 1) return fail(DS_E_INVALID, "audit_every must be >= 1");
@@ -255,6 +266,7 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
   const bool shadow = (op->flags & DS_F_SHADOW) != 0;
   const bool use_mfma = uses_mfma(pr, op);
   const bool precise = (op->flags & DS_F_PRECISE) != 0;
+  const bool mat = L.mat != 0;
   const int maxpad = std::max(L.pad[0], L.pad[1]);
 
   EventTimer tm;
@@ -274,6 +286,7 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
   for (int k = 0; k < 4; ++k) ia.agg[k] = L.agg[k];
   ia.vcnt = L.vcnt; ia.nchk = L.nchk; ia.rbmax = L.rbmax;
   ia.precise = precise ? 1 : 0;
+  ia.mat = mat ? 1 : 0;
   ia.ctrl = L.ctrl;
   HIP_TRY(launch_ingest(ia, maxpad, st));
   HIP_TRY(launch_offsets(L.bank[0].slot, W, L.rows, L.off[0], L.off[1], L.ctrl, st));
@@ -287,6 +300,13 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
                      : ctrl.err_code == 2 ? "m out of range [1, m_max]"
                                           : "eps not finite and > 0";
     return fail(DS_E_INVALID, "lane " + std::to_string(ctrl.err_lane) + ": " + what);
+  }
+  if (mat) {
+    CostArgs ca;
+    ca.X = pr->X; ca.Y = pr->Y; ca.center = L.center; ca.slot = L.bank[0].slot; ca.Q = L.Q;
+    ca.W = W; ca.n_max = pr->n_max; ca.m_max = pr->m_max; ca.d = d;
+    ca.pad0 = L.pad[0]; ca.pad1 = L.pad[1];
+    HIP_TRY(launch_cost(ca, st));
   }
   // uniform lane shapes: work item -> slot is a division, no table lookup
   bool uniform = true;
@@ -334,6 +354,7 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
     l.slot = L.bank[bank].slot; l.dec = L.bank[bank].dec;
     l.audit = L.audit; l.vcnt = L.vcnt; l.ctrl = L.ctrl;
     l.hsnap = R->snap_dev; l.nchk = L.nchk;
+    l.Q = L.Q; l.q_lane = (size_t)L.pad[0] * L.pad[1]; l.q_ld = L.pad[1];
     return l;
   };
   // DS_F_TIMING: both launches of every kSampleEvery-th cycle (and the final
@@ -348,6 +369,7 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
   // per item (shorter sweeps); many items -> more rows per wave (fewer column
   // re-reads). Every variant computes the same bits.
   auto pick = [&](int items) -> int {
+    if (mat) return VAR_MEDIUM;   // one layout: 64-row items, one block each
     if (use_mfma && uniform && items >= kWideItems) return VAR_WIDE;
     return items >= (use_mfma ? kMediumItemsMfma : kMediumItemsValu) ? VAR_MEDIUM : VAR_NARROW;
   };
@@ -362,7 +384,8 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
     // not the queue around it
     const int e0 = timed ? tm.take() : -1, e1 = timed ? tm.take() : -1;
     hipEvent_t h0 = e0 >= 0 ? (*tm.pool)[e0] : nullptr, h1 = e1 >= 0 ? (*tm.pool)[e1] : nullptr;
-    if (precise) HIP_TRY(launch_update_f64(l, d, variant, blocks, st, h0, h1));
+    if (mat) HIP_TRY(launch_update_mat(l, blocks, st, h0, h1));
+    else if (precise) HIP_TRY(launch_update_f64(l, d, variant, blocks, st, h0, h1));
     else HIP_TRY(launch_update(l, d, use_mfma, variant, blocks, st, h0, h1));
     if (timed) {
       tm.spans[0].push_back({e0, e1});

@@ -36,6 +36,7 @@ constexpr int kRowsMfma = 32;    // rows per work item, matrix-core kernel
 constexpr int kRowsValu = 64;    // rows per work item, vector-ALU kernel
 constexpr int kMaxW = 4096;
 constexpr int kMaxDSmall = 32;   // matrix-free kernels
+constexpr int kMatMaxPts = 8192; // materialised cost: points per lane side (LDS staging)
 constexpr float kFastRange = 64.f;  // max spread of the bound (log2 units) for anchored sums
 constexpr float kFastRangePrecise = 1.f;  // the same for the float64 state
 constexpr int kMaxTimed = 4096;     // timed launches per solve (DS_F_TIMING)
@@ -120,6 +121,7 @@ enum { AGG_F = 0, AGG_G = 1, AGG_ROW = 2, AGG_COL = 3 };
 struct Layout {
   int W, n_max, m_max, d, dp, dh;
   int es;            // state element size in floats: 1 float32, 2 float64 (precise)
+  int mat;           // materialised cost (no point records; Q below)
   int pad[2];        // npad, mpad
   int rbmax;         // max row blocks of either side
   int rows;          // rows per work item (kernel dependent)
@@ -131,6 +133,7 @@ struct Layout {
   Audit* audit;      // [W]
   int* off[2];       // work item offsets per role [W + 1]
   Ctrl* ctrl;
+  float* Q;          // materialised cost [W][pad0][pad1] by caller lane, base-2 units
   size_t bytes;
 };
 
@@ -177,6 +180,9 @@ struct Launch {
   Ctrl* ctrl;
   HostSnap* hsnap;                // may be null
   int* nchk;                      // [W] check passes per caller lane
+  const float* Q;                 // materialised cost (caller lane l at Q + l * q_lane)
+  size_t q_lane;                  // floats per lane
+  int q_ld;                       // row stride of Q (padded target count)
 };
 
 struct ScanArgs {          // compaction map over the slots of the current bank
@@ -210,6 +216,7 @@ struct IngestArgs {
   int W, n_max, m_max, d, dp, dh;
   int pad[2];
   int precise;            // float64 state
+  int mat;                // materialised cost: no records, cold start gam^y = 0
   Bank bank;
   float* center;
   float4* agg[4];
@@ -229,6 +236,18 @@ hipError_t launch_update(const Launch& a, int d, bool use_mfma, int variant, int
                          hipStream_t st, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 hipError_t launch_update_f64(const Launch& a, int d, int variant, int blocks, hipStream_t st,
                              hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
+hipError_t launch_update_mat(const Launch& a, int blocks, hipStream_t st, hipEvent_t e0 = nullptr,
+                             hipEvent_t e1 = nullptr);
+
+// Q_ij = kappa_t ||x_i - y_j||^2 for every lane (one launch, before the first cycle)
+struct CostArgs {
+  const float* X; const float* Y;
+  const float* center;
+  const SlotInfo* slot;   // ingest layout: slot t = caller lane t
+  float* Q;
+  int W, n_max, m_max, d, pad0, pad1;
+};
+hipError_t launch_cost(const CostArgs& a, hipStream_t st);
 hipError_t launch_scan(const ScanArgs& a, hipStream_t st);
 hipError_t launch_offsets(SlotInfo* slot, int A, int rows, int* off_f, int* off_g, Ctrl* ctrl,
                           hipStream_t st);

@@ -804,6 +804,226 @@ void k_update_f64(Launch L) {
                                     Mt, St, rhat);
 }
 
+// ----------------------------------------------- materialised-cost half-steps
+// For large d (or on request) the cost of every lane is built once in base-2
+// units, Q_ij = kappa ||x_i - y_j||^2, and the half-steps stream it from HBM:
+//     lse_i = log2 sum_j 2^(gam_j - Q_ij)   (f-half: rows of Q)
+//     lse_j = log2 sum_i 2^(gam_i - Q_ij)   (g-half: columns of Q)
+// where gam = kappa * potential (no quadratic fold: no point records exist).
+// Q is indexed by caller lane and never moved by compaction. Both kernels use
+// 64-row work items, eight waves, and the column operand staged in LDS.
+
+// Build: one 32x32 tile per wave, x~.y~ on the matrix cores over the centred
+// coordinates, then kappa (|x|^2 + |y|^2 - 2 x.y) clamped at 0. The padded
+// region is written too (zero coordinates), so every entry a half-step can
+// touch is finite.
+__global__ __launch_bounds__(256) void k_cost(CostArgs c) {
+  const int t = blockIdx.y;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int h = lane >> 5, r = lane & 31;
+  const int tiles_j = c.pad1 / 32;
+  const int tile = blockIdx.x * 4 + wave;
+  if (tile >= (c.pad0 / 32) * tiles_j) return;
+  const int ti = tile / tiles_j, tj = tile - ti * tiles_j;
+  const SlotInfo si = c.slot[t];
+  const int i = ti * 32 + r, j = tj * 32 + r;
+  const bool vi = i < si.n, vj = j < si.m;
+  const float* xr = c.X + ((size_t)t * c.n_max + (vi ? i : 0)) * c.d;
+  const float* yr = c.Y + ((size_t)t * c.m_max + (vj ? j : 0)) * c.d;
+  const float* cc = c.center + (size_t)t * c.d;
+  f32x16 acc = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  float nx = 0.f, ny = 0.f;
+  // matrix core s of a K step of 8 pairs component k0+s (lanes 0-31) with
+  // k0+4+s (lanes 32-63) of the same row and column
+  for (int k0 = 0; k0 < c.d; k0 += 8) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int k = k0 + 4 * h + q;
+      const float a = (vi && k < c.d) ? xr[k] - cc[k] : 0.f;
+      const float b = (vj && k < c.d) ? yr[k] - cc[k] : 0.f;
+      nx = fmaf(a, a, nx);
+      ny = fmaf(b, b, ny);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, acc, 0, 0, 0);
+    }
+  }
+  nx += __shfl_xor(nx, 32, 64);
+  ny += __shfl_xor(ny, 32, 64);
+  const float kap = si.kappa;
+  float* Qt = c.Q + (size_t)t * c.pad0 * c.pad1;
+  // lane l holds D[m][l % 32] for m = 8 (v / 4) + 4 (l / 32) + v % 4
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int m = 8 * (v >> 2) + 4 * h + (v & 3);
+    const float nxm = __shfl(nx, m, 64);
+    const float q = kap * fmaxf(nxm + ny - 2.f * acc[v], 0.f);
+    Qt[(size_t)(ti * 32 + m) * c.pad1 + j] = q;
+  }
+}
+
+// f-half (and the final row check): wave w sweeps rows w, w+8, .. of the
+// item, its lanes striding over the columns four at a time.
+__global__ __launch_bounds__(512, 2) void k_mat_rows(Launch L) {
+  __shared__ __align__(16) float sh_gam[kMatMaxPts];
+  __shared__ float2 sh_row[kRowsValu];
+  const int b = blockIdx.x;
+  const int pi = b >= L.nb0;
+  const Pass P = pi ? L.p[1] : L.p[0];
+  int s, rb;
+  SlotInfo si;
+  if (!locate_item<1>(L, P, pi ? b - L.nb0 : b, s, rb, si)) return;
+  const bool upd = P.kind == KIND_UPDATE;
+  float rhat = NAN;
+  if (!upd && !check_facts(L, P, si, rhat)) return;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nrows = P.role ? si.m : si.n;
+  const int ncols = P.role ? si.n : si.m;
+  const int nc4 = (ncols + 3) & ~3;
+  // the column operand, padded to a multiple of 4 with dead columns
+  const float* gcol = P.gam_col + (size_t)s * P.padc;
+  for (int j = threadIdx.x; j < nc4; j += blockDim.x) sh_gam[j] = j < ncols ? gcol[j] : -INFINITY;
+  const int i_own = rb * kRowsValu + lane;
+  const bool owner = wave == 0 && i_own < nrows;
+  float lse_own = INFINITY, lm = 0.f, w = 0.f;
+  if (owner) {
+    const size_t idx = (size_t)s * P.padr + i_own;
+    lse_own = P.lse_in[idx];
+    lm = P.lm_row[idx];
+    w = P.w_row[(size_t)si.lane * P.w_ld + i_own];
+  }
+  bool fast = false;
+  float M = 0.f;
+  if (upd) update_facts(L, P, si, fast, M);
+  __syncthreads();
+  const float* Qt = L.Q + (size_t)si.lane * L.q_lane;
+  for (int rr = wave; rr < kRowsValu; rr += 8) {
+    const int i = rb * kRowsValu + rr;
+    float Mr = -INFINITY, Sr = 0.f;
+    if (i < nrows) {
+      const float lse_i = P.lse_in[(size_t)s * P.padr + i];
+      float bias = 0.f;
+      if (lse_i != INFINITY) {
+        if (!upd) bias = -lse_i;
+        else if (fast) bias = -(lse_i + M);
+      }
+      const float* q = Qt + (size_t)i * L.q_ld;
+      float mrun = fast ? 0.f : -INFINITY, srun = 0.f;
+      for (int j = 4 * lane; j < nc4; j += 256) {
+        const float4 qv = *reinterpret_cast<const float4*>(q + j);
+        const float4 gv = *reinterpret_cast<const float4*>(sh_gam + j);
+        const float z0 = (gv.x + bias) - qv.x, z1 = (gv.y + bias) - qv.y;
+        const float z2 = (gv.z + bias) - qv.z, z3 = (gv.w + bias) - qv.w;
+        if (fast) {
+          srun += (ex2(z0) + ex2(z1)) + (ex2(z2) + ex2(z3));
+        } else {
+          const float mn = fmaxf(mrun, fmaxf(fmaxf(z0, z1), fmaxf(z2, z3)));
+          const float mref = (mn == -INFINITY) ? 0.f : mn;
+          srun = srun * ex2(mrun - mref) +
+                 ((ex2(z0 - mref) + ex2(z1 - mref)) + (ex2(z2 - mref) + ex2(z3 - mref)));
+          mrun = mn;
+        }
+      }
+      // fixed-tree merge of the 64 lanes
+      if (fast) {
+        Mr = 0.f;
+        Sr = wave64(srun, OpAdd());
+      } else {
+        Mr = wave64(mrun, OpMax());
+        const float mref = (Mr == -INFINITY) ? 0.f : Mr;
+        Sr = wave64(srun * ex2(mrun - mref), OpAdd());
+      }
+    }
+    if (lane == 0) sh_row[rr] = make_float2(Mr, Sr);
+  }
+  __syncthreads();
+  if (wave != 0) return;
+  const float2 mt = sh_row[lane];
+  const float Mt = (mt.x == -INFINITY) ? 0.f : mt.x;
+  const float St = (mt.x == -INFINITY) ? 0.f : mt.y * ex2(mt.x - Mt);
+  finish_rows<kRowsValu, 1, float>(L, P, s, si, rb, owner, owner && lse_own != INFINITY, fast, M,
+                                   lse_own, lm, w, Mt, St, rhat);
+}
+
+// g-half (and the column check): lane l owns target point j = rb * 64 + l
+// (a column of Q); the eight waves split the source points into contiguous
+// chunks, merged per lane in chunk order.
+__global__ __launch_bounds__(512, 2) void k_mat_cols(Launch L) {
+  __shared__ float sh_gam[kMatMaxPts];
+  __shared__ float2 sh_part[8][kRowsValu];
+  const int b = blockIdx.x;
+  const int pi = b >= L.nb0;
+  const Pass P = pi ? L.p[1] : L.p[0];
+  int s, rb;
+  SlotInfo si;
+  if (!locate_item<1>(L, P, pi ? b - L.nb0 : b, s, rb, si)) return;
+  const bool upd = P.kind == KIND_UPDATE;
+  float rhat = NAN;
+  if (!upd && !check_facts(L, P, si, rhat)) return;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nrows = P.role ? si.m : si.n;   // target points (this kernel's rows)
+  const int ncols = P.role ? si.n : si.m;   // source points
+  const float* gcol = P.gam_col + (size_t)s * P.padc;
+  for (int i = threadIdx.x; i < ncols; i += blockDim.x) sh_gam[i] = gcol[i];
+  const int j = rb * kRowsValu + lane;
+  const bool in_prefix = j < nrows;
+  const size_t jdx = (size_t)s * P.padr + j;
+  const float lse_old = P.lse_in[jdx];
+  const bool owner = wave == 0 && in_prefix;
+  float lm = 0.f, w = 0.f;
+  if (owner) {
+    lm = P.lm_row[jdx];
+    w = P.w_row[(size_t)si.lane * P.w_ld + j];
+  }
+  bool fast = false;
+  float M = 0.f;
+  if (upd) update_facts(L, P, si, fast, M);
+  const bool live = in_prefix && lse_old != INFINITY;
+  float bias = 0.f;
+  if (live) {
+    if (!upd) bias = -lse_old;
+    else if (fast) bias = -(lse_old + M);
+  }
+  __syncthreads();
+  const int ch = (ncols + 7) / 8;
+  const int i0 = min(ncols, wave * ch), i1 = min(ncols, i0 + ch);
+  const float* q = L.Q + (size_t)si.lane * L.q_lane + j;
+  float mrun = fast ? 0.f : -INFINITY, srun = 0.f;
+  if (fast) {
+    float sa = 0.f, sb = 0.f;
+    int i = i0;
+    for (; i + 1 < i1; i += 2) {
+      const float q0 = q[(size_t)i * L.q_ld], q1 = q[(size_t)(i + 1) * L.q_ld];
+      sa += ex2((sh_gam[i] + bias) - q0);
+      sb += ex2((sh_gam[i + 1] + bias) - q1);
+    }
+    if (i < i1) sa += ex2((sh_gam[i] + bias) - q[(size_t)i * L.q_ld]);
+    srun = sa + sb;
+  } else {
+    for (int i = i0; i < i1; ++i) {
+      const float z = (sh_gam[i] + bias) - q[(size_t)i * L.q_ld];
+      const float mn = fmaxf(mrun, z);
+      const float mref = (mn == -INFINITY) ? 0.f : mn;
+      srun = srun * ex2(mrun - mref) + ex2(z - mref);
+      mrun = mn;
+    }
+  }
+  sh_part[wave][lane] = make_float2(mrun, srun);   // (-inf, 0) for an empty chunk
+  __syncthreads();
+  if (wave != 0) return;
+  float Mt = 0.f, St = 0.f;
+  if (owner) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int g = 0; g < 8; ++g) mx = fmaxf(mx, sh_part[g][lane].x);
+    Mt = (mx == -INFINITY) ? 0.f : mx;
+#pragma unroll
+    for (int g = 0; g < 8; ++g) St += sh_part[g][lane].y * ex2(sh_part[g][lane].x - Mt);
+  }
+  finish_rows<kRowsValu, 1, float>(L, P, s, si, rb, owner, owner && live, fast, M, lse_old, lm, w,
+                                   Mt, St, rhat);
+}
+
 // ------------------------------------------------------------- block scan
 __device__ __forceinline__ int block_exclusive_scan(int v, int* sh, int& total) {
   // wave inclusive scan by shuffles, then wave totals in slot order
@@ -1101,6 +1321,23 @@ __global__ __launch_bounds__(256) void k_ingest_points(IngestArgs p, int chunk) 
       const float mass = (q < cnt) ? w[(size_t)t * ld + q] : 0.f;
       const bool live = (q < cnt) && (mass != 0.f);
       const double lm = live ? log2((double)mass) : -(double)INFINITY;
+      if (p.mat) {
+        // no point records; gam = kappa * potential, cold start g^0 = 0
+        p.bank.lm[side][idx] = (float)lm;
+        for (int par = 0; par < 2; ++par) {
+          if (!live) {
+            p.bank.lse[side][par][idx] = INFINITY;
+            p.bank.gam[side][par][idx] = -INFINITY;
+          } else if (side == 0) {
+            p.bank.lse[0][par][idx] = NAN;
+            p.bank.gam[0][par][idx] = NAN;
+          } else {
+            p.bank.gam[1][par][idx] = 0.f;
+            p.bank.lse[1][par][idx] = (float)lm;
+          }
+        }
+        continue;
+      }
       if (p.precise) {
         // float64 state: records in natural component order
         double* rec = reinterpret_cast<double*>(p.bank.rec[side]) + idx * p.dp;
@@ -1283,6 +1520,21 @@ hipError_t launch_update_f64(const Launch& a, int d, int variant, int blocks, hi
     case 16: return launch_f64_d<16>(a, variant, blocks, st, e0, e1);
     default: return hipErrorInvalidValue;
   }
+}
+
+hipError_t launch_update_mat(const Launch& a, int blocks, hipStream_t st, hipEvent_t e0,
+                             hipEvent_t e1) {
+  if (blocks <= 0) return hipSuccess;
+  if (a.p[0].role == 0)
+    hipExtLaunchKernelGGL(k_mat_rows, dim3(blocks), dim3(512), 0, st, e0, e1, 0, a);
+  else
+    hipExtLaunchKernelGGL(k_mat_cols, dim3(blocks), dim3(512), 0, st, e0, e1, 0, a);
+  return hipGetLastError();
+}
+hipError_t launch_cost(const CostArgs& a, hipStream_t st) {
+  const int tiles = (a.pad0 / 32) * (a.pad1 / 32);
+  hipLaunchKernelGGL(k_cost, dim3((tiles + 3) / 4, a.W), dim3(256), 0, st, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_scan(const ScanArgs& a, hipStream_t st) {

@@ -76,6 +76,22 @@ def test_precise_state_validation_and_size():
     assert _bytes(_problem(d=17), opp)[0] == 4
 
 
+def test_materialised_cost_validation_and_size():
+    """d > 32 selects the materialised cost: the workspace holds W n_pad m_pad
+    floats of cost; the float64 state and forced kernels are refused for it,
+    and so are more than 8192 points per side."""
+    op = ds._options(1e-3, None, 100, 1, "active", 0)
+    code, n512 = _bytes(_problem(W=2, n_max=256, m_max=200, d=512), op)
+    assert code == 0 and n512 >= 2 * 256 * 256 * 4
+    opm = ds._options(1e-3, None, 100, 1, "active", ds.F_MATERIALIZE)
+    code, nm = _bytes(_problem(W=2, n_max=256, m_max=200, d=3), opm)
+    assert code == 0 and nm >= 2 * 256 * 256 * 4
+    for fl in (ds.F_PRECISE, ds.F_FORCE_VALU, ds.F_FORCE_MFMA):
+        o = ds._options(1e-3, None, 100, 1, "active", fl)
+        assert _bytes(_problem(d=64), o)[0] == 4
+    assert _bytes(_problem(n_max=9000, d=64), op)[0] == 4
+
+
 def test_solve_rejects_bad_arguments_before_device_work():
     lib = ds.load_library()
     op = ds._options(1e-3, None, 100, 1, "active", 0)

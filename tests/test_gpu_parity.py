@@ -13,7 +13,7 @@ from tests.gpu_support import compare, log, run_gpu, run_oracle
 
 pytestmark = pytest.mark.gpu
 
-F_SHADOW, F_FORCE_VALU, F_FORCE_MFMA, F_PRECISE = 1, 4, 8, 16
+F_SHADOW, F_FORCE_VALU, F_FORCE_MFMA, F_PRECISE, F_MATERIALIZE = 1, 4, 8, 16, 32
 
 
 def _case(name, w, tol, flags=0, **kw):
@@ -80,6 +80,54 @@ def test_telemetry_full_size_sampled():
             f"max_res_err={rep['max_res_err']:.2e} near_threshold={rep['near_threshold']}")
         if flags == F_PRECISE:
             assert rep["beyond_1e6"] == 0
+
+
+def test_features_large_d_reduced_ragged():
+    """d = 512 (ImageNet-feature-shaped): the materialised cost path, ragged
+    sizes in one window."""
+    w = wl.make("c4", W=4, n=256, m=240, hetero=(90, 256), pad_value=np.nan)
+    _case("c4-reduced", w, 1e-3)
+
+
+@pytest.mark.parametrize("name", ["c2", "c5"])
+def test_materialised_cost_small_d(name):
+    """The materialised cost on request at small d: parity on the mixture
+    window and on NaN-padded heterogeneous lanes."""
+    if name == "c2":
+        w, kw = wl.make("c2", W=6, n=200, m=176), {}
+    else:
+        w, kw = wl.make("c5", W=8, n=400, m=360, hetero=(40, 400), pad_value=np.nan), dict(max_iter=3000)
+    _case(f"{name}-materialised", w, 1e-2 if name == "c2" else 1e-3, flags=F_MATERIALIZE, **kw)
+
+
+def test_features_full_size_sampled():
+    """Full ImageNet-feature-shaped window (W=32, n=m=4096, d=512) in its
+    launch configuration: fixed work (3 cycles) of one lane against the
+    oracle, then a real solve at tol 1e-3 whose returned potentials the oracle
+    re-evaluates (float64 residual <= tol + 1e-5, equal to the reported one)."""
+    w = wl.make("c4")
+    log("[case] c4 full size fixed work 3 cycles")
+    g = run_gpu(w, 1e-9, max_iter=3)
+    t = 5
+    fw = oracle.solve_lane(w.X[t], w.Y[t], w.a[t], w.b[t], w.eps[t], 1e-9, fixed_iters=3)
+    scale = max(np.abs(fw["f"]).max(), np.abs(fw["g"]).max(), float(w.eps[t]))
+    err = max(np.abs(g["f"][t] - fw["f"]).max(), np.abs(g["g"][t] - fw["g"]).max()) / scale
+    log(f"  lane {t}: pot err {err:.2e}, res gpu {g['residual'][t]:.6e} or {fw['residual']:.6e}")
+    assert err <= 1e-4
+    assert abs(g["residual"][t] - fw["residual"]) <= 1e-5
+    log("[case] c4 full size tol 1e-3")
+    g = run_gpu(w, 1e-3)
+    st = g["stats"]
+    assert np.all(g["status"] == oracle.CONVERGED)
+    assert st.slots_update == int(g["depth"].sum())
+    assert list(g["order"]) == sorted(range(w.W), key=lambda q: (g["depth"][q], q))
+    C = oracle.sq_euclidean_cost(w.X[t], w.Y[t])
+    rr, rc = oracle.marginal_residuals(C, g["f"][t], g["g"][t], w.a[t].astype(np.float64),
+                                       w.b[t].astype(np.float64), float(w.eps[t]))
+    log(f"  lane {t}: depth {g['depth'][t]} f64 residual of gpu state {max(rr, rc):.6e} "
+        f"reported {g['residual'][t]:.6e}")
+    assert max(rr, rc) <= 1e-3 + 1e-5
+    assert abs(max(rr, rc) - g["residual"][t]) <= 1e-5
 
 
 @pytest.mark.parametrize("name", ["c1", "c5"])
@@ -190,7 +238,8 @@ def test_bitwise_lane_independence_and_determinism():
     assert solo["depth"][0] == g["depth"][3]
 
 
-@pytest.mark.parametrize("flags", [0, F_FORCE_VALU, F_PRECISE], ids=["mfma", "valu", "precise"])
+@pytest.mark.parametrize("flags", [0, F_FORCE_VALU, F_PRECISE, F_MATERIALIZE],
+                         ids=["mfma", "valu", "precise", "materialised"])
 def test_launch_layouts_are_bitwise_identical(flags):
     """The host picks the update kernel's work layout (row tiles and column
     groups per wave) from each launch's width; a lane's bits must not depend
