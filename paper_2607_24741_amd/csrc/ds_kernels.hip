@@ -696,7 +696,9 @@ void k_update_valu(Launch L) {
 template <int D, int GW>
 __global__ __launch_bounds__(64 * (kGroups / GW), (kGroups / GW == 8 ? 2 : 4))
 void k_update_f64(Launch L) {
+  constexpr int DPc = D + (D & 1);
   __shared__ double2 sh_part[kGroups][kRowsValu];
+  __shared__ __align__(16) double sh_tile[kGroups / GW][2][kColTile * DPc + kColTile];
   const int b = blockIdx.x;
   const int pi = b >= L.nb0;
   const Pass P = pi ? L.p[1] : L.p[0];
@@ -738,55 +740,95 @@ void k_update_f64(Launch L) {
 
   const int ct = (ncols + kColTile - 1) / kColTile;
   const int tpg = (ct + kGroups - 1) / kGroups;
-  // Column data is the same for every lane. In float64 one column is up to
-  // 2 (d + 1) dwords, too many for scalar registers, so it is read through the
-  // vector path as a broadcast: the offset below is zero in every lane but is
-  // not provably uniform, which keeps the reads off the scalar path.
-  const int zero = (int)__builtin_amdgcn_mbcnt_lo(0u, 0u);
-  const double* __restrict__ ccol =
-      reinterpret_cast<const double*>(P.rec_col) + (size_t)s * P.padc * DP + zero;
-  const double* __restrict__ gcol =
-      reinterpret_cast<const double*>(P.gam_col) + (size_t)s * P.padc + zero;
+  // Column data is the same for every lane, and in float64 one column is up
+  // to 2 (d + 1) dwords. Each wave stages its tiles in its own LDS double
+  // buffer (records, then gam) with coalesced loads and reads them back as
+  // broadcasts; only the wave itself touches its buffer, so no block barrier
+  // is needed (a wave's LDS operations complete in order).
+  constexpr int TREC = kColTile * DP;   // doubles of records per tile
+  constexpr int NV2 = TREC / 2;         // double2 per tile
+  constexpr int PER = (NV2 + 63) / 64;  // double2 per lane
+  double* buf0 = sh_tile[wave][0];
+  double* buf1 = sh_tile[wave][1];
+  const double* rec_lane = reinterpret_cast<const double*>(P.rec_col) + (size_t)s * P.padc * DP;
+  const double* gam_lane = reinterpret_cast<const double*>(P.gam_col) + (size_t)s * P.padc;
+  // lane l moves double2 number q * 64 + l of a tile (clamped: the last lanes
+  // of a partial round repeat an in-range element, harmlessly)
+  static_assert(PER <= 4, "a float64 tile is at most 4 double2 per lane");
+#define DS_F64_LD(q) ((q) < PER ? src_[min((q) * 64 + lane, NV2 - 1)] : make_double2(0.0, 0.0))
+#define DS_F64_FETCH(t)                                                                    \
+  do {                                                                                     \
+    const double2* src_ = reinterpret_cast<const double2*>(rec_lane + (size_t)(t) * TREC); \
+    pv0 = DS_F64_LD(0); pv1 = DS_F64_LD(1); pv2 = DS_F64_LD(2); pv3 = DS_F64_LD(3);        \
+    pg = gam_lane[(t) * kColTile + (lane & (kColTile - 1))];                               \
+  } while (0)
+#define DS_F64_ST(q, v) \
+  if ((q) < PER) reinterpret_cast<double2*>(dst_)[min((q) * 64 + lane, NV2 - 1)] = (v)
+#define DS_F64_STASH(dst)                                                                  \
+  do {                                                                                     \
+    double* dst_ = (dst);                                                                  \
+    DS_F64_ST(0, pv0); DS_F64_ST(1, pv1); DS_F64_ST(2, pv2); DS_F64_ST(3, pv3);             \
+    if (lane < kColTile) dst_[TREC + lane] = pg;                                           \
+    __builtin_amdgcn_wave_barrier();                                                       \
+  } while (0)
 #pragma unroll
   for (int u = 0; u < GW; ++u) {
     const int g = wave * GW + u;
-    const int j0 = min(ct, g * tpg) * kColTile;
-    const int j1 = min(ct, g * tpg + tpg) * kColTile;
-    double mrun = -(double)INFINITY, srun = 0.0;
-    if (fast) {
-      double sacc[2] = {0.0, 0.0};
-      for (int j = j0; j < j1; j += 2) {
-#pragma unroll
-        for (int v = 0; v < 2; ++v) {
-          const double* cj = ccol + (size_t)(j + v) * DP;
-          double z = gcol[j + v] + bias;
-#pragma unroll
-          for (int k = 0; k < D; ++k) z = fma(xr[k], cj[k], z);
-          sacc[v] += (double)ex2((float)z);
-        }
-      }
-      srun = sacc[0] + sacc[1];
-      mrun = 0.0;
-    } else {
-      for (int j = j0; j < j1; j += 4) {
-        double z[4];
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const double* cj = ccol + (size_t)(j + v) * DP;
-          double zz = gcol[j + v] + bias;
-#pragma unroll
-          for (int k = 0; k < D; ++k) zz = fma(xr[k], cj[k], zz);
-          z[v] = zz;
-        }
-        const double tm = fmax(fmax(z[0], z[1]), fmax(z[2], z[3]));
-        const double mn = fmax(mrun, tm);
-        const double mref = (mn == -(double)INFINITY) ? 0.0 : mn;
-        const double ts = ((double)ex2((float)(z[0] - mref)) + (double)ex2((float)(z[1] - mref))) +
-                          ((double)ex2((float)(z[2] - mref)) + (double)ex2((float)(z[3] - mref)));
-        srun = srun * (double)ex2((float)(mrun - mref)) + ts;
-        mrun = mn;
-      }
+    const int tA = min(ct, g * tpg), tB = min(ct, g * tpg + tpg);
+    double mrun = fast ? 0.0 : -(double)INFINITY, srun = 0.0;
+    double sacc[2] = {0.0, 0.0};
+    if (tA < tB) {
+      double2 pv0, pv1, pv2, pv3;
+      double pg;
+      DS_F64_FETCH(tA);
+      DS_F64_STASH(buf0);
     }
+    for (int t = tA; t < tB; ++t) {
+      const double* cur = ((t - tA) & 1) ? buf1 : buf0;
+      double* nxt = ((t - tA) & 1) ? buf0 : buf1;
+      double2 pv0, pv1, pv2, pv3;
+      double pg = 0.0;
+      const bool more = t + 1 < tB;
+      if (more) DS_F64_FETCH(t + 1);
+      if (fast) {
+        for (int c = 0; c < kColTile; c += 2) {
+#pragma unroll
+          for (int v = 0; v < 2; ++v) {
+            const double* cj = cur + (c + v) * DP;
+            double z = cur[TREC + c + v] + bias;
+#pragma unroll
+            for (int k = 0; k < D; ++k) z = fma(xr[k], cj[k], z);
+            sacc[v] += (double)ex2((float)z);
+          }
+        }
+      } else {
+        for (int c = 0; c < kColTile; c += 4) {
+          double z[4];
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const double* cj = cur + (c + v) * DP;
+            double zz = cur[TREC + c + v] + bias;
+#pragma unroll
+            for (int k = 0; k < D; ++k) zz = fma(xr[k], cj[k], zz);
+            z[v] = zz;
+          }
+          const double tm = fmax(fmax(z[0], z[1]), fmax(z[2], z[3]));
+          const double mn = fmax(mrun, tm);
+          const double mref = (mn == -(double)INFINITY) ? 0.0 : mn;
+          const double ts = ((double)ex2((float)(z[0] - mref)) + (double)ex2((float)(z[1] - mref))) +
+                            ((double)ex2((float)(z[2] - mref)) + (double)ex2((float)(z[3] - mref)));
+          srun = srun * (double)ex2((float)(mrun - mref)) + ts;
+          mrun = mn;
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+      if (more) DS_F64_STASH(nxt);
+    }
+#undef DS_F64_FETCH
+#undef DS_F64_STASH
+#undef DS_F64_LD
+#undef DS_F64_ST
+    if (fast) srun = sacc[0] + sacc[1];
     sh_part[g][lane] = make_double2(mrun, srun);   // (-inf, 0) for an empty group
   }
   __syncthreads();
