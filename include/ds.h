@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define DS_API_VERSION 1
+#define DS_API_VERSION 2
 
 typedef enum {
   DS_OK = 0,
@@ -117,7 +117,18 @@ typedef struct {
   int32_t audit_every; /* audit grid spacing in cycles, >= 1                      */
   int32_t mode;        /* ds_mode                                                 */
   uint32_t flags;      /* DS_F_*                                                  */
+  int32_t streams;     /* concurrent sub-batches, 0..4; 0 => automatic (see below) */
 } ds_options;
+/* Sub-batches (active mode only). The window is cut into `streams` contiguous
+ * lane ranges, each solved with its own control loop, workspace part and HIP
+ * stream (the first on the caller's stream, the others on streams of the
+ * library that start behind the work already queued on the caller's stream
+ * and that the caller's stream waits for before the call returns). Lanes are
+ * independent, so every output is bit-identical to the one-batch solve; the
+ * launch latencies of one sub-batch overlap the work of the others. Automatic:
+ * one sub-batch below 32 lanes, in the static and logical modes (they share
+ * one final cycle across the window) and with the materialised cost; two
+ * from 32 lanes; three from 48. ds_workspace_bytes accounts for the split. */
 
 /* Outputs, in caller lane order. Device pointers. */
 typedef struct {
@@ -148,9 +159,10 @@ typedef struct {
   int32_t missed_ready;       /* DS_F_SHADOW only                                   */
   int32_t update_launches;    /* DS_F_TIMING: number of timed (sampled) launches     */
   double ms_total;            /* wall time of the call (host clock)                 */
-  double ms_update;           /* DS_F_TIMING: summed event time of the timed launches
-                                 (both launches of every 32nd cycle, and the final
-                                 audit), bracketed by HIP events on the stream     */
+  double ms_update;           /* DS_F_TIMING: summed duration of the timed launches
+                                 (both launches of every 32nd cycle of every
+                                 sub-batch, and the final audit), from HIP events
+                                 in each launch's own dispatch                      */
   int64_t timed_pair_evals;   /* DS_F_TIMING: algorithmic (i, j) terms of those
                                  launches (lanes running at that cycle; the checks
                                  sharing a g-launch are not counted)               */
@@ -159,6 +171,7 @@ typedef struct {
   int32_t* width_trace;       /* optional HOST buffer: A_k for k = 1..             */
   int32_t width_trace_len;    /* capacity in; entries written out                  */
   size_t workspace_bytes;     /* bytes of workspace the call used                   */
+  int32_t sub_batches;        /* concurrent sub-batches the call ran (see streams)  */
 } ds_stats;
 
 /* Version of this header the library was built from (DS_API_VERSION). */

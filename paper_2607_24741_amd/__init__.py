@@ -27,6 +27,7 @@ __all__ = ["solve", "workspace_bytes", "load_library", "library_path", "DSError"
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 _LIBPATH = os.path.join(_PKG, "_lib", "libdrainsinkhorn.so")
+API_VERSION = 2   # the structs below mirror include/ds.h at this version
 
 MODES = {"active": 0, "static": 1, "logical": 2}
 LANE_CONVERGED, LANE_MAX_ITER, LANE_NONFINITE = 0, 1, 2
@@ -52,7 +53,8 @@ class _Problem(ctypes.Structure):
 class _Options(ctypes.Structure):
     _fields_ = [("tol", ctypes.c_float), ("screen_tol", ctypes.c_float),
                 ("max_iter", ctypes.c_int32), ("audit_every", ctypes.c_int32),
-                ("mode", ctypes.c_int32), ("flags", ctypes.c_uint32)]
+                ("mode", ctypes.c_int32), ("flags", ctypes.c_uint32),
+                ("streams", ctypes.c_int32)]
 
 
 class _Result(ctypes.Structure):
@@ -75,7 +77,7 @@ class _Stats(ctypes.Structure):
                 ("ms_check", ctypes.c_double), ("ms_compact", ctypes.c_double),
                 ("width_trace", ctypes.POINTER(ctypes.c_int32)),
                 ("width_trace_len", ctypes.c_int32),
-                ("workspace_bytes", ctypes.c_size_t)]
+                ("workspace_bytes", ctypes.c_size_t), ("sub_batches", ctypes.c_int32)]
 
 
 _lib = None
@@ -96,6 +98,9 @@ def load_library():
             "`python -m paper_2607_24741_amd.build` (or __graft_entry__.build()).")
     lib = ctypes.CDLL(_LIBPATH)
     lib.ds_api_version.restype = ctypes.c_int
+    if lib.ds_api_version() != API_VERSION:
+        raise RuntimeError(f"{_LIBPATH} implements ABI version {lib.ds_api_version()}, this "
+                           f"binding expects {API_VERSION}: rebuild the library")
     lib.ds_workspace_bytes.argtypes = [ctypes.POINTER(_Problem), ctypes.POINTER(_Options),
                                        ctypes.POINTER(ctypes.c_size_t)]
     lib.ds_workspace_bytes.restype = ctypes.c_int
@@ -115,18 +120,19 @@ def _check(lib, code):
         raise DSError(code, lib.ds_last_error_message().decode())
 
 
-def _options(tol, screen_tol, max_iter, audit_every, mode, flags):
+def _options(tol, screen_tol, max_iter, audit_every, mode, flags, streams=0):
     if mode not in MODES:
         raise ValueError(f"mode must be one of {sorted(MODES)}")
     return _Options(tol=float(tol), screen_tol=float(screen_tol or 0.0), max_iter=int(max_iter),
-                    audit_every=int(audit_every), mode=MODES[mode], flags=int(flags))
+                    audit_every=int(audit_every), mode=MODES[mode], flags=int(flags),
+                    streams=int(streams))
 
 
 def workspace_bytes(W, n_max, m_max, d, *, tol=1e-3, max_iter=5000, audit_every=1,
-                    mode="active", flags=0) -> int:
+                    mode="active", flags=0, streams=0) -> int:
     lib = load_library()
     pr = _Problem(W=W, n_max=n_max, m_max=m_max, d=d)
-    op = _options(tol, None, max_iter, audit_every, mode, flags)
+    op = _options(tol, None, max_iter, audit_every, mode, flags, streams)
     out = ctypes.c_size_t(0)
     _check(lib, lib.ds_workspace_bytes(ctypes.byref(pr), ctypes.byref(op), ctypes.byref(out)))
     return int(out.value)
@@ -154,6 +160,7 @@ class Stats:
     ms_compact: float
     width_trace: list
     workspace_bytes: int
+    sub_batches: int
     row_residual: object = None   # [W] tensor
     col_residual: object = None   # [W] tensor
 
@@ -163,8 +170,8 @@ def _ptr(t):
 
 
 def solve(X, Y, a, b, eps, tol, *, n=None, m=None, max_iter=5000, audit_every=1,
-          mode="active", screen_tol=None, flags=0, return_stats=False, workspace=None,
-          trace_len=0, out=None):
+          mode="active", screen_tol=None, flags=0, streams=0, return_stats=False,
+          workspace=None, trace_len=0, out=None):
     """Solve W independent entropic OT problems on the current GPU.
 
     X [W, n_max, d], Y [W, m_max, d], a [W, n_max], b [W, m_max], eps [W]:
@@ -192,7 +199,7 @@ def solve(X, Y, a, b, eps, tol, *, n=None, m=None, max_iter=5000, audit_every=1,
             raise ValueError(f"{name} must be a contiguous int32 tensor of shape ({W},) on {dev}")
     pr = _Problem(W=W, n_max=n_max, m_max=m_max, d=d, X=_ptr(X), Y=_ptr(Y), a=_ptr(a),
                   b=_ptr(b), eps=_ptr(eps), n=_ptr(n), m=_ptr(m))
-    op = _options(tol, screen_tol, max_iter, audit_every, mode, flags)
+    op = _options(tol, screen_tol, max_iter, audit_every, mode, flags, streams)
     need = ctypes.c_size_t(0)
     _check(lib, lib.ds_workspace_bytes(ctypes.byref(pr), ctypes.byref(op), ctypes.byref(need)))
     if workspace is None:
@@ -231,5 +238,6 @@ def solve(X, Y, a, b, eps, tol, *, n=None, m=None, max_iter=5000, audit_every=1,
                   st.l_max, st.cycles, st.audits, st.screen_positive, st.check_failures,
                   st.compactions, st.missed_ready, st.update_launches, st.ms_total, st.ms_update,
                   st.timed_pair_evals, st.ms_check, st.ms_compact, wt, st.workspace_bytes,
+                  st.sub_batches,
                   out["row_residual"], out["col_residual"])
     return ret + (stats,)

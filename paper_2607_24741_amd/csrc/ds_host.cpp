@@ -21,7 +21,10 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <memory>
+#include <mutex>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "ds.h"
@@ -37,6 +40,8 @@ ds_err fail(ds_err e, const std::string& msg) {
 }
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+constexpr int kMaxParts = 4;   // concurrent sub-batches of one call
 
 bool uses_mfma(const ds_problem* pr, const ds_options* op);
 bool uses_mat(const ds_problem* pr, const ds_options* op) {
@@ -86,9 +91,9 @@ ds::Layout plan(const ds_problem* pr, const ds_options* op, void* ws) {
     }
     B.slot = c.take<ds::SlotInfo>(W);
     B.dec = c.take<ds::Decision>(W);
+    for (int k = 0; k < 4; ++k) B.agg[k] = c.take<float4>(W * (size_t)L.rbmax);
   }
   L.center = c.take<float>(W * (size_t)L.d);
-  for (int k = 0; k < 4; ++k) L.agg[k] = c.take<float4>(W * (size_t)L.rbmax);
   L.vcnt = c.take<int>(W);
   L.nchk = c.take<int>(W);
   L.audit = c.take<ds::Audit>(W);
@@ -124,6 +129,9 @@ ds_err check_problem(const ds_problem* pr, const ds_options* op) {
   if (op->max_iter < 1) return fail(DS_E_INVALID, "max_iter must be >= 1");
   if (op->audit_every < 1) return fail(DS_E_INVALID, "audit_every must be >= 1");
   if (op->mode < DS_MODE_ACTIVE || op->mode > DS_MODE_LOGICAL) return fail(DS_E_INVALID, "unknown mode");
+  if (op->streams < 0 || op->streams > kMaxParts) return fail(DS_E_INVALID, "streams must be in 0..4");
+  if (op->streams > 1 && op->mode != DS_MODE_ACTIVE)
+    return fail(DS_E_INVALID, "sub-batches (streams > 1) need the active mode");
   if ((op->flags & DS_F_FORCE_VALU) && (op->flags & DS_F_FORCE_MFMA))
     return fail(DS_E_INVALID, "DS_F_FORCE_VALU and DS_F_FORCE_MFMA are exclusive");
   if ((op->flags & DS_F_FORCE_VALU) && pr->d > 16)
@@ -145,38 +153,55 @@ ds_err check_problem(const ds_problem* pr, const ds_options* op) {
       return fail(DS_E_HIP, std::string(#expr) + ": " + hipGetErrorString(_e));  \
   } while (0)
 
-// Per-device host resources kept for the life of the process: a pinned ring
-// for control snapshots and a pool of timing events.
+// Host resources of one sub-batch solve, kept for the life of the process in a
+// per-device pool (a call takes one per sub-batch and returns them at its end):
+// a pinned control snapshot, run-ahead events, timing events, and a stream of
+// its own (default priority, not synchronising with the legacy default stream)
+// for sub-batches beyond the first.
 constexpr int kRing = 16;
 struct DeviceRes {
-  bool ready = false;
+  bool busy = false;
   ds::HostSnap* snap = nullptr;      // pinned, device-written control mirror (host view)
   ds::HostSnap* snap_dev = nullptr;  // the same memory as the device addresses it
   hipEvent_t ring_ev[kRing];
+  hipEvent_t join_ev = nullptr;      // end of this sub-batch's work on its stream
+  hipStream_t stream = nullptr;
   std::vector<hipEvent_t> timing;
 };
-thread_local DeviceRes g_res[64];
+std::mutex g_pool_mu;
+std::vector<std::unique_ptr<DeviceRes>> g_pool[64];
 
-hipError_t device_res(DeviceRes** out) {
+// A free resource set of the current device (created on first need).
+hipError_t acquire_res(DeviceRes** out) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
   if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
-  DeviceRes& r = g_res[dev];
-  if (!r.ready) {
-    e = hipHostMalloc(reinterpret_cast<void**>(&r.snap), sizeof(ds::HostSnap),
-                      hipHostMallocMapped | hipHostMallocCoherent);
+  std::lock_guard<std::mutex> lock(g_pool_mu);
+  for (auto& r : g_pool[dev])
+    if (!r->busy) { r->busy = true; *out = r.get(); return hipSuccess; }
+  auto r = std::make_unique<DeviceRes>();
+  e = hipHostMalloc(reinterpret_cast<void**>(&r->snap), sizeof(ds::HostSnap),
+                    hipHostMallocMapped | hipHostMallocCoherent);
+  if (e != hipSuccess) return e;
+  e = hipHostGetDevicePointer(reinterpret_cast<void**>(&r->snap_dev), r->snap, 0);
+  if (e != hipSuccess) return e;
+  for (int i = 0; i < kRing; ++i) {
+    e = hipEventCreateWithFlags(&r->ring_ev[i], hipEventDisableTiming);
     if (e != hipSuccess) return e;
-    e = hipHostGetDevicePointer(reinterpret_cast<void**>(&r.snap_dev), r.snap, 0);
-    if (e != hipSuccess) return e;
-    for (int i = 0; i < kRing; ++i) {
-      e = hipEventCreateWithFlags(&r.ring_ev[i], hipEventDisableTiming);
-      if (e != hipSuccess) return e;
-    }
-    r.ready = true;
   }
-  *out = &r;
+  e = hipEventCreateWithFlags(&r->join_ev, hipEventDisableTiming);
+  if (e != hipSuccess) return e;
+  e = hipStreamCreateWithFlags(&r->stream, hipStreamNonBlocking);
+  if (e != hipSuccess) return e;
+  r->busy = true;
+  *out = r.get();
+  g_pool[dev].push_back(std::move(r));
   return hipSuccess;
+}
+void release_res(DeviceRes* r) {
+  std::lock_guard<std::mutex> lock(g_pool_mu);
+  r->busy = false;
 }
 
 struct EventTimer {
@@ -209,57 +234,26 @@ struct EventTimer {
   }
 };
 
-}  // namespace
+// One sub-batch (or the whole window): ingest, the control loop of cycles,
+// the final audit and the emission of its lanes, all on stream st. Fills the
+// counters the caller merges into ds_stats.
+struct Timed { int cycle, kind; };
+struct PartOut {
+  ds::Ctrl ctrl;
+  int launched = 0, compactions = 0, n_timed = 0;
+  int64_t bytes_compacted = 0;
+  bool timing = false;
+  std::vector<Timed> timed;
+  double ms_update = 0.0, ms_compact = 0.0;
+  std::vector<int32_t> nchk;
+  std::vector<ds::SlotInfo> lanes;
+  size_t ws_bytes = 0;
+};
 
-extern "C" {
-
-int ds_api_version(void) { return DS_API_VERSION; }
-
-const char* ds_error_string(ds_err e) {
-  switch (e) {
-    case DS_OK: return "ok";
-    case DS_E_INVALID: return "invalid argument";
-    case DS_E_WORKSPACE: return "workspace missing, misaligned or too small";
-    case DS_E_HIP: return "HIP runtime error";
-    case DS_E_UNSUPPORTED: return "unsupported configuration";
-    case DS_E_INTERNAL: return "internal error";
-  }
-  return "unknown error";
-}
-
-const char* ds_last_error_message(void) { return g_last_error.c_str(); }
-
-ds_err ds_workspace_bytes(const ds_problem* pr, const ds_options* op, size_t* bytes) {
-  g_last_error.clear();
-  if (!bytes) return fail(DS_E_INVALID, "bytes must not be NULL");
-  ds_err e = check_problem(pr, op);
-  if (e != DS_OK) return e;
-  *bytes = plan(pr, op, nullptr).bytes;
-  return DS_OK;
-}
-
-ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res, void* ws,
-                size_t ws_bytes, void* stream_v, ds_stats* stats) {
+ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* res, void* ws,
+                  hipStream_t st, DeviceRes* R, PartOut& out) {
   using namespace ds;
-  const auto t_start = std::chrono::steady_clock::now();
-  g_last_error.clear();
-  ds_err e = check_problem(pr, op);
-  if (e != DS_OK) return e;
-  if (!res) return fail(DS_E_INVALID, "result must not be NULL");
-  if (!pr->X || !pr->Y || !pr->a || !pr->b || !pr->eps)
-    return fail(DS_E_INVALID, "X, Y, a, b and eps must not be NULL");
-  if (!res->f || !res->g || !res->depth || !res->residual || !res->status)
-    return fail(DS_E_INVALID, "f, g, depth, residual and status must not be NULL");
-  Layout L = plan(pr, op, nullptr);
-  if (!ws) return fail(DS_E_WORKSPACE, "workspace is NULL");
-  if (reinterpret_cast<uintptr_t>(ws) % 256) return fail(DS_E_WORKSPACE, "workspace must be 256-byte aligned");
-  if (ws_bytes < L.bytes)
-    return fail(DS_E_WORKSPACE, "workspace too small: need " + std::to_string(L.bytes) + " bytes");
-  L = plan(pr, op, ws);
-  hipStream_t st = reinterpret_cast<hipStream_t>(stream_v);
-  DeviceRes* R = nullptr;
-  HIP_TRY(device_res(&R));
-
+  Layout L = plan(pr, op, ws);
   const int W = pr->W, d = pr->d;
   const int mode = op->mode;
   const bool active = (mode == DS_MODE_ACTIVE);
@@ -283,7 +277,6 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
   ia.pad[0] = L.pad[0]; ia.pad[1] = L.pad[1];
   ia.bank = L.bank[0];
   ia.center = L.center;
-  for (int k = 0; k < 4; ++k) ia.agg[k] = L.agg[k];
   ia.vcnt = L.vcnt; ia.nchk = L.nchk; ia.rbmax = L.rbmax;
   ia.precise = precise ? 1 : 0;
   ia.mat = mat ? 1 : 0;
@@ -333,14 +326,16 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
     u.w_ld = role ? pr->m_max : pr->n_max;
     u.off = L.off[role];
     if (kind == 0) {
-      u.agg_out = L.agg[role == 0 ? AGG_F : AGG_G];
-      u.agg_bound = L.agg[role == 0 ? AGG_G : AGG_F];
+      u.agg_out = B.agg[role == 0 ? AGG_F : AGG_G];
+      u.agg_bound = B.agg[role == 0 ? AGG_G : AGG_F];
     } else {
-      u.agg_out = L.agg[role == 0 ? AGG_ROW : AGG_COL];
-      u.agg_screen = L.agg[AGG_F];
-      u.agg_rowchk = L.agg[AGG_ROW];
+      u.agg_out = B.agg[role == 0 ? AGG_ROW : AGG_COL];
+      u.agg_screen = B.agg[AGG_F];
+      u.agg_rowchk = B.agg[AGG_ROW];
     }
     u.A = A; u.ipl = ipl[role];
+    u.nr = role ? lanes[0].m : lanes[0].n;   // read only when ipl > 0 (uniform shapes)
+    u.nc = role ? lanes[0].n : lanes[0].m;
     u.padr = L.pad[rs]; u.padc = L.pad[cs];
     u.role = role; u.kind = kind;
     return u;
@@ -358,12 +353,11 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
     return l;
   };
   // DS_F_TIMING: both launches of every kSampleEvery-th cycle (and the final
-  // audit) are bracketed by events; the rest run untouched. Each timed launch
-  // remembers its cycle so its algorithmic (i, j) terms can be counted from the
-  // completion depths afterwards (kind 0: update halves of cycle k, kind 1:
-  // one marginal pass of the final audit).
+  // audit) carry events in their own dispatch; the rest run untouched. Each
+  // timed launch remembers its cycle so its algorithmic (i, j) terms can be
+  // counted from the completion depths afterwards (kind 0: update halves of
+  // cycle k, kind 1: one marginal pass of the final audit).
   constexpr int kSampleEvery = 32;
-  struct Timed { int cycle, kind; };
   std::vector<Timed> timed_launches;
   // Kernel variant by the width bound of the launch: few items -> more waves
   // per item (shorter sweeps); many items -> more rows per wave (fewer column
@@ -435,7 +429,7 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
       ma.src = L.bank[bank]; ma.dst = L.bank[bank ^ 1]; ma.ctrl = L.ctrl;
       ma.A = A; ma.dp = L.dp; ma.compact = 1; ma.emit_all = 0; ma.mode = mode;
       ma.pad[0] = L.pad[0]; ma.pad[1] = L.pad[1];
-      ma.n_max = pr->n_max; ma.m_max = pr->m_max; ma.chunk = 1024; ma.es = L.es;
+      ma.n_max = pr->n_max; ma.m_max = pr->m_max; ma.chunk = 1024; ma.es = L.es; ma.rbmax = L.rbmax;
       ma.f = res->f; ma.g = res->g; ma.depth = res->depth; ma.residual = res->residual;
       ma.row_res = res->row_residual; ma.col_res = res->col_residual; ma.status = res->status;
       HIP_TRY(launch_move(ma, A, maxpad, st));
@@ -449,8 +443,8 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
     }
     if (A <= 0) { finished = true; break; }
     const int pk = k & 1, pk1 = (k - 1) & 1;
-    const bool audit_prev = (k - 1 >= 1) && ((k - 1) % ae == 0);
     const bool sample = (k % kSampleEvery) == 0;
+    const bool audit_prev = (k - 1 >= 1) && ((k - 1) % ae == 0);
     // f-half of cycle k (+ row screen of state k-1)
     Launch lf = make_launch();
     lf.p[0] = make_pass(0, 0, pk1, pk, pk1);
@@ -487,8 +481,8 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
       q.push_back({idx, k});
     }
   }
+  HIP_TRY(hipMemcpyAsync(&ctrl, L.ctrl, sizeof(Ctrl), hipMemcpyDeviceToHost, st));
   HIP_TRY(hipStreamSynchronize(st));
-  HIP_TRY(hipMemcpy(&ctrl, L.ctrl, sizeof(Ctrl), hipMemcpyDeviceToHost));
   A = ctrl.A;
 
   // ------------------------------------------------------- final audit
@@ -515,8 +509,8 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
     r = run(lw, vw, lw.nb0, true, K, 1);
     if (r != DS_OK) return r;
     A = saveA;
+    HIP_TRY(hipMemcpyAsync(&ctrl, L.ctrl, sizeof(Ctrl), hipMemcpyDeviceToHost, st));
     HIP_TRY(hipStreamSynchronize(st));
-    HIP_TRY(hipMemcpy(&ctrl, L.ctrl, sizeof(Ctrl), hipMemcpyDeviceToHost));
   }
   // ------------------------------------------------------------ emission
   {
@@ -526,12 +520,175 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
     ma.A = A; ma.dp = L.dp; ma.compact = 0; ma.emit_all = (mode == DS_MODE_STATIC); ma.mode = mode;
     ma.final_par = ctrl.final_cycle & 1;
     ma.pad[0] = L.pad[0]; ma.pad[1] = L.pad[1];
-    ma.n_max = pr->n_max; ma.m_max = pr->m_max; ma.chunk = 1024; ma.es = L.es;
+    ma.n_max = pr->n_max; ma.m_max = pr->m_max; ma.chunk = 1024; ma.es = L.es; ma.rbmax = L.rbmax;
     ma.f = res->f; ma.g = res->g; ma.depth = res->depth; ma.residual = res->residual;
     ma.row_res = res->row_residual; ma.col_res = res->col_residual; ma.status = res->status;
     HIP_TRY(launch_move(ma, A, maxpad, st));
-    if (res->order) HIP_TRY(launch_order(res->depth, W, res->order, st));
   }
+  out.nchk.resize(W);
+  HIP_TRY(hipMemcpyAsync(out.nchk.data(), L.nchk, sizeof(int32_t) * W, hipMemcpyDeviceToHost, st));
+  HIP_TRY(hipStreamSynchronize(st));
+  out.ctrl = ctrl;
+  out.launched = launched;
+  out.compactions = compactions;
+  out.bytes_compacted = bytes_compacted;
+  out.timing = tm.on;
+  out.n_timed = (int)tm.spans[0].size();
+  if (tm.on) {
+    out.ms_update = tm.total(0);
+    out.ms_compact = tm.total(1);
+  }
+  out.timed = std::move(timed_launches);
+  out.lanes = std::move(lanes);
+  out.ws_bytes = L.bytes;
+  return DS_OK;
+}
+
+// Sub-batches: contiguous lane ranges solved concurrently, each on its own
+// stream with its own workspace part and control loop. Lanes are independent,
+// so the results are those of one batch bit for bit; the launch latencies of
+// one sub-batch overlap the work of the others. Active mode only (the static
+// and logical modes share one final cycle across the window).
+int parts_of(const ds_problem* pr, const ds_options* op) {
+  if (op->streams > 0) return std::min(op->streams, pr->W);
+  if (op->mode != DS_MODE_ACTIVE || uses_mat(pr, op)) return 1;
+  return pr->W >= 48 ? 3 : (pr->W >= 32 ? 2 : 1);
+}
+int part_lo(const ds_problem* pr, int parts, int p) {
+  return (int)((int64_t)pr->W * p / parts);
+}
+ds_problem sub_problem(const ds_problem* pr, int lo, int hi) {
+  ds_problem s = *pr;
+  s.W = hi - lo;
+  s.X = pr->X + (size_t)lo * pr->n_max * pr->d;
+  s.Y = pr->Y + (size_t)lo * pr->m_max * pr->d;
+  s.a = pr->a + (size_t)lo * pr->n_max;
+  s.b = pr->b + (size_t)lo * pr->m_max;
+  s.eps = pr->eps + lo;
+  s.n = pr->n ? pr->n + lo : nullptr;
+  s.m = pr->m ? pr->m + lo : nullptr;
+  return s;
+}
+ds_result sub_result(const ds_problem* pr, const ds_result* res, int lo) {
+  ds_result s = *res;
+  s.f = res->f + (size_t)lo * pr->n_max;
+  s.g = res->g + (size_t)lo * pr->m_max;
+  s.depth = res->depth + lo;
+  s.residual = res->residual + lo;
+  s.row_residual = res->row_residual ? res->row_residual + lo : nullptr;
+  s.col_residual = res->col_residual ? res->col_residual + lo : nullptr;
+  s.status = res->status + lo;
+  s.order = nullptr;
+  return s;
+}
+// workspace offset of every part (and the total, last)
+std::vector<size_t> part_offsets(const ds_problem* pr, const ds_options* op, int parts) {
+  std::vector<size_t> off(parts + 1, 0);
+  for (int p = 0; p < parts; ++p) {
+    const ds_problem s = sub_problem(pr, part_lo(pr, parts, p), part_lo(pr, parts, p + 1));
+    off[p + 1] = off[p] + align_up(plan(&s, op, nullptr).bytes, 256);
+  }
+  return off;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ds_api_version(void) { return DS_API_VERSION; }
+
+const char* ds_error_string(ds_err e) {
+  switch (e) {
+    case DS_OK: return "ok";
+    case DS_E_INVALID: return "invalid argument";
+    case DS_E_WORKSPACE: return "workspace missing, misaligned or too small";
+    case DS_E_HIP: return "HIP runtime error";
+    case DS_E_UNSUPPORTED: return "unsupported configuration";
+    case DS_E_INTERNAL: return "internal error";
+  }
+  return "unknown error";
+}
+
+const char* ds_last_error_message(void) { return g_last_error.c_str(); }
+
+ds_err ds_workspace_bytes(const ds_problem* pr, const ds_options* op, size_t* bytes) {
+  g_last_error.clear();
+  if (!bytes) return fail(DS_E_INVALID, "bytes must not be NULL");
+  ds_err e = check_problem(pr, op);
+  if (e != DS_OK) return e;
+  const int parts = parts_of(pr, op);
+  *bytes = part_offsets(pr, op, parts)[parts];
+  return DS_OK;
+}
+
+ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res, void* ws,
+                size_t ws_bytes, void* stream_v, ds_stats* stats) {
+  using namespace ds;
+  const auto t_start = std::chrono::steady_clock::now();
+  g_last_error.clear();
+  ds_err e = check_problem(pr, op);
+  if (e != DS_OK) return e;
+  if (!res) return fail(DS_E_INVALID, "result must not be NULL");
+  if (!pr->X || !pr->Y || !pr->a || !pr->b || !pr->eps)
+    return fail(DS_E_INVALID, "X, Y, a, b and eps must not be NULL");
+  if (!res->f || !res->g || !res->depth || !res->residual || !res->status)
+    return fail(DS_E_INVALID, "f, g, depth, residual and status must not be NULL");
+  const int parts = parts_of(pr, op);
+  const std::vector<size_t> off = part_offsets(pr, op, parts);
+  if (!ws) return fail(DS_E_WORKSPACE, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(ws) % 256) return fail(DS_E_WORKSPACE, "workspace must be 256-byte aligned");
+  if (ws_bytes < off[parts])
+    return fail(DS_E_WORKSPACE, "workspace too small: need " + std::to_string(off[parts]) + " bytes");
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream_v);
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  const int W = pr->W;
+  const int mode = op->mode;
+  const bool active = (mode == DS_MODE_ACTIVE);
+  const int ae = op->audit_every;
+
+  // resources of every part; parts beyond the first start behind the work
+  // already queued on the caller's stream
+  std::vector<DeviceRes*> Rs(parts, nullptr);
+  struct Releaser {
+    std::vector<DeviceRes*>& v;
+    ~Releaser() { for (DeviceRes* r : v) if (r) release_res(r); }
+  } releaser{Rs};
+  for (int p = 0; p < parts; ++p) HIP_TRY(acquire_res(&Rs[p]));
+  const bool timing = (op->flags & DS_F_TIMING) != 0;
+  if (parts > 1) {
+    HIP_TRY(hipEventRecord(Rs[0]->join_ev, st));
+    for (int p = 1; p < parts; ++p) HIP_TRY(hipStreamWaitEvent(Rs[p]->stream, Rs[0]->join_ev, 0));
+  }
+  std::vector<PartOut> outs(parts);
+  std::vector<ds_err> errs(parts, DS_OK);
+  std::vector<std::string> msgs(parts);
+  auto work = [&](int p) {
+    if (p > 0) {
+      const hipError_t he = hipSetDevice(dev);
+      if (he != hipSuccess) { errs[p] = DS_E_HIP; msgs[p] = hipGetErrorString(he); return; }
+    }
+    const int lo = part_lo(pr, parts, p), hi = part_lo(pr, parts, p + 1);
+    const ds_problem sp = sub_problem(pr, lo, hi);
+    const ds_result sr = sub_result(pr, res, lo);
+    hipStream_t s = p == 0 ? st : Rs[p]->stream;
+    errs[p] = solve_part(&sp, op, &sr, static_cast<char*>(ws) + off[p], s, Rs[p], outs[p]);
+    if (errs[p] != DS_OK) msgs[p] = g_last_error;
+    if (p > 0 && errs[p] == DS_OK) {
+      const hipError_t he = hipEventRecord(Rs[p]->join_ev, s);
+      if (he != hipSuccess) { errs[p] = DS_E_HIP; msgs[p] = hipGetErrorString(he); }
+    }
+  };
+  {
+    std::vector<std::thread> th;
+    for (int p = 1; p < parts; ++p) th.emplace_back(work, p);
+    work(0);
+    for (auto& t : th) t.join();
+  }
+  for (int p = 0; p < parts; ++p)
+    if (errs[p] != DS_OK) return fail(errs[p], msgs[p]);
+  for (int p = 1; p < parts; ++p) HIP_TRY(hipStreamWaitEvent(st, Rs[p]->join_ev, 0));
+  if (res->order) HIP_TRY(launch_order(res->depth, W, res->order, st));
   std::vector<int32_t> depth(W), status(W);
   HIP_TRY(hipMemcpyAsync(depth.data(), res->depth, sizeof(int32_t) * W, hipMemcpyDeviceToHost, st));
   HIP_TRY(hipMemcpyAsync(status.data(), res->status, sizeof(int32_t) * W, hipMemcpyDeviceToHost, st));
@@ -549,32 +706,39 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
     // of every cycle up to its depth (active) or up to l_max (static, logical);
     // speculative halves are not algorithmic work and are not counted here
     std::vector<int64_t> nm(W);
-    for (int t = 0; t < W; ++t) nm[t] = (int64_t)lanes[t].n * (int64_t)lanes[t].m;
-    std::vector<int32_t> nchk(W);
-    HIP_TRY(hipMemcpy(nchk.data(), L.nchk, sizeof(int32_t) * W, hipMemcpyDeviceToHost));
-    int64_t upd = 0, chk = 0;
-    for (int t = 0; t < W; ++t) {
-      upd += 2 * (int64_t)(active ? depth[t] : lmax) * nm[t];
-      chk += (int64_t)nchk[t] * nm[t];
+    int64_t upd = 0, chk = 0, retire_events = 0;
+    int launched = 0, finished_all = 1;
+    for (int p = 0; p < parts; ++p) {
+      const int lo = part_lo(pr, parts, p);
+      const PartOut& o = outs[p];
+      for (size_t u = 0; u < o.lanes.size(); ++u) {
+        const int t = lo + (int)u;
+        nm[t] = (int64_t)o.lanes[u].n * (int64_t)o.lanes[u].m;
+        chk += (int64_t)o.nchk[u] * nm[t];
+      }
+      retire_events += o.ctrl.retire_events;
+      launched = std::max(launched, o.launched);
+      finished_all &= o.ctrl.finished ? 1 : 0;
+      S.screen_positive += o.ctrl.screen_pos;
+      S.check_failures += o.ctrl.check_fail;
+      S.missed_ready += o.ctrl.missed_ready;
+      S.compactions += o.compactions;
+      S.update_launches += o.n_timed;   // timed launches
+      S.workspace_bytes += o.ws_bytes;
+      S.bytes_compacted += o.bytes_compacted;
     }
+    for (int t = 0; t < W; ++t) upd += 2 * (int64_t)(active ? depth[t] : lmax) * nm[t];
     S.pair_evals = upd;
     S.check_pair_evals = chk;
-    S.halfsteps_executed = 0;
     // every lane ran its l_t cycles; a lane retired at an ordinary audit also
     // ran the cycle after it (its discarded f-half and the g-half that shared
     // the launch with its check)
-    S.halfsteps_executed = active ? 2 * sum_l + 2 * (int64_t)ctrl.retire_events
-                                  : 2 * (int64_t)W * (lmax + (ctrl.finished ? 1 : 0));
+    S.halfsteps_executed = active ? 2 * sum_l + 2 * retire_events
+                                  : 2 * (int64_t)W * (lmax + (finished_all ? 1 : 0));
     S.cycles = launched;
+    S.sub_batches = parts;
     S.audits = 0;
     for (int k = 1; k <= launched; ++k) S.audits += (k % ae == 0) ? 1 : 0;
-    S.screen_positive = ctrl.screen_pos;
-    S.check_failures = ctrl.check_fail;
-    S.missed_ready = ctrl.missed_ready;
-    S.compactions = compactions;
-    S.update_launches = (int)tm.spans[0].size();   // timed (sampled) launches
-    S.workspace_bytes = L.bytes;
-    S.bytes_compacted = bytes_compacted;
     if (stats->width_trace && stats->width_trace_len > 0) {
       const int cap = stats->width_trace_len;
       int n = 0;
@@ -586,22 +750,25 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
       S.width_trace_len = n;
     }
     S.width_trace = stats->width_trace;
-    if (tm.on) {
+    if (timing) {
       // algorithmic terms of the timed launches: one half-step over the lanes
-      // still running at that cycle, or one marginal pass of the final audit
+      // of its sub-batch still running at that cycle, or one marginal pass of
+      // the final audit
       int64_t tp = 0;
-      for (const Timed& q : timed_launches) {
-        for (int t = 0; t < W; ++t) {
-          const bool in = q.kind == 0 ? (active ? depth[t] >= q.cycle : q.cycle <= lmax)
-                                      : (mode == DS_MODE_STATIC || depth[t] == q.cycle);
-          if (in) tp += nm[t];
-        }
+      for (int p = 0; p < parts; ++p) {
+        const int lo = part_lo(pr, parts, p), hi = part_lo(pr, parts, p + 1);
+        int plmax = 0;
+        for (int t = lo; t < hi; ++t) plmax = std::max(plmax, depth[t]);
+        for (const Timed& q : outs[p].timed)
+          for (int t = lo; t < hi; ++t) {
+            const bool in = q.kind == 0 ? (active ? depth[t] >= q.cycle : q.cycle <= plmax)
+                                        : (mode == DS_MODE_STATIC || depth[t] == q.cycle);
+            if (in) tp += nm[t];
+          }
+        S.ms_update += outs[p].ms_update;
+        S.ms_compact += outs[p].ms_compact;
       }
       S.timed_pair_evals = tp;
-    }
-    if (tm.on) {
-      S.ms_update = tm.total(0);
-      S.ms_compact = tm.total(1);
       S.ms_check = 0.0;
     }
     S.ms_total = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t_start).count();

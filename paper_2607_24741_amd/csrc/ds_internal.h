@@ -39,7 +39,7 @@ constexpr int kMaxDSmall = 32;   // matrix-free kernels
 constexpr int kMatMaxPts = 8192; // materialised cost: points per lane side (LDS staging)
 constexpr float kFastRange = 64.f;  // max spread of the bound (log2 units) for anchored sums
 constexpr float kFastRangePrecise = 1.f;  // the same for the float64 state
-constexpr int kMaxTimed = 4096;     // timed launches per solve (DS_F_TIMING)
+constexpr int kMaxTimed = 4096;     // timed launches per sub-batch (DS_F_TIMING)
 // launch-variant thresholds (work items of the launch, see launch_update)
 constexpr int kWideItems = 1536;
 constexpr int kMediumItemsMfma = 512;
@@ -104,6 +104,13 @@ struct Decision {
 // With the float64 (precise) state every array below holds doubles in the same
 // shape (the float pointers are reinterpreted) and records are not
 // de-interleaved.
+// Row-block aggregates of a pass, by slot: {screen or residual partial sum,
+// min and max of the lse change, non-finite flag}. [0] f-half, [1] g-half,
+// [2] row check, [3] column check. Slot indexing lets a block fetch its lane's
+// aggregates together with its operands, before it has read its slot record;
+// compaction carries them to the survivors' new slots.
+enum { AGG_F = 0, AGG_G = 1, AGG_ROW = 2, AGG_COL = 3 };
+
 struct Bank {
   float* rec[2];     // side 0 (x), side 1 (y): [W][pad][dp] scaled, centred, de-interleaved
   float* lm[2];      // log2 masses [W][pad]; -inf for dead points
@@ -111,12 +118,8 @@ struct Bank {
   float* gam[2][2];  // [side][parity] [W][pad]; -inf for dead points
   SlotInfo* slot;    // [W]
   Decision* dec;     // [W]
+  float4* agg[4];    // [W][rbmax] row-block aggregates by slot
 };
-
-// Row-block aggregates, indexed by caller lane id (they never move):
-// {screen or residual partial sum, min and max of the lse change, non-finite
-// flag}. [0] f-half, [1] g-half, [2] row check, [3] column check.
-enum { AGG_F = 0, AGG_G = 1, AGG_ROW = 2, AGG_COL = 3 };
 
 struct Layout {
   int W, n_max, m_max, d, dp, dh;
@@ -127,7 +130,6 @@ struct Layout {
   int rows;          // rows per work item (kernel dependent)
   Bank bank[2];
   float* center;     // [W][d] (ingest only)
-  float4* agg[4];    // [W][rbmax]
   int* vcnt;         // [W] column-check arrival counters
   int* nchk;         // [W] marginal evaluation passes spent on checks, per caller lane
   Audit* audit;      // [W]
@@ -159,6 +161,7 @@ struct Pass {
   const float4* agg_screen;  // column check: the f-half aggregates (row screen)
   const float4* agg_rowchk;  // final column check: the row-check aggregates
   int A, ipl;             // slots; uniform items per lane (0: use off)
+  int nr, nc;             // uniform lane shapes (ipl > 0): rows and columns of every lane
   int padr, padc, w_ld;
   int role;               // 0: rows are x (f-half), 1: rows are y (g-half)
   int kind;               // 0: update, 1: check (marginal ratio of the input state)
@@ -201,6 +204,7 @@ struct MoveArgs {
   int A, dp, compact, emit_all, mode;
   int pad[2];
   int es;                 // state element size in floats (1 or 2)
+  int rbmax;              // row-block aggregates per slot
   int n_max, m_max;
   int final_par;          // parity of the final state (static mode emission)
   int chunk;              // points per block per side
@@ -219,7 +223,6 @@ struct IngestArgs {
   int mat;                // materialised cost: no records, cold start gam^y = 0
   Bank bank;
   float* center;
-  float4* agg[4];
   int* vcnt;
   int* nchk;
   int rbmax;

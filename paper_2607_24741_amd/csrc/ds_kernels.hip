@@ -160,17 +160,17 @@ __device__ void retire_lane(const Launch& L, const Pass& P, int s, const SlotInf
 }
 
 // -------------------------------------------------- lane-level aggregates
-// Fixed-order reduction (by one wave) of one lane's row-block aggregates
+// Fixed-order reduction (by one wave) of the row-block aggregates of slot s
 // {sum, min, max, non-finite flag}; every lane of the wave returns the same bits.
 struct LaneAgg {
   float sum, dmin, dmax;
   int bad;
 };
-__device__ __forceinline__ LaneAgg lane_aggregate(const float4* agg, int lane_id, int rbmax,
-                                                  int nrb, bool coherent) {
+__device__ __forceinline__ LaneAgg lane_aggregate(const float4* agg, int s, int rbmax, int nrb,
+                                                  bool coherent) {
   LaneAgg g;
   float t0 = 0.f, t1 = INFINITY, t2 = -INFINITY, t3 = 0.f;
-  const float4* base = agg + (size_t)lane_id * rbmax;
+  const float4* base = agg + (size_t)s * rbmax;
   for (int q = (int)(threadIdx.x & 63); q < nrb; q += 64) {
     const float4 v = coherent ? ld_dev4(base + q) : base[q];
     t0 += v.x;
@@ -191,20 +191,20 @@ __device__ __forceinline__ LaneAgg lane_aggregate(const float4* agg, int lane_id
 // Update: lse_new - lse_old lies in [min_j dgam_j, max_j dgam_j], dgam being
 // the latest change of the column operand (= -(change of the column lse)), so
 // anchored (max-free) sums are safe when that spread is small; M = -min dgam.
-__device__ __forceinline__ void update_facts(const Launch& L, const Pass& P, const SlotInfo& si,
+__device__ __forceinline__ void update_facts(const Launch& L, const Pass& P, int s, int ncols,
                                              bool& fast, float& M, float range = kFastRange) {
-  const int ncols = P.role ? si.n : si.m;
-  const LaneAgg g = lane_aggregate(P.agg_bound, si.lane, L.rbmax, row_blocks(ncols, L.rows), false);
+  const LaneAgg g = lane_aggregate(P.agg_bound, s, L.rbmax, row_blocks(ncols, L.rows), false);
   fast = !g.bad && g.dmin <= g.dmax && (g.dmax - g.dmin) <= range;
   M = -g.dmin;
 }
 // Check: whether this lane is checked at all (screen-positive, non-finite
-// screen, or every lane), and the row screen of the audited state.
-__device__ __forceinline__ bool check_facts(const Launch& L, const Pass& P, const SlotInfo& si,
+// screen, or every lane), and the row screen of the audited state (n_x: the
+// lane's source points, whose row blocks carry the screen).
+__device__ __forceinline__ bool check_facts(const Launch& L, const Pass& P, int s, int n_x,
                                             float& rhat) {
   rhat = NAN;
   if (P.role == 1 && !P.final_audit) {
-    const LaneAgg g = lane_aggregate(P.agg_screen, si.lane, L.rbmax, row_blocks(si.n, L.rows), false);
+    const LaneAgg g = lane_aggregate(P.agg_screen, s, L.rbmax, row_blocks(n_x, L.rows), false);
     rhat = g.sum;
     return P.verify_all || !isfinite(g.sum) || g.sum <= L.tau_screen;
   }
@@ -272,7 +272,7 @@ __device__ void finish_rows(const Launch& L, const Pass& P, int s, const SlotInf
     }
   }
   const int nu = min(NU, nrb - rb0);
-  float4* dst = P.agg_out + (size_t)si.lane * L.rbmax + rb0;
+  float4* dst = P.agg_out + (size_t)s * L.rbmax + rb0;
   const bool deciding = P.kind == KIND_VERIFY && P.role == 1 && P.decide;
   if (!deciding) {
     if (lane == 0)
@@ -298,10 +298,10 @@ __device__ void finish_rows(const Launch& L, const Pass& P, int s, const SlotInf
   last = __builtin_amdgcn_readfirstlane(last);
   if (!last) return;
   // last item of a checked lane: column residual and the decision
-  const LaneAgg gc = lane_aggregate(P.agg_out, si.lane, L.rbmax, nrb, true);
+  const LaneAgg gc = lane_aggregate(P.agg_out, s, L.rbmax, nrb, true);
   float rrow = rhat;
   if (P.final_audit) {
-    const LaneAgg gr = lane_aggregate(P.agg_rowchk, si.lane, L.rbmax, row_blocks(si.n, UNIT), false);
+    const LaneAgg gr = lane_aggregate(P.agg_rowchk, s, L.rbmax, row_blocks(si.n, UNIT), false);
     rrow = gr.sum;
   }
   if (lane != 0) return;
@@ -346,33 +346,90 @@ __device__ __forceinline__ int xcd_item(int b, int N) {
   return x * q + min(x, r) + (b >> 3);
 }
 
-// Decide what block b of a pass does: the slot s and the first row block rb0
-// of its item (RPI row blocks per item; RPI > 1 only for uniform lane shapes).
-// Returns false when the block has no work.
-template <int RPI>
-__device__ __forceinline__ bool locate_item(const Launch& L, const Pass& P, int b, int& s,
-                                            int& rb0, SlotInfo& si) {
-  const Ctrl* c = L.ctrl;
-  if (!P.final_audit && c->finished) return false;
-  const int A = min(P.A, c->A);
-  if (P.ipl > 0) {
-    const int ipi = (P.ipl + RPI - 1) / RPI;   // items per lane
-    const int N = ipi * A;
-    if (b >= N) return false;
-    const int item = xcd_item(b, N);
-    s = item / ipi;
-    rb0 = (item - s * ipi) * RPI;
-  } else {
-    const int N = P.off[A];
-    if (b >= N) return false;
-    const int item = xcd_item(b, N);
-    s = find_slot(P.off, A, item);
-    rb0 = item - P.off[s];
-  }
-  si = L.slot[s];
+// Ties the device-state values a block checks (slot record, control block) to
+// a value computed from the item's own loads, so the compiler cannot test them
+// -- and wait for them -- before those loads are in flight.
+__device__ __forceinline__ void behind(SlotInfo& si, int& c_fin, int& c_A, float dep) {
+  __asm__ volatile("" : "+v"(si.lane), "+v"(si.n), "+v"(si.m), "+v"(si.done), "+v"(si.passed),
+                   "+v"(c_fin), "+v"(c_A) : "v"(dep));
+}
+
+// Whether the item of slot s has work, given the control block's finished
+// flag and width and the slot record.
+__device__ __forceinline__ bool item_live(const Launch& L, const Pass& P, int s, const SlotInfo& si,
+                                          int c_finished, int c_A) {
+  if (!P.final_audit && c_finished) return false;
+  if (s >= c_A) return false;
   if (P.kind == KIND_UPDATE) return !(si.done && L.mode == MODE_ACTIVE);
   if (si.done) return false;
   if (!P.final_audit && si.passed) return false;
+  return true;
+}
+
+// Uniform lane shapes (P.ipl > 0): block b of pass pi takes item
+// xcd_item(b, nb) of the pass's own nb blocks, so its slot s and first row
+// block rb0 (RPI row blocks per item) follow from the launch alone and the
+// block can issue its operand loads before any read of device state. The host
+// sizes every pass to at least the items of the device-side layout, so every
+// item is covered; blocks past it are dropped by item_live(). False only for
+// slots beyond the launch's own width bound (never read).
+template <int RPI>
+__device__ __forceinline__ bool item_uniform(const Launch& L, const Pass& P, int pi, int b, int& s,
+                                             int& rb0) {
+  const int nb = pi ? (int)gridDim.x - L.nb0 : L.nb0;
+  const int ipi = (P.ipl + RPI - 1) / RPI;   // items per lane
+  const int item = xcd_item(b, nb);
+  s = item / ipi;
+  rb0 = (item - s * ipi) * RPI;
+  return s < P.A;
+}
+
+// Mixed lane shapes: the item comes from the offsets table of the device-side
+// layout (slot s, first row block rb0); false when the block has no work.
+__device__ __forceinline__ bool locate_item(const Launch& L, const Pass& P, int b, int& s,
+                                            int& rb0, SlotInfo& si) {
+  const Ctrl* c = L.ctrl;
+  const int fin = c->finished;
+  const int A = min(P.A, c->A);
+  if (!P.final_audit && fin) return false;
+  const int N = P.off[A];
+  if (b >= N) return false;
+  const int item = xcd_item(b, N);
+  s = find_slot(P.off, A, item);
+  rb0 = item - P.off[s];
+  si = L.slot[s];
+  return item_live(L, P, s, si, fin, A);
+}
+
+// Where block b of a pass works (slot s, first row block rb0, the lane's row
+// and column counts). With uniform shapes the control block and slot record
+// are only requested here (c_fin, c_A, si) and checked by item_live() once
+// the item's own loads are in flight; otherwise they are already checked.
+template <int RPI, int UNI = -1>
+__device__ __forceinline__ bool place_item(const Launch& L, const Pass& P, int pi, int b, int& s,
+                                           int& rb0, int& nrows, int& ncols, SlotInfo& si,
+                                           int& c_fin, int& c_A) {
+  // UNI: 1 / 0 when the caller is compiled for uniform / mixed shapes only
+  if (UNI == 1 || (UNI < 0 && P.ipl > 0)) {
+    if (!item_uniform<RPI>(L, P, pi, b, s, rb0)) return false;
+    // Read through the vector memory path (a zero offset the compiler cannot
+    // prove uniform): scalar loads complete out of order, so any later use of
+    // a kernel argument would wait for these, while vector loads are waited
+    // for in issue order, after the operand loads issued behind them.
+    const int z = (int)__builtin_amdgcn_mbcnt_lo(0u, 0u);
+    c_fin = L.ctrl[z].finished;
+    c_A = L.ctrl[z].A;
+    si = L.slot[s + z];
+    nrows = P.nr;
+    ncols = P.nc;
+    return true;
+  }
+  if (UNI == 1) return false;
+  if (!locate_item(L, P, b, s, rb0, si)) return false;   // (RPI == 1: mixed shapes)
+  c_fin = 0;
+  c_A = 0x7fffffff;
+  nrows = P.role ? si.m : si.n;
+  ncols = P.role ? si.n : si.m;
   return true;
 }
 
@@ -399,31 +456,39 @@ constexpr int mfma_min_blocks() {
                                         : (DH <= 8 ? 4 : 2));
 }
 
-template <int DH, int RT, int GW>
+// UNI: compiled for uniform lane shapes (work item -> slot by division) or
+// for mixed shapes (offsets table); the host launches the one that matches.
+template <int DH, int RT, int GW, bool UNI>
 __global__ __launch_bounds__(64 * (kGroups / GW), (mfma_min_blocks<DH, RT, GW>()))
 void k_update_mfma(Launch L) {
+  static_assert(UNI || RT == 1, "two row tiles per item need uniform lane shapes");
   constexpr int NW = kGroups / GW;
   constexpr int ROWS = 32 * RT;
   constexpr int DP = 2 * DH;
   __shared__ float2 sh_part[kGroups][2][ROWS];
   const int b = blockIdx.x;
   const int pi = b >= L.nb0;
-  const Pass P = pi ? L.p[1] : L.p[0];
-  int s, rb0;
+  const Pass P = L.p[pi];
+  int s, rb0, nrows, ncols, c_fin, c_A;
   SlotInfo si;
-  if (!locate_item<RT>(L, P, pi ? b - L.nb0 : b, s, rb0, si)) return;
+  if (!place_item<RT, UNI ? 1 : 0>(L, P, pi, pi ? b - L.nb0 : b, s, rb0, nrows, ncols, si, c_fin,
+                                   c_A))
+    return;
   const bool upd = P.kind == KIND_UPDATE;
   float rhat = NAN;
-  if (!upd && !check_facts(L, P, si, rhat)) return;
+  if (!upd) {
+    const bool chk = check_facts(L, P, s, P.role ? ncols : nrows, rhat);
+    if (UNI) behind(si, c_fin, c_A, rhat);
+    if (!item_live(L, P, s, si, c_fin, c_A) || !chk) return;
+  }
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform (SGPR)
   const int h = lane >> 5;
   const int r = lane & 31;
-  const int nrows = P.role ? si.m : si.n;
-  const int ncols = P.role ? si.n : si.m;
 
-  // Every load of the item (row data, first column tile) is issued before the
-  // update facts are reduced, so their latencies overlap.
+  // Every load of the item (row data, first column tile, the lane facts) is
+  // issued before the block waits on any of them -- with uniform lane shapes
+  // also before its slot record and the control block are checked.
   float lse_t[RT], bv[RT][DH + 1];
 #pragma unroll
   for (int q = 0; q < RT; ++q) {
@@ -437,10 +502,7 @@ void k_update_mfma(Launch L) {
   const int orow = rb0 * 32 + lane;
   const bool owner = wave == 0 && lane < ROWS && orow < nrows;
   float own_lm = 0.f, own_w = 0.f;
-  if (owner) {
-    own_lm = P.lm_row[(size_t)s * P.padr + orow];
-    own_w = P.w_row[(size_t)si.lane * P.w_ld + orow];
-  }
+  if (owner) own_lm = P.lm_row[(size_t)s * P.padr + orow];
 
   const int ct = (ncols + kColTile - 1) / kColTile;
   const int tpg = (ct + kGroups - 1) / kGroups;
@@ -460,7 +522,12 @@ void k_update_mfma(Launch L) {
 
   bool fast = false;
   float M = 0.f;
-  if (upd) update_facts(L, P, si, fast, M);
+  if (upd) {
+    update_facts(L, P, s, ncols, fast, M);
+    if (UNI) behind(si, c_fin, c_A, M);
+    if (!item_live(L, P, s, si, c_fin, c_A)) return;
+  }
+  if (owner) own_w = P.w_row[(size_t)si.lane * P.w_ld + orow];   // caller masses, by lane id
 #pragma unroll
   for (int q = 0; q < RT; ++q) {
     const bool live_q = (rb0 + q) * 32 + r < nrows && lse_t[q] != INFINITY;
@@ -586,16 +653,17 @@ void k_update_valu(Launch L) {
   const int b = blockIdx.x;
   const int pi = b >= L.nb0;
   const Pass P = pi ? L.p[1] : L.p[0];
-  int s, rb;
+  int s, rb, nrows, ncols, c_fin, c_A;
   SlotInfo si;
-  if (!locate_item<1>(L, P, pi ? b - L.nb0 : b, s, rb, si)) return;
+  if (!place_item<1>(L, P, pi, pi ? b - L.nb0 : b, s, rb, nrows, ncols, si, c_fin, c_A)) return;
   const bool upd = P.kind == KIND_UPDATE;
   float rhat = NAN;
-  if (!upd && !check_facts(L, P, si, rhat)) return;
+  if (!upd) {
+    const bool chk = check_facts(L, P, s, P.role ? ncols : nrows, rhat);
+    if (!item_live(L, P, s, si, c_fin, c_A) || !chk) return;
+  }
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform (SGPR)
-  const int nrows = P.role ? si.m : si.n;
-  const int ncols = P.role ? si.n : si.m;
   const int i = rb * kRowsValu + lane;
   constexpr int DP = 2 * DH;
   // row loads are issued before the update facts are reduced
@@ -604,17 +672,18 @@ void k_update_valu(Launch L) {
   const bool in_prefix = i < nrows;
   const bool owner = wave == 0 && in_prefix;
   float lm = 0.f, w = 0.f;
-  if (owner) {
-    lm = P.lm_row[ridx];
-    w = P.w_row[(size_t)si.lane * P.w_ld + i];
-  }
+  if (owner) lm = P.lm_row[ridx];
   float xr[D];
   const float* rrow = P.rec_row + ridx * DP;
 #pragma unroll
   for (int k = 0; k < D; ++k) xr[k] = rrow[k];
   bool fast = false;
   float M = 0.f;
-  if (upd) update_facts(L, P, si, fast, M);
+  if (upd) {
+    update_facts(L, P, s, ncols, fast, M);
+    if (!item_live(L, P, s, si, c_fin, c_A)) return;
+  }
+  if (owner) w = P.w_row[(size_t)si.lane * P.w_ld + i];   // caller masses, by lane id
   const bool live = in_prefix && (lse_old != INFINITY);
   float bias = 0.f;
   if (live) {
@@ -702,16 +771,17 @@ void k_update_f64(Launch L) {
   const int b = blockIdx.x;
   const int pi = b >= L.nb0;
   const Pass P = pi ? L.p[1] : L.p[0];
-  int s, rb;
+  int s, rb, nrows, ncols, c_fin, c_A;
   SlotInfo si;
-  if (!locate_item<1>(L, P, pi ? b - L.nb0 : b, s, rb, si)) return;
+  if (!place_item<1>(L, P, pi, pi ? b - L.nb0 : b, s, rb, nrows, ncols, si, c_fin, c_A)) return;
   const bool upd = P.kind == KIND_UPDATE;
   float rhat = NAN;
-  if (!upd && !check_facts(L, P, si, rhat)) return;
+  if (!upd) {
+    const bool chk = check_facts(L, P, s, P.role ? ncols : nrows, rhat);
+    if (!item_live(L, P, s, si, c_fin, c_A) || !chk) return;
+  }
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform (SGPR)
-  const int nrows = P.role ? si.m : si.n;
-  const int ncols = P.role ? si.n : si.m;
   const int i = rb * kRowsValu + lane;
   constexpr int DP = D + (D & 1);
   const size_t ridx = (size_t)s * P.padr + i;
@@ -720,17 +790,18 @@ void k_update_f64(Launch L) {
   const bool owner = wave == 0 && in_prefix;
   double lm = 0.0;
   float w = 0.f;
-  if (owner) {
-    lm = reinterpret_cast<const double*>(P.lm_row)[ridx];
-    w = P.w_row[(size_t)si.lane * P.w_ld + i];
-  }
+  if (owner) lm = reinterpret_cast<const double*>(P.lm_row)[ridx];
   double xr[D];
   const double* rrow = reinterpret_cast<const double*>(P.rec_row) + ridx * DP;
 #pragma unroll
   for (int k = 0; k < D; ++k) xr[k] = rrow[k];
   bool fast = false;
   float M = 0.f;
-  if (upd) update_facts(L, P, si, fast, M, kFastRangePrecise);
+  if (upd) {
+    update_facts(L, P, s, ncols, fast, M, kFastRangePrecise);
+    if (!item_live(L, P, s, si, c_fin, c_A)) return;
+  }
+  if (owner) w = P.w_row[(size_t)si.lane * P.w_ld + i];   // caller masses, by lane id
   const bool live = in_prefix && (lse_old != (double)INFINITY);
   double bias = 0.0;
   if (live) {
@@ -910,16 +981,17 @@ __global__ __launch_bounds__(512, 2) void k_mat_rows(Launch L) {
   const int b = blockIdx.x;
   const int pi = b >= L.nb0;
   const Pass P = pi ? L.p[1] : L.p[0];
-  int s, rb;
+  int s, rb, nrows, ncols, c_fin, c_A;
   SlotInfo si;
-  if (!locate_item<1>(L, P, pi ? b - L.nb0 : b, s, rb, si)) return;
+  if (!place_item<1>(L, P, pi, pi ? b - L.nb0 : b, s, rb, nrows, ncols, si, c_fin, c_A)) return;
   const bool upd = P.kind == KIND_UPDATE;
   float rhat = NAN;
-  if (!upd && !check_facts(L, P, si, rhat)) return;
+  if (!upd) {
+    const bool chk = check_facts(L, P, s, P.role ? ncols : nrows, rhat);
+    if (!item_live(L, P, s, si, c_fin, c_A) || !chk) return;
+  }
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int nrows = P.role ? si.m : si.n;
-  const int ncols = P.role ? si.n : si.m;
   const int nc4 = (ncols + 3) & ~3;
   // the column operand, padded to a multiple of 4 with dead columns
   const float* gcol = P.gam_col + (size_t)s * P.padc;
@@ -931,11 +1003,14 @@ __global__ __launch_bounds__(512, 2) void k_mat_rows(Launch L) {
     const size_t idx = (size_t)s * P.padr + i_own;
     lse_own = P.lse_in[idx];
     lm = P.lm_row[idx];
-    w = P.w_row[(size_t)si.lane * P.w_ld + i_own];
   }
   bool fast = false;
   float M = 0.f;
-  if (upd) update_facts(L, P, si, fast, M);
+  if (upd) {
+    update_facts(L, P, s, ncols, fast, M);
+    if (!item_live(L, P, s, si, c_fin, c_A)) return;
+  }
+  if (owner) w = P.w_row[(size_t)si.lane * P.w_ld + i_own];   // caller masses, by lane id
   __syncthreads();
   const float* Qt = L.Q + (size_t)si.lane * L.q_lane;
   for (int rr = wave; rr < kRowsValu; rr += 8) {
@@ -995,16 +1070,17 @@ __global__ __launch_bounds__(512, 2) void k_mat_cols(Launch L) {
   const int b = blockIdx.x;
   const int pi = b >= L.nb0;
   const Pass P = pi ? L.p[1] : L.p[0];
-  int s, rb;
+  int s, rb, nrows, ncols, c_fin, c_A;     // rows: target points, columns: source points
   SlotInfo si;
-  if (!locate_item<1>(L, P, pi ? b - L.nb0 : b, s, rb, si)) return;
+  if (!place_item<1>(L, P, pi, pi ? b - L.nb0 : b, s, rb, nrows, ncols, si, c_fin, c_A)) return;
   const bool upd = P.kind == KIND_UPDATE;
   float rhat = NAN;
-  if (!upd && !check_facts(L, P, si, rhat)) return;
+  if (!upd) {
+    const bool chk = check_facts(L, P, s, P.role ? ncols : nrows, rhat);
+    if (!item_live(L, P, s, si, c_fin, c_A) || !chk) return;
+  }
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int nrows = P.role ? si.m : si.n;   // target points (this kernel's rows)
-  const int ncols = P.role ? si.n : si.m;   // source points
   const float* gcol = P.gam_col + (size_t)s * P.padc;
   for (int i = threadIdx.x; i < ncols; i += blockDim.x) sh_gam[i] = gcol[i];
   const int j = rb * kRowsValu + lane;
@@ -1013,13 +1089,14 @@ __global__ __launch_bounds__(512, 2) void k_mat_cols(Launch L) {
   const float lse_old = P.lse_in[jdx];
   const bool owner = wave == 0 && in_prefix;
   float lm = 0.f, w = 0.f;
-  if (owner) {
-    lm = P.lm_row[jdx];
-    w = P.w_row[(size_t)si.lane * P.w_ld + j];
-  }
+  if (owner) lm = P.lm_row[jdx];
   bool fast = false;
   float M = 0.f;
-  if (upd) update_facts(L, P, si, fast, M);
+  if (upd) {
+    update_facts(L, P, s, ncols, fast, M);
+    if (!item_live(L, P, s, si, c_fin, c_A)) return;
+  }
+  if (owner) w = P.w_row[(size_t)si.lane * P.w_ld + j];   // caller masses, by lane id
   const bool live = in_prefix && lse_old != INFINITY;
   float bias = 0.f;
   if (live) {
@@ -1258,9 +1335,17 @@ __global__ __launch_bounds__(256) void k_move(MoveArgs p) {
       const int q0 = c0 * p.dp * es / 4, q1 = lim * p.dp * es / 4;
       for (int q = q0 + threadIdx.x; q < q1; q += blockDim.x) rd[q] = rs[q];
     }
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
-      p.dst.slot[ns] = si;
-      p.dst.dec[ns] = d;
+    if (blockIdx.x == 0) {
+      // the row-block aggregates follow the lane (the next f-half reads the
+      // g-half's ones as its bound)
+      for (int q = threadIdx.x; q < 4 * p.rbmax; q += blockDim.x) {
+        const int a = q / p.rbmax, e = q - a * p.rbmax;
+        p.dst.agg[a][(size_t)ns * p.rbmax + e] = p.src.agg[a][(size_t)s * p.rbmax + e];
+      }
+      if (threadIdx.x == 0) {
+        p.dst.slot[ns] = si;
+        p.dst.dec[ns] = d;
+      }
     }
   }
 }
@@ -1341,7 +1426,7 @@ __global__ __launch_bounds__(256) void k_ingest_lanes(IngestArgs p) {
   // no previous half-step: the first update of each side runs unanchored
   const float4 none = make_float4(0.f, INFINITY, -INFINITY, 1.f);
   for (int q = threadIdx.x; q < p.rbmax; q += blockDim.x)
-    for (int k = 0; k < 4; ++k) p.agg[k][(size_t)t * p.rbmax + q] = none;
+    for (int k = 0; k < 4; ++k) p.bank.agg[k][(size_t)t * p.rbmax + q] = none;
 }
 
 // Grid (chunks, W): points of both sides of lane t.
@@ -1463,10 +1548,18 @@ __global__ void k_ctrl_init(Ctrl* c, int W) {
 template <int DH>
 static hipError_t launch_mfma_dh(const Launch& a, int variant, int blocks, hipStream_t st,
                                  hipEvent_t e0, hipEvent_t e1) {
-  switch (variant) {
-    case VAR_NARROW: hipExtLaunchKernelGGL((k_update_mfma<DH, 1, 1>), dim3(blocks), dim3(512), 0, st, e0, e1, 0, a); break;
-    case VAR_MEDIUM: hipExtLaunchKernelGGL((k_update_mfma<DH, 1, 2>), dim3(blocks), dim3(256), 0, st, e0, e1, 0, a); break;
-    default: hipExtLaunchKernelGGL((k_update_mfma<DH, 2, 2>), dim3(blocks), dim3(256), 0, st, e0, e1, 0, a); break;
+  const bool uni = a.p[0].ipl > 0;   // both passes of a launch share the shapes
+  if (variant == VAR_WIDE && !uni) return hipErrorInvalidValue;
+  if (uni) {
+    switch (variant) {
+      case VAR_NARROW: hipExtLaunchKernelGGL((k_update_mfma<DH, 1, 1, true>), dim3(blocks), dim3(512), 0, st, e0, e1, 0, a); break;
+      case VAR_MEDIUM: hipExtLaunchKernelGGL((k_update_mfma<DH, 1, 2, true>), dim3(blocks), dim3(256), 0, st, e0, e1, 0, a); break;
+      default: hipExtLaunchKernelGGL((k_update_mfma<DH, 2, 2, true>), dim3(blocks), dim3(256), 0, st, e0, e1, 0, a); break;
+    }
+  } else if (variant == VAR_NARROW) {
+    hipExtLaunchKernelGGL((k_update_mfma<DH, 1, 1, false>), dim3(blocks), dim3(512), 0, st, e0, e1, 0, a);
+  } else {
+    hipExtLaunchKernelGGL((k_update_mfma<DH, 1, 2, false>), dim3(blocks), dim3(256), 0, st, e0, e1, 0, a);
   }
   return hipGetLastError();
 }

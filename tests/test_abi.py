@@ -28,7 +28,7 @@ def test_library_exports_every_declared_function():
                           "ds_last_error_message"}
     for nm in names:
         assert hasattr(lib, nm), nm
-    assert lib.ds_api_version() == 1
+    assert lib.ds_api_version() == 2
     for code in range(6):
         assert lib.ds_error_string(code).decode()
 
@@ -114,3 +114,26 @@ def test_solve_rejects_bad_arguments_before_device_work():
     assert lib.ds_solve(ctypes.byref(pr), ctypes.byref(op), ctypes.byref(res),
                         ctypes.c_void_p(0x1000), 16, None, None) == 2
     assert "workspace" in lib.ds_last_error_message().decode()
+
+
+def test_sub_batch_validation_and_size():
+    """streams is 0 (automatic) .. 4; more than one sub-batch needs the active
+    mode; the workspace of a split window holds one part per sub-batch, each
+    sized like a window of its own lanes."""
+    lib = ds.load_library()
+    for s in (-1, 5):
+        assert _bytes(_problem(W=64), ds._options(1e-3, None, 100, 1, "active", 0, s))[0] == 1
+    for mode in ("static", "logical"):
+        assert _bytes(_problem(W=64), ds._options(1e-3, None, 100, 1, mode, 0, 2))[0] == 1
+        assert _bytes(_problem(W=64), ds._options(1e-3, None, 100, 1, mode, 0, 1))[0] == 0
+    _bytes(_problem(W=64), ds._options(1e-3, None, 100, 1, "static", 0, 2))
+    assert "active mode" in lib.ds_last_error_message().decode()
+    one = _bytes(_problem(W=64), ds._options(1e-3, None, 100, 1, "active", 0, 1))[1]
+    parts = [_bytes(_problem(W=w), ds._options(1e-3, None, 100, 1, "active", 0, 1))[1]
+             for w in (21, 21, 22)]
+    three = _bytes(_problem(W=64), ds._options(1e-3, None, 100, 1, "active", 0, 3))[1]
+    assert three == sum(parts) and three >= one
+    # automatic: three sub-batches from 48 lanes, two from 32, one below
+    auto = lambda W: _bytes(_problem(W=W), ds._options(1e-3, None, 100, 1, "active", 0, 0))[1]
+    for W, k in ((64, 3), (40, 2), (16, 1)):
+        assert auto(W) == _bytes(_problem(W=W), ds._options(1e-3, None, 100, 1, "active", 0, k))[1]
