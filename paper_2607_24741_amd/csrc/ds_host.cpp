@@ -155,15 +155,13 @@ ds_err check_problem(const ds_problem* pr, const ds_options* op) {
 
 // Host resources of one sub-batch solve, kept for the life of the process in a
 // per-device pool (a call takes one per sub-batch and returns them at its end):
-// a pinned control snapshot, run-ahead events, timing events, and a stream of
+// a pinned control snapshot, a join event, timing events, and a stream of
 // its own (default priority, not synchronising with the legacy default stream)
 // for sub-batches beyond the first.
-constexpr int kRing = 16;
 struct DeviceRes {
   bool busy = false;
   ds::HostSnap* snap = nullptr;      // pinned, device-written control mirror (host view)
   ds::HostSnap* snap_dev = nullptr;  // the same memory as the device addresses it
-  hipEvent_t ring_ev[kRing];
   hipEvent_t join_ev = nullptr;      // end of this sub-batch's work on its stream
   hipStream_t stream = nullptr;
   std::vector<hipEvent_t> timing;
@@ -186,10 +184,6 @@ hipError_t acquire_res(DeviceRes** out) {
   if (e != hipSuccess) return e;
   e = hipHostGetDevicePointer(reinterpret_cast<void**>(&r->snap_dev), r->snap, 0);
   if (e != hipSuccess) return e;
-  for (int i = 0; i < kRing; ++i) {
-    e = hipEventCreateWithFlags(&r->ring_ev[i], hipEventDisableTiming);
-    if (e != hipSuccess) return e;
-  }
   e = hipEventCreateWithFlags(&r->join_ev, hipEventDisableTiming);
   if (e != hipSuccess) return e;
   e = hipStreamCreateWithFlags(&r->stream, hipStreamNonBlocking);
@@ -372,7 +366,9 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
     const int lanes_ub = (items + ipl[role] - 1) / ipl[role];
     return lanes_ub * ((ipl[role] + 1) / 2);
   };
+  int seqno = 0;   // update launches issued (see HostSnap::progress)
   auto run = [&](Launch l, int variant, int blocks, bool sample, int cycle, int kind) -> ds_err {
+    l.seqno = ++seqno;
     const bool timed = tm.on && sample && (int)timed_launches.size() < kMaxTimed;
     // the events are part of the kernel's own dispatch: they time the kernel,
     // not the queue around it
@@ -391,13 +387,11 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
   // ------------------------------------------------------------ main loop
   const int max_iter = op->max_iter, ae = op->audit_every;
   const int kLag = 8;          // cycles the host may run ahead of the device
-  const int kEvery = 4;        // cycles between run-ahead events
   volatile HostSnap* hs = R->snap;
   hs->n_active = W; hs->n_retired = 0; hs->compacted = 0; hs->epoch = 0; hs->finished = 0;
   hs->items_act_f = items[0]; hs->items_act_g = items[1];
-  struct Pending { int idx, cycle; };
-  std::vector<Pending> q;
-  int ring_next = 0, epoch = 0;
+  hs->progress = 0;
+  int epoch = 0;
   bool finished = false;
   int launched = 0;
   int compactions = 0;
@@ -406,9 +400,16 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
                              (int64_t)(sizeof(SlotInfo) + sizeof(Decision));
   for (int k = 1; k <= max_iter; ++k) {
     // bounded run-ahead: wait for the device only when too far behind
-    while (!q.empty() && q.front().cycle <= k - kLag) {
-      HIP_TRY(hipEventSynchronize(R->ring_ev[q.front().idx]));
-      q.erase(q.begin());
+    // (block 0 of every update launch publishes the launch's sequence
+    // number; the stream is polled now and then so a failed launch surfaces
+    // as an error instead of a wait that never ends)
+    for (int spin = 0; seqno - hs->progress > 2 * kLag; ++spin) {
+      if ((spin & 1023) == 1023) {
+        const hipError_t qe = hipStreamQuery(st);
+        if (qe == hipSuccess) break;                  // idle: nothing left to wait for
+        if (qe != hipErrorNotReady) HIP_TRY(qe);
+      }
+      std::this_thread::yield();
     }
     const int s_fin = hs->finished, s_ep = hs->epoch, s_ret = hs->n_retired;
     const int s_cmp = hs->compacted, s_act = hs->n_active;
@@ -474,12 +475,6 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
     r = run(lg, vg, blocks, sample, k, 0);
     if (r != DS_OK) return r;
     launched = k;
-    if (k % kEvery == 0) {
-      const int idx = ring_next;
-      ring_next = (ring_next + 1) % kRing;
-      HIP_TRY(hipEventRecord(R->ring_ev[idx], st));
-      q.push_back({idx, k});
-    }
   }
   HIP_TRY(hipMemcpyAsync(&ctrl, L.ctrl, sizeof(Ctrl), hipMemcpyDeviceToHost, st));
   HIP_TRY(hipStreamSynchronize(st));

@@ -79,8 +79,11 @@ struct Ctrl {
 
 // Best-effort mirror of the control counters in pinned host memory, written
 // by the device with system-scope stores (no copy on the stream).
+// `progress`: sequence number of the latest update launch that has started on
+// the device (its block 0 writes it first thing), so every earlier launch of
+// the stream has completed.
 struct HostSnap {
-  int n_active, n_retired, compacted, epoch, finished, items_act_f, items_act_g, pad;
+  int n_active, n_retired, compacted, epoch, finished, items_act_f, items_act_g, progress;
 };
 
 // Per slot audit scratch (indexed by the slot at audit time).
@@ -186,6 +189,7 @@ struct Launch {
   const float* Q;                 // materialised cost (caller lane l at Q + l * q_lane)
   size_t q_lane;                  // floats per lane
   int q_ld;                       // row stride of Q (padded target count)
+  int seqno;                      // launch sequence number (progress mirror)
 };
 
 struct ScanArgs {          // compaction map over the slots of the current bank

@@ -64,6 +64,11 @@ __device__ __forceinline__ float2 ld_dev2(const float2* p) {
 __device__ __forceinline__ void st_sys(int* p, int v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
 }
+// Block 0 of an update launch publishes the launch's sequence number to the
+// host before anything else: every earlier launch of the stream has completed.
+__device__ __forceinline__ void note_progress(const Launch& L) {
+  if (blockIdx.x == 0 && threadIdx.x == 0 && L.hsnap) st_sys(&L.hsnap->progress, L.seqno);
+}
 // all of this wave's outstanding memory operations have completed
 __device__ __forceinline__ void wait_mem() { __builtin_amdgcn_s_waitcnt(0); }
 __device__ __forceinline__ float lg2(float x) { return __builtin_amdgcn_logf(x); }
@@ -461,6 +466,7 @@ constexpr int mfma_min_blocks() {
 template <int DH, int RT, int GW, bool UNI>
 __global__ __launch_bounds__(64 * (kGroups / GW), (mfma_min_blocks<DH, RT, GW>()))
 void k_update_mfma(Launch L) {
+  note_progress(L);
   static_assert(UNI || RT == 1, "two row tiles per item need uniform lane shapes");
   constexpr int NW = kGroups / GW;
   constexpr int ROWS = 32 * RT;
@@ -649,6 +655,7 @@ void k_update_mfma(Launch L) {
 template <int D, int DH, int GW>
 __global__ __launch_bounds__(64 * (kGroups / GW), (kGroups / GW == 8 ? 4 : 8))
 void k_update_valu(Launch L) {
+  note_progress(L);
   __shared__ float2 sh_part[kGroups][kRowsValu];
   const int b = blockIdx.x;
   const int pi = b >= L.nb0;
@@ -765,6 +772,7 @@ void k_update_valu(Launch L) {
 template <int D, int GW>
 __global__ __launch_bounds__(64 * (kGroups / GW), (kGroups / GW == 8 ? 2 : 4))
 void k_update_f64(Launch L) {
+  note_progress(L);
   constexpr int DPc = D + (D & 1);
   __shared__ double2 sh_part[kGroups][kRowsValu];
   __shared__ __align__(16) double sh_tile[kGroups / GW][2][kColTile * DPc + kColTile];
@@ -976,6 +984,7 @@ __global__ __launch_bounds__(256) void k_cost(CostArgs c) {
 // f-half (and the final row check): wave w sweeps rows w, w+8, .. of the
 // item, its lanes striding over the columns four at a time.
 __global__ __launch_bounds__(512, 2) void k_mat_rows(Launch L) {
+  note_progress(L);
   __shared__ __align__(16) float sh_gam[kMatMaxPts];
   __shared__ float2 sh_row[kRowsValu];
   const int b = blockIdx.x;
@@ -1065,6 +1074,7 @@ __global__ __launch_bounds__(512, 2) void k_mat_rows(Launch L) {
 // (a column of Q); the eight waves split the source points into contiguous
 // chunks, merged per lane in chunk order.
 __global__ __launch_bounds__(512, 2) void k_mat_cols(Launch L) {
+  note_progress(L);
   __shared__ float sh_gam[kMatMaxPts];
   __shared__ float2 sh_part[8][kRowsValu];
   const int b = blockIdx.x;
