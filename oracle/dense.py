@@ -13,10 +13,11 @@ from __future__ import annotations
 import numpy as np
 
 
-def dense_scaling_lane(x, y, a, b, eps, tol, *, max_iter=5000, audit_every=1):
+def dense_scaling_lane(x, y, a, b, eps, tol, *, max_iter=5000, audit_every=1, v0=None):
     """Returns f = eps log u, g = eps log v, depth, row/col residuals, status.
 
-    Status codes are the oracle's: 0 converged, 1 max-iter.
+    Status codes are the oracle's: 0 converged, 1 max-iter. ``v0`` is the
+    starting column scaling (a proposal; default v = 1).
     """
     x = np.asarray(x, dtype=np.float64)
     y = np.asarray(y, dtype=np.float64)
@@ -31,7 +32,7 @@ def dense_scaling_lane(x, y, a, b, eps, tol, *, max_iter=5000, audit_every=1):
     if C.max() / eps > 600.0:
         raise ValueError("dense scaling would underflow; use a smaller C/eps")
     K = np.exp(-C / eps)
-    v = np.ones(m)
+    v = np.ones(m) if v0 is None else np.asarray(v0, dtype=np.float64).copy()
     u = np.ones(n)
     status, depth = 1, max_iter
     r_row = r_col = np.nan

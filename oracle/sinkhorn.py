@@ -90,8 +90,9 @@ def dual_objective(C, f, g, a, b, eps):
 
 # --------------------------------------------------------------------- one lane
 def solve_lane(x, y, a, b, eps, tol, *, max_iter=5000, audit_every=1,
-               fixed_iters=None, precision="f64", history=False):
-    """Solve one lane from a cold start and stop on the two-sided audit.
+               fixed_iters=None, precision="f64", history=False, g0=None):
+    """Solve one lane from a proposal (cold by default) and stop on the
+    two-sided audit.
 
     Readings taken (each listed in the design doc):
       * cold proposal f = g = 0 (all formal runs use cold proposals, Sec. 5 /
@@ -107,7 +108,11 @@ def solve_lane(x, y, a, b, eps, tol, *, max_iter=5000, audit_every=1,
       * a non-finite residual at an audit ends the lane with NONFINITE; a lane
         still failing at max_iter ends with MAX_ITER (no sequential fallback);
       * a zero mass a_i = 0 (b_j = 0) removes that point from the problem and
-        its output potential is written 0.
+        its output potential is written 0;
+      * ``g0`` (length m) is a proposal (Sec. 2: carried or warm-started dual
+        potentials): the iteration starts from g = g0 instead of the cold
+        g = 0. Because f is updated first, only the target potential of a
+        proposal enters the trajectory.
 
     ``fixed_iters=k`` runs exactly k cycles with no stopping test and reports
     the residual of the final state (fixed-work parity, Sec. 3.2).
@@ -145,6 +150,8 @@ def solve_lane(x, y, a, b, eps, tol, *, max_iter=5000, audit_every=1,
 
     f = np.zeros(xs.shape[0], dtype=dt)
     g = np.zeros(ys.shape[0], dtype=dt)
+    if g0 is not None:
+        g = np.asarray(g0, dtype=np.float64)[col_live].astype(dt)
     hist = []
     status, depth = MAX_ITER, 0
     r_row = r_col = np.nan
@@ -194,7 +201,7 @@ def _lane_job(args):
 
 def solve(X, Y, a, b, eps, tol, *, n=None, m=None, max_iter=5000, audit_every=1,
           fixed_iters=None, precision="f64", history=False, lanes=None,
-          processes=None):
+          processes=None, g0=None):
     """Solve a window of W independent lanes (candidate-axis packing).
 
     eq:pack-commutes (Sec. 3.1): the packed map equals the per-lane maps applied
@@ -203,6 +210,7 @@ def solve(X, Y, a, b, eps, tol, *, n=None, m=None, max_iter=5000, audit_every=1,
     lane's valid prefix (default: full). ``lanes`` restricts the run to a subset
     of lane indices (outputs of other lanes stay zero / depth 0).
     ``processes`` > 1 spreads lanes over a process pool (largest first).
+    ``g0`` [W, m_max] is an optional proposal (initial target potentials).
 
     Returns f [W, n_max], g [W, m_max] (zero beyond each lane's prefix), depth,
     residual, row_residual, col_residual, status [W], and ``order``: lane
@@ -221,7 +229,8 @@ def solve(X, Y, a, b, eps, tol, *, n=None, m=None, max_iter=5000, audit_every=1,
     lanes = list(range(W)) if lanes is None else [int(t) for t in lanes]
     kw = dict(max_iter=max_iter, audit_every=audit_every, fixed_iters=fixed_iters,
               precision=precision, history=history)
-    jobs = [((X[t, :n[t]], Y[t, :m[t]], a[t, :n[t]], b[t, :m[t]], eps[t], tol), kw)
+    jobs = [((X[t, :n[t]], Y[t, :m[t]], a[t, :n[t]], b[t, :m[t]], eps[t], tol),
+             dict(kw, g0=None if g0 is None else np.asarray(g0)[t, :m[t]]))
             for t in lanes]
     if processes is not None and processes > 1 and len(jobs) > 1:
         import multiprocessing as mp

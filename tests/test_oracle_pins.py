@@ -336,6 +336,82 @@ def test_column_marginal_is_current_at_every_audit():
         assert rr >= 0
 
 
+# ---------------------------------------------------------------- proposals
+def test_cold_proposal_is_the_zero_proposal():
+    rng = np.random.default_rng(21)
+    x, y, a, b = _lane(rng, 9, 7, 2)
+    cold = oracle.solve_lane(x, y, a, b, 0.25, 1e-7)
+    zero = oracle.solve_lane(x, y, a, b, 0.25, 1e-7, g0=np.zeros(7))
+    for k in ("f", "g"):
+        assert np.array_equal(cold[k], zero[k])
+    assert cold["depth"] == zero["depth"] and cold["residual"] == zero["residual"]
+
+
+@pytest.mark.parametrize("audit", [1, 3])
+def test_proposal_matches_dense_scaling_from_v0(audit):
+    """A proposal g0 is the starting scaling v = exp(g0 / eps) of the printed
+    multiplicative iteration (eq:sinkhorn-cycle): same depth, same potentials."""
+    rng = np.random.default_rng(22 + audit)
+    x, y, a, b = _lane(rng, 8, 11, 2)
+    eps, tol = 0.4, 1e-7
+    g0 = 0.3 * rng.standard_normal(11)
+    ref = oracle.dense_scaling_lane(x, y, a, b, eps, tol, audit_every=audit, v0=np.exp(g0 / eps))
+    got = oracle.solve_lane(x, y, a, b, eps, tol, audit_every=audit, g0=g0)
+    cold = oracle.solve_lane(x, y, a, b, eps, tol, audit_every=audit)
+    assert got["depth"] == ref["depth"] and got["status"] == ref["status"] == oracle.CONVERGED
+    scale = max(np.abs(ref["f"]).max(), np.abs(ref["g"]).max(), eps)
+    np.testing.assert_allclose(got["f"], ref["f"], rtol=0, atol=1e-10 * scale)
+    np.testing.assert_allclose(got["g"], ref["g"], rtol=0, atol=1e-10 * scale)
+    # the proposal really changed the trajectory
+    assert np.abs(got["f"] - cold["f"]).max() > 1e-9
+
+
+def test_proposal_continues_the_cold_trajectory():
+    """The iteration is a map on g: starting from the cold run's g after k
+    cycles reproduces that run from cycle k + 1 on, bit for bit, and the
+    stopping depth drops by exactly k (Sec. 2: a carried proposal shortens the
+    completion depth)."""
+    rng = np.random.default_rng(24)
+    x, y, a, b = _lane(rng, 10, 9, 3)
+    eps, tol = 0.3, 1e-8
+    cold = oracle.solve_lane(x, y, a, b, eps, tol)
+    k = cold["depth"] // 3
+    assert k >= 2
+    mid = oracle.solve_lane(x, y, a, b, eps, tol, fixed_iters=k)
+    warm = oracle.solve_lane(x, y, a, b, eps, tol, g0=mid["g"])
+    assert warm["depth"] == cold["depth"] - k
+    assert np.array_equal(warm["f"], cold["f"]) and np.array_equal(warm["g"], cold["g"])
+    assert warm["residual"] == cold["residual"]
+
+
+def test_proposal_gauge_shift_moves_only_the_potentials():
+    """(f, g) -> (f - c, g + c) leaves pi unchanged (Sec. 4.2): a proposal
+    shifted by c yields the same depth and residuals and potentials shifted by
+    exactly that gauge."""
+    rng = np.random.default_rng(25)
+    x, y, a, b = _lane(rng, 12, 8, 2)
+    eps, tol, c = 0.35, 1e-8, 0.73
+    mid = oracle.solve_lane(x, y, a, b, eps, tol, fixed_iters=4)
+    base = oracle.solve_lane(x, y, a, b, eps, tol, g0=mid["g"])
+    shift = oracle.solve_lane(x, y, a, b, eps, tol, g0=mid["g"] + c)
+    assert shift["depth"] == base["depth"]
+    np.testing.assert_allclose(shift["f"], base["f"] - c, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(shift["g"], base["g"] + c, rtol=0, atol=1e-12)
+    assert abs(shift["residual"] - base["residual"]) < 1e-14
+
+
+def test_batch_proposal_reaches_each_lane():
+    rng = np.random.default_rng(26)
+    lanes = [_lane(rng, 6, 5, 2) for _ in range(3)]
+    X = np.stack([l[0] for l in lanes]); Y = np.stack([l[1] for l in lanes])
+    A = np.stack([l[2] for l in lanes]); B = np.stack([l[3] for l in lanes])
+    G0 = 0.2 * rng.standard_normal((3, 5))
+    out = oracle.solve(X, Y, A, B, [0.3, 0.4, 0.5], 1e-7, g0=G0)
+    for t in range(3):
+        one = oracle.solve_lane(X[t], Y[t], A[t], B[t], [0.3, 0.4, 0.5][t], 1e-7, g0=G0[t])
+        assert np.array_equal(out["f"][t], one["f"]) and out["depth"][t] == one["depth"]
+
+
 # ------------------------------------------------------------- edge semantics
 def test_zero_mass_point_behaves_like_padding():
     rng = np.random.default_rng(14)
