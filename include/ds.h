@@ -105,6 +105,12 @@ typedef struct {
   const float* eps;     /* [W] entropic regularisation, finite and > 0             */
   const int32_t* n;     /* [W] valid prefix sizes 1..n_max; NULL => all n_max      */
   const int32_t* m;     /* [W] valid prefix sizes 1..m_max; NULL => all m_max      */
+  const float* g0;      /* [W, m_max] proposal: initial target potential g^0 in the
+                           output convention (a warm start or a carried solution,
+                           Sec. 2); NULL => the cold proposal g^0 = 0. f is updated
+                           first, so a proposal's source potential never enters
+                           the trajectory. A non-finite entry on a live point
+                           makes that lane NONFINITE at its first audit.        */
 } ds_problem;
 /* Points beyond a lane's prefix are never read. A zero mass on the valid prefix
  * removes that point from the problem (its output potential is 0). A negative

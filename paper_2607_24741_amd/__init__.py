@@ -47,7 +47,7 @@ class _Problem(ctypes.Structure):
     _fields_ = [("W", ctypes.c_int32), ("n_max", ctypes.c_int32), ("m_max", ctypes.c_int32),
                 ("d", ctypes.c_int32), ("X", ctypes.c_void_p), ("Y", ctypes.c_void_p),
                 ("a", ctypes.c_void_p), ("b", ctypes.c_void_p), ("eps", ctypes.c_void_p),
-                ("n", ctypes.c_void_p), ("m", ctypes.c_void_p)]
+                ("n", ctypes.c_void_p), ("m", ctypes.c_void_p), ("g0", ctypes.c_void_p)]
 
 
 class _Options(ctypes.Structure):
@@ -169,13 +169,15 @@ def _ptr(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
-def solve(X, Y, a, b, eps, tol, *, n=None, m=None, max_iter=5000, audit_every=1,
+def solve(X, Y, a, b, eps, tol, *, n=None, m=None, g0=None, max_iter=5000, audit_every=1,
           mode="active", screen_tol=None, flags=0, streams=0, return_stats=False,
           workspace=None, trace_len=0, out=None):
     """Solve W independent entropic OT problems on the current GPU.
 
     X [W, n_max, d], Y [W, m_max, d], a [W, n_max], b [W, m_max], eps [W]:
-    contiguous float32 CUDA tensors; n, m optional int32 [W] valid prefixes.
+    contiguous float32 CUDA tensors; n, m optional int32 [W] valid prefixes;
+    g0 an optional float32 [W, m_max] proposal (initial target potential;
+    default: the cold proposal g^0 = 0).
     Returns (f, g, depth, residual, status, order) and, with
     ``return_stats=True``, a Stats record as well. ``workspace`` may be a
     pre-allocated uint8 CUDA tensor of at least ``workspace_bytes(...)``.
@@ -188,7 +190,9 @@ def solve(X, Y, a, b, eps, tol, *, n=None, m=None, max_iter=5000, audit_every=1,
     if dev.type != "cuda":
         raise ValueError("inputs must be CUDA (HIP) tensors")
     for name, t, shape in (("X", X, (W, n_max, d)), ("Y", Y, (W, m_max, d)), ("a", a, (W, n_max)),
-                           ("b", b, (W, m_max)), ("eps", eps, (W,))):
+                           ("b", b, (W, m_max)), ("eps", eps, (W,)), ("g0", g0, (W, m_max))):
+        if t is None and name == "g0":
+            continue
         if t.dtype != torch.float32 or not t.is_contiguous() or t.device != dev:
             raise ValueError(f"{name} must be a contiguous float32 tensor on {dev}")
         if tuple(t.shape) != shape:
@@ -198,7 +202,7 @@ def solve(X, Y, a, b, eps, tol, *, n=None, m=None, max_iter=5000, audit_every=1,
                               or tuple(t.shape) != (W,)):
             raise ValueError(f"{name} must be a contiguous int32 tensor of shape ({W},) on {dev}")
     pr = _Problem(W=W, n_max=n_max, m_max=m_max, d=d, X=_ptr(X), Y=_ptr(Y), a=_ptr(a),
-                  b=_ptr(b), eps=_ptr(eps), n=_ptr(n), m=_ptr(m))
+                  b=_ptr(b), eps=_ptr(eps), n=_ptr(n), m=_ptr(m), g0=_ptr(g0))
     op = _options(tol, screen_tol, max_iter, audit_every, mode, flags, streams)
     need = ctypes.c_size_t(0)
     _check(lib, lib.ds_workspace_bytes(ctypes.byref(pr), ctypes.byref(op), ctypes.byref(need)))

@@ -265,7 +265,7 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
   // ---------------------------------------------------------------- ingest
   IngestArgs ia;
   std::memset(&ia, 0, sizeof(ia));
-  ia.X = pr->X; ia.Y = pr->Y; ia.a = pr->a; ia.b = pr->b; ia.eps = pr->eps;
+  ia.X = pr->X; ia.Y = pr->Y; ia.a = pr->a; ia.b = pr->b; ia.eps = pr->eps; ia.g0 = pr->g0;
   ia.n = pr->n; ia.m = pr->m;
   ia.W = W; ia.n_max = pr->n_max; ia.m_max = pr->m_max; ia.d = d; ia.dp = L.dp; ia.dh = L.dh;
   ia.pad[0] = L.pad[0]; ia.pad[1] = L.pad[1];
@@ -562,6 +562,7 @@ ds_problem sub_problem(const ds_problem* pr, int lo, int hi) {
   s.eps = pr->eps + lo;
   s.n = pr->n ? pr->n + lo : nullptr;
   s.m = pr->m ? pr->m + lo : nullptr;
+  s.g0 = pr->g0 ? pr->g0 + (size_t)lo * pr->m_max : nullptr;
   return s;
 }
 ds_result sub_result(const ds_problem* pr, const ds_result* res, int lo) {

@@ -220,6 +220,7 @@ struct MoveArgs {
 
 struct IngestArgs {
   const float* X; const float* Y; const float* a; const float* b; const float* eps;
+  const float* g0;        // proposal g^0 [W][m_max] (null: cold start)
   const int* n; const int* m;
   int W, n_max, m_max, d, dp, dh;
   int pad[2];

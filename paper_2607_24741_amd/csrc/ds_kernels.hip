@@ -1458,8 +1458,11 @@ __global__ __launch_bounds__(256) void k_ingest_points(IngestArgs p, int chunk) 
       const float mass = (q < cnt) ? w[(size_t)t * ld + q] : 0.f;
       const bool live = (q < cnt) && (mass != 0.f);
       const double lm = live ? log2((double)mass) : -(double)INFINITY;
+      // proposal g^0 (0: cold start), in base-2 units: kappa g^0
+      const double kg0 = (side == 1 && live && p.g0) ? si.kappa64 * (double)p.g0[(size_t)t * ld + q]
+                                                     : 0.0;
       if (p.mat) {
-        // no point records; gam = kappa * potential, cold start g^0 = 0
+        // no point records; gam = kappa * potential, starting from g^0
         p.bank.lm[side][idx] = (float)lm;
         for (int par = 0; par < 2; ++par) {
           if (!live) {
@@ -1469,8 +1472,8 @@ __global__ __launch_bounds__(256) void k_ingest_points(IngestArgs p, int chunk) 
             p.bank.lse[0][par][idx] = NAN;
             p.bank.gam[0][par][idx] = NAN;
           } else {
-            p.bank.gam[1][par][idx] = 0.f;
-            p.bank.lse[1][par][idx] = (float)lm;
+            p.bank.gam[1][par][idx] = (float)kg0;
+            p.bank.lse[1][par][idx] = (float)(lm - kg0);
           }
         }
         continue;
@@ -1497,8 +1500,8 @@ __global__ __launch_bounds__(256) void k_ingest_points(IngestArgs p, int chunk) 
             lse[idx] = (double)NAN;   // no f^0: the first f-half runs unanchored
             gam[idx] = (double)NAN;
           } else {
-            gam[idx] = -0.5 * nrm;    // cold start g^0 = 0
-            lse[idx] = lm + 0.5 * nrm;
+            gam[idx] = kg0 - 0.5 * nrm;   // kappa (g^0 - |y - c|^2)
+            lse[idx] = lm - gam[idx];
           }
         }
         continue;
@@ -1528,8 +1531,8 @@ __global__ __launch_bounds__(256) void k_ingest_points(IngestArgs p, int chunk) 
           p.bank.lse[0][par][idx] = NAN;
           p.bank.gam[0][par][idx] = NAN;
         } else {
-          // cold start g^0 = 0  =>  gam^y = -kappa |y - c|^2 = -|y~|^2 / 2
-          const float gam0 = -0.5f * nrm;
+          // gam^y = kappa (g^0 - |y - c|^2) = kappa g^0 - |y~|^2 / 2 (cold start: g^0 = 0)
+          const float gam0 = p.g0 ? (float)(kg0 - 0.5 * (double)nrm) : -0.5f * nrm;
           p.bank.gam[1][par][idx] = gam0;
           p.bank.lse[1][par][idx] = (float)lm - gam0;
         }

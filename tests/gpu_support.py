@@ -45,7 +45,9 @@ def procs():
 def to_device(w, device="cuda:0"):
     import torch
     t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(device)
-    return dict(X=t(w.X), Y=t(w.Y), a=t(w.a), b=t(w.b), eps=t(w.eps), n=t(w.n), m=t(w.m))
+    g0 = getattr(w, "g0", None)   # optional proposal [W, m_max] float32
+    return dict(X=t(w.X), Y=t(w.Y), a=t(w.a), b=t(w.b), eps=t(w.eps), n=t(w.n), m=t(w.m),
+                g0=None if g0 is None else t(g0))
 
 
 def run_gpu(w, tol, *, device="cuda:0", **kw):
@@ -53,7 +55,7 @@ def run_gpu(w, tol, *, device="cuda:0", **kw):
     import paper_2607_24741_amd as ds
     dv = to_device(w, device)
     out = ds.solve(dv["X"], dv["Y"], dv["a"], dv["b"], dv["eps"], tol, n=dv["n"], m=dv["m"],
-                   return_stats=True, trace_len=kw.pop("trace_len", 20000), **kw)
+                   g0=dv["g0"], return_stats=True, trace_len=kw.pop("trace_len", 20000), **kw)
     f, g, depth, res, status, order, st = out
     torch.cuda.synchronize()
     return dict(f=f.cpu().numpy().astype(np.float64), g=g.cpu().numpy().astype(np.float64),
@@ -65,7 +67,7 @@ def run_gpu(w, tol, *, device="cuda:0", **kw):
 
 def run_oracle(w, tol, *, lanes=None, **kw):
     return oracle.solve(w.X, w.Y, w.a, w.b, w.eps, tol, n=w.n, m=w.m, history=True,
-                        lanes=lanes, processes=procs(), **kw)
+                        lanes=lanes, processes=procs(), g0=getattr(w, "g0", None), **kw)
 
 
 def pot_err(fg, fo, gg, go, eps):
@@ -79,8 +81,10 @@ def decision_consistent(w, t, tol, depth_gpu, status_gpu, audit_every, band=RES_
     must have r_or >= tol - band, and the audit at which it stopped (if it
     converged) must have r_or <= tol + band. Returns (ok, worst margin)."""
     nt, mt = int(w.n[t]), int(w.m[t])
+    g0 = getattr(w, "g0", None)
     run = oracle.solve_lane(w.X[t, :nt], w.Y[t, :mt], w.a[t, :nt], w.b[t, :mt], w.eps[t], 0.0,
-                            max_iter=depth_gpu, audit_every=audit_every, history=True)
+                            max_iter=depth_gpu, audit_every=audit_every, history=True,
+                            g0=None if g0 is None else g0[t, :mt])
     r = {k: max(a, b) for k, a, b in run["history"]}
     worst = 0.0
     for k, rk in r.items():

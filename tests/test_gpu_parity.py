@@ -9,7 +9,7 @@ import pytest
 
 import oracle
 from paper_2607_24741_amd import workloads as wl
-from tests.gpu_support import compare, log, run_gpu, run_oracle
+from tests.gpu_support import compare, log, procs, run_gpu, run_oracle
 
 pytestmark = pytest.mark.gpu
 
@@ -267,6 +267,9 @@ def test_sub_batches_are_bitwise_identical(cfg):
         w = wl.make("c2", W=24, n=256, m=256)
     else:
         w = wl.make("c5", W=24, n=600, m=600, hetero=(40, 600))
+        # with a proposal: each sub-batch must read its own lanes' rows of it
+        rng = np.random.default_rng(5)
+        w.g0 = (0.01 * rng.standard_normal((w.W, w.Y.shape[1]))).astype(np.float32)
     log(f"[case] sub-batches {cfg}: W={w.W} tol 1e-3, streams 1")
     base = run_gpu(w, 1e-3, max_iter=3000, streams=1)
     for s in (2, 3, 4):
@@ -276,6 +279,30 @@ def test_sub_batches_are_bitwise_identical(cfg):
             assert np.array_equal(g[k], base[k], equal_nan=True), (s, k)
         for k in ("slots_update", "pair_evals", "halfsteps_executed", "l_max", "check_pair_evals"):
             assert getattr(g["stats"], k) == getattr(base["stats"], k), (s, k)
+
+
+@pytest.mark.parametrize("flags", [0, F_FORCE_VALU, F_PRECISE, F_MATERIALIZE],
+                         ids=["mfma", "valu", "precise", "materialised"])
+def test_proposal_parity(flags):
+    """A proposal g0 (Sec. 2: a carried or warm-started target potential)
+    replaces the cold start and the GPU follows the oracle's trajectory from
+    the same float32 g0. Ragged c2-shaped lanes; g0 is the oracle's own state
+    after 12 cycles shifted by a per-lane gauge constant (the shift must come
+    back out exactly in the potentials, Sec. 4.2), except lane 0, which gets a
+    random g0. g0 is NaN past each lane's prefix (never read)."""
+    w = wl.make("c2", W=6, n=200, m=176)
+    mid = oracle.solve(w.X, w.Y, w.a, w.b, w.eps, 1e-2, n=w.n, m=w.m, fixed_iters=12,
+                       processes=procs())
+    rng = np.random.default_rng(9)
+    g0 = mid["g"] + rng.uniform(-1.0, 1.0, size=(w.W, 1))
+    g0[0] = 0.05 * rng.standard_normal(w.Y.shape[1])
+    for t in range(w.W):
+        g0[t, int(w.m[t]):] = np.nan
+    w.g0 = g0.astype(np.float32)
+    g, o, rep = _case("c2-reduced-proposal", w, 1e-2, flags=flags)
+    cold = run_oracle(wl.make("c2", W=6, n=200, m=176), 1e-2)
+    # carried lanes start 12 cycles in: they finish no later than from cold
+    assert np.all(o["depth"][1:] <= cold["depth"][1:])
 
 
 def test_padding_isolation():
