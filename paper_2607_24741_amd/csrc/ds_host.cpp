@@ -343,6 +343,7 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
     l.slot = L.bank[bank].slot; l.dec = L.bank[bank].dec;
     l.audit = L.audit; l.vcnt = L.vcnt; l.ctrl = L.ctrl;
     l.hsnap = R->snap_dev; l.nchk = L.nchk;
+    l.progress = &R->snap_dev->progress;
     l.Q = L.Q; l.q_lane = (size_t)L.pad[0] * L.pad[1]; l.q_ld = L.pad[1];
     return l;
   };

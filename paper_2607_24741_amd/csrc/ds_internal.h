@@ -189,7 +189,8 @@ struct Launch {
   const float* Q;                 // materialised cost (caller lane l at Q + l * q_lane)
   size_t q_lane;                  // floats per lane
   int q_ld;                       // row stride of Q (padded target count)
-  int seqno;                      // launch sequence number (progress mirror)
+  int* progress;                  // &hsnap->progress as the device addresses it (may be null)
+  int seqno;                      // launch sequence number written there
 };
 
 struct ScanArgs {          // compaction map over the slots of the current bank

@@ -66,8 +66,11 @@ __device__ __forceinline__ void st_sys(int* p, int v) {
 }
 // Block 0 of an update launch publishes the launch's sequence number to the
 // host before anything else: every earlier launch of the stream has completed.
+// A plain int store (the snapshot is uncached, coherent host memory): type-based
+// alias analysis then keeps the float operand loads that follow it on the
+// scalar path, which an atomic store would forbid.
 __device__ __forceinline__ void note_progress(const Launch& L) {
-  if (blockIdx.x == 0 && threadIdx.x == 0 && L.hsnap) st_sys(&L.hsnap->progress, L.seqno);
+  if (blockIdx.x == 0 && threadIdx.x == 0 && L.progress) *L.progress = L.seqno;
 }
 // all of this wave's outstanding memory operations have completed
 __device__ __forceinline__ void wait_mem() { __builtin_amdgcn_s_waitcnt(0); }
