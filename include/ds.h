@@ -80,7 +80,8 @@ typedef enum {
 enum {
   DS_F_SHADOW = 1u,     /* also run the full check on screen-negative lanes and
                            count already-releasable lanes the screen missed      */
-  DS_F_TIMING = 2u,     /* time every update launch with HIP events (ds_stats)  */
+  DS_F_TIMING = 2u,     /* time the update launches of every 32nd cycle with HIP
+                           events in their dispatches (ds_stats)                 */
   DS_F_FORCE_VALU = 4u, /* use the vector-ALU update kernels for any d <= 32     */
   DS_F_FORCE_MFMA = 8u, /* use the matrix-core update kernels for any d <= 32    */
   DS_F_PRECISE = 16u,   /* float64 state and exponent arguments (vector-ALU
@@ -88,9 +89,17 @@ enum {
                            for small eps, where float32 rounding of exponents of
                            size C/eps reaches the tolerance bands; the outputs
                            stay float32                                         */
-  DS_F_MATERIALIZE = 32u /* build the cost C (base-2 units, float32) once per call
+  DS_F_MATERIALIZE = 32u, /* build the cost C (base-2 units, float32) once per call
                            in the workspace and stream it from HBM in every
                            half-step; always on for d > 32 (n_max, m_max <= 8192) */
+  DS_F_GUARD = 64u      /* guarded release (eq:release-contract in float64): a lane
+                           whose float32 row screen is within the guard margin
+                           (r^ <= (1 + 1/64) tau_screen, or non-finite) is verified by a
+                           float64 evaluation of both marginals of exactly the
+                           float32 potentials the caller will receive (cost formed
+                           in float64 from the caller's coordinates); that residual
+                           decides the release and is the one reported. One extra
+                           launch per audit cycle; n_max, m_max <= 8192.         */
 };
 
 /* One window of W lanes. Device pointers. */

@@ -101,6 +101,9 @@ ds::Layout plan(const ds_problem* pr, const ds_options* op, void* ws) {
   L.off[1] = c.take<int>(W + 1);
   L.ctrl = c.take<ds::Ctrl>(1);
   L.Q = L.mat ? c.take<float>(W * (size_t)L.pad[0] * (size_t)L.pad[1]) : nullptr;
+  L.guard = (op->flags & DS_F_GUARD) ? 1 : 0;
+  for (int side = 0; side < 2; ++side)
+    L.agg64[side] = L.guard ? c.take<double2>(W * (size_t)L.rbmax) : nullptr;
   L.bytes = align_up(c.off, 256);
   return L;
 }
@@ -125,6 +128,8 @@ ds_err check_problem(const ds_problem* pr, const ds_options* op) {
     if (pr->n_max > ds::kMatMaxPts || pr->m_max > ds::kMatMaxPts)
       return fail(DS_E_UNSUPPORTED, "the materialised cost supports at most 8192 points per side");
   }
+  if ((op->flags & DS_F_GUARD) && (pr->n_max > ds::kMatMaxPts || pr->m_max > ds::kMatMaxPts))
+    return fail(DS_E_UNSUPPORTED, "guarded release (DS_F_GUARD) supports at most 8192 points per side");
   if (!(op->tol > 0.f) || !std::isfinite(op->tol)) return fail(DS_E_INVALID, "tol must be finite and > 0");
   if (op->max_iter < 1) return fail(DS_E_INVALID, "max_iter must be >= 1");
   if (op->audit_every < 1) return fail(DS_E_INVALID, "audit_every must be >= 1");
@@ -252,6 +257,7 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
   const int mode = op->mode;
   const bool active = (mode == DS_MODE_ACTIVE);
   const bool shadow = (op->flags & DS_F_SHADOW) != 0;
+  const bool guard = (op->flags & DS_F_GUARD) != 0;
   const bool use_mfma = uses_mfma(pr, op);
   const bool precise = (op->flags & DS_F_PRECISE) != 0;
   const bool mat = L.mat != 0;
@@ -334,6 +340,24 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
     u.role = role; u.kind = kind;
     return u;
   };
+  // float64 verification launches (guarded release): pass 0 is the row marginal
+  // (rows = x), pass 1 the column marginal
+  GuardArgs ga;
+  std::memset(&ga, 0, sizeof(ga));
+  for (int role = 0; role < 2; ++role) {
+    ga.w_col[role] = role ? pr->a : pr->b;
+    ga.w_ld_col[role] = role ? pr->n_max : pr->m_max;
+    ga.xy_row[role] = role ? pr->Y : pr->X;
+    ga.xy_col[role] = role ? pr->X : pr->Y;
+    ga.ld_row[role] = role ? pr->m_max : pr->n_max;
+    ga.ld_col[role] = role ? pr->n_max : pr->m_max;
+    ga.agg64[role] = L.agg64[role];
+  }
+  ga.eps = pr->eps; ga.d = pr->d; ga.es = L.es;
+  // the float32 screen and the float64 residual of the returned potentials
+  // differ by the rounding of the state to float32 outputs (~1e-5 on c2-like
+  // lanes): a lane is verified once its screen is within 1/64 of the threshold
+  ga.tau_guard = (op->screen_tol > 0.f ? op->screen_tol : op->tol) * (1.f + 1.f / 64.f);
   auto make_launch = [&]() {
     Launch l;
     std::memset(&l, 0, sizeof(l));
@@ -455,13 +479,26 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
     lf.nb0 = blocks_of(vf, 0, items[0]);
     ds_err r = run(lf, vf, lf.nb0, sample, k, 0);
     if (r != DS_OK) return r;
+    if (audit_prev && guard) {
+      // guarded release: float64 verification of state k-1 (both marginals of
+      // the potentials the emission would write) before the g-half
+      Launch lc = make_launch();
+      lc.p[0] = make_pass(0, 1, pk1, pk1, pk1);   // row marginal of state k-1
+      lc.p[1] = make_pass(1, 1, pk1, pk1, pk1);   // column marginal of state k-1
+      for (Pass& q : lc.p) {
+        q.depth = k - 1;
+        q.verify_all = shadow ? 1 : 0;
+      }
+      lc.nb0 = std::max(items[0], 0);
+      HIP_TRY(launch_check64(lc, ga, lc.nb0 + std::max(items[1], 0), st));
+    }
     // g-half of cycle k (+ column check and decision for state k-1)
     // (the check blocks come first: most of them exit at once)
     Launch lg = make_launch();
     const int vg = pick(items[1]);
     const int nbg = blocks_of(vg, 1, items[1]);
     int blocks = nbg;
-    if (audit_prev) {
+    if (audit_prev && !guard) {
       lg.p[0] = make_pass(1, 1, pk1, pk1, pk1);   // column marginal of state k-1
       lg.p[0].decide = 1;
       lg.p[0].verify_all = shadow ? 1 : 0;
@@ -489,21 +526,33 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
     const int K = ctrl.finished ? ctrl.final_cycle : launched;
     const int pK = K & 1;
     HIP_TRY(launch_zero_counters(L.vcnt, W, st));
-    Launch lv = make_launch();
-    lv.p[0] = make_pass(0, 1, pK, pK, pK);
-    lv.p[0].final_audit = 1; lv.p[0].depth = K; lv.p[0].verify_all = 1;
-    const int vv = pick(ctrl.items_f);
-    lv.nb0 = blocks_of(vv, 0, ctrl.items_f);
     int saveA = A;
-    ds_err r = run(lv, vv, lv.nb0, true, K, 1);
-    if (r != DS_OK) return r;
-    Launch lw = make_launch();
-    lw.p[0] = make_pass(1, 1, pK, pK, pK);
-    lw.p[0].final_audit = 1; lw.p[0].decide = 1; lw.p[0].depth = K; lw.p[0].verify_all = 1;
-    const int vw = pick(ctrl.items_g);
-    lw.nb0 = blocks_of(vw, 1, ctrl.items_g);
-    r = run(lw, vw, lw.nb0, true, K, 1);
-    if (r != DS_OK) return r;
+    if (guard) {
+      // both marginals of state K in float64, every lane still running
+      Launch lc = make_launch();
+      lc.p[0] = make_pass(0, 1, pK, pK, pK);
+      lc.p[1] = make_pass(1, 1, pK, pK, pK);
+      for (Pass& q : lc.p) {
+        q.final_audit = 1; q.depth = K; q.verify_all = 1; q.decide = 1;
+      }
+      lc.nb0 = ctrl.items_f;
+      HIP_TRY(launch_check64(lc, ga, ctrl.items_f + ctrl.items_g, st));
+    } else {
+      Launch lv = make_launch();
+      lv.p[0] = make_pass(0, 1, pK, pK, pK);
+      lv.p[0].final_audit = 1; lv.p[0].depth = K; lv.p[0].verify_all = 1;
+      const int vv = pick(ctrl.items_f);
+      lv.nb0 = blocks_of(vv, 0, ctrl.items_f);
+      ds_err r = run(lv, vv, lv.nb0, true, K, 1);
+      if (r != DS_OK) return r;
+      Launch lw = make_launch();
+      lw.p[0] = make_pass(1, 1, pK, pK, pK);
+      lw.p[0].final_audit = 1; lw.p[0].decide = 1; lw.p[0].depth = K; lw.p[0].verify_all = 1;
+      const int vw = pick(ctrl.items_g);
+      lw.nb0 = blocks_of(vw, 1, ctrl.items_g);
+      r = run(lw, vw, lw.nb0, true, K, 1);
+      if (r != DS_OK) return r;
+    }
     A = saveA;
     HIP_TRY(hipMemcpyAsync(&ctrl, L.ctrl, sizeof(Ctrl), hipMemcpyDeviceToHost, st));
     HIP_TRY(hipStreamSynchronize(st));

@@ -139,6 +139,8 @@ struct Layout {
   int* off[2];       // work item offsets per role [W + 1]
   Ctrl* ctrl;
   float* Q;          // materialised cost [W][pad0][pad1] by caller lane, base-2 units
+  double2* agg64[2]; // guarded checks: per row block float64 partials [W][rbmax] (else null)
+  int guard;
   size_t bytes;
 };
 
@@ -191,6 +193,19 @@ struct Launch {
   int q_ld;                       // row stride of Q (padded target count)
   int* progress;                  // &hsnap->progress as the device addresses it (may be null)
   int seqno;                      // launch sequence number written there
+};
+
+// Extra arguments of the float64 verification launch (guarded release), per
+// pass (p[0] of its Launch: row marginal, rows = x; p[1]: column marginal).
+struct GuardArgs {
+  const float* w_col[2]; int w_ld_col[2];   // the column side's caller masses
+  const float* xy_row[2];                   // caller coordinates of the row side
+  const float* xy_col[2];                   // and of the column side, by lane id
+  int ld_row[2], ld_col[2];                 // their point strides (n_max / m_max)
+  double2* agg64[2];      // [W][rbmax] per row block {sum |marginal - mass|, non-finite}
+  const float* eps;       // caller eps [W]
+  int d, es;              // point dimension; state element size in floats
+  float tau_guard;        // screen threshold with the guard margin
 };
 
 struct ScanArgs {          // compaction map over the slots of the current bank
@@ -257,6 +272,8 @@ struct CostArgs {
   int W, n_max, m_max, d, pad0, pad1;
 };
 hipError_t launch_cost(const CostArgs& a, hipStream_t st);
+// float64 two-sided check of the audited state (both marginals, two passes)
+hipError_t launch_check64(const Launch& a, const GuardArgs& g, int blocks, hipStream_t st);
 hipError_t launch_scan(const ScanArgs& a, hipStream_t st);
 hipError_t launch_offsets(SlotInfo* slot, int A, int rows, int* off_f, int* off_g, Ctrl* ctrl,
                           hipStream_t st);

@@ -374,7 +374,12 @@ __device__ __forceinline__ bool item_live(const Launch& L, const Pass& P, int s,
   return true;
 }
 
-// Uniform lane shapes (P.ipl > 0): block b of pass pi takes item
+// Blocks of pass pi of a launch.
+__device__ __forceinline__ int pass_blocks(const Launch& L, int pi) {
+  return pi ? (int)gridDim.x - L.nb0 : L.nb0;
+}
+
+// Uniform lane shapes (P.ipl > 0): block b of a pass takes item
 // xcd_item(b, nb) of the pass's own nb blocks, so its slot s and first row
 // block rb0 (RPI row blocks per item) follow from the launch alone and the
 // block can issue its operand loads before any read of device state. The host
@@ -382,9 +387,7 @@ __device__ __forceinline__ bool item_live(const Launch& L, const Pass& P, int s,
 // item is covered; blocks past it are dropped by item_live(). False only for
 // slots beyond the launch's own width bound (never read).
 template <int RPI>
-__device__ __forceinline__ bool item_uniform(const Launch& L, const Pass& P, int pi, int b, int& s,
-                                             int& rb0) {
-  const int nb = pi ? (int)gridDim.x - L.nb0 : L.nb0;
+__device__ __forceinline__ bool item_uniform(const Pass& P, int nb, int b, int& s, int& rb0) {
   const int ipi = (P.ipl + RPI - 1) / RPI;   // items per lane
   const int item = xcd_item(b, nb);
   s = item / ipi;
@@ -409,17 +412,17 @@ __device__ __forceinline__ bool locate_item(const Launch& L, const Pass& P, int 
   return item_live(L, P, s, si, fin, A);
 }
 
-// Where block b of a pass works (slot s, first row block rb0, the lane's row
-// and column counts). With uniform shapes the control block and slot record
+// Where block b of a pass of nb blocks works (slot s, first row block rb0, the
+// lane's row and column counts). With uniform shapes the control block and slot record
 // are only requested here (c_fin, c_A, si) and checked by item_live() once
 // the item's own loads are in flight; otherwise they are already checked.
 template <int RPI, int UNI = -1>
-__device__ __forceinline__ bool place_item(const Launch& L, const Pass& P, int pi, int b, int& s,
+__device__ __forceinline__ bool place_item(const Launch& L, const Pass& P, int nb, int b, int& s,
                                            int& rb0, int& nrows, int& ncols, SlotInfo& si,
                                            int& c_fin, int& c_A) {
   // UNI: 1 / 0 when the caller is compiled for uniform / mixed shapes only
   if (UNI == 1 || (UNI < 0 && P.ipl > 0)) {
-    if (!item_uniform<RPI>(L, P, pi, b, s, rb0)) return false;
+    if (!item_uniform<RPI>(P, nb, b, s, rb0)) return false;
     // Read through the vector memory path (a zero offset the compiler cannot
     // prove uniform): scalar loads complete out of order, so any later use of
     // a kernel argument would wait for these, while vector loads are waited
@@ -480,8 +483,8 @@ void k_update_mfma(Launch L) {
   const Pass P = L.p[pi];
   int s, rb0, nrows, ncols, c_fin, c_A;
   SlotInfo si;
-  if (!place_item<RT, UNI ? 1 : 0>(L, P, pi, pi ? b - L.nb0 : b, s, rb0, nrows, ncols, si, c_fin,
-                                   c_A))
+  if (!place_item<RT, UNI ? 1 : 0>(L, P, pass_blocks(L, pi), pi ? b - L.nb0 : b, s, rb0, nrows,
+                                   ncols, si, c_fin, c_A))
     return;
   const bool upd = P.kind == KIND_UPDATE;
   float rhat = NAN;
@@ -662,10 +665,12 @@ void k_update_valu(Launch L) {
   __shared__ float2 sh_part[kGroups][kRowsValu];
   const int b = blockIdx.x;
   const int pi = b >= L.nb0;
-  const Pass P = pi ? L.p[1] : L.p[0];
+  const Pass P = L.p[pi];
   int s, rb, nrows, ncols, c_fin, c_A;
   SlotInfo si;
-  if (!place_item<1>(L, P, pi, pi ? b - L.nb0 : b, s, rb, nrows, ncols, si, c_fin, c_A)) return;
+  if (!place_item<1>(L, P, pass_blocks(L, pi), pi ? b - L.nb0 : b, s, rb, nrows, ncols, si, c_fin,
+                     c_A))
+    return;
   const bool upd = P.kind == KIND_UPDATE;
   float rhat = NAN;
   if (!upd) {
@@ -781,10 +786,12 @@ void k_update_f64(Launch L) {
   __shared__ __align__(16) double sh_tile[kGroups / GW][2][kColTile * DPc + kColTile];
   const int b = blockIdx.x;
   const int pi = b >= L.nb0;
-  const Pass P = pi ? L.p[1] : L.p[0];
+  const Pass P = L.p[pi];
   int s, rb, nrows, ncols, c_fin, c_A;
   SlotInfo si;
-  if (!place_item<1>(L, P, pi, pi ? b - L.nb0 : b, s, rb, nrows, ncols, si, c_fin, c_A)) return;
+  if (!place_item<1>(L, P, pass_blocks(L, pi), pi ? b - L.nb0 : b, s, rb, nrows, ncols, si, c_fin,
+                     c_A))
+    return;
   const bool upd = P.kind == KIND_UPDATE;
   float rhat = NAN;
   if (!upd) {
@@ -992,10 +999,12 @@ __global__ __launch_bounds__(512, 2) void k_mat_rows(Launch L) {
   __shared__ float2 sh_row[kRowsValu];
   const int b = blockIdx.x;
   const int pi = b >= L.nb0;
-  const Pass P = pi ? L.p[1] : L.p[0];
+  const Pass P = L.p[pi];
   int s, rb, nrows, ncols, c_fin, c_A;
   SlotInfo si;
-  if (!place_item<1>(L, P, pi, pi ? b - L.nb0 : b, s, rb, nrows, ncols, si, c_fin, c_A)) return;
+  if (!place_item<1>(L, P, pass_blocks(L, pi), pi ? b - L.nb0 : b, s, rb, nrows, ncols, si, c_fin,
+                     c_A))
+    return;
   const bool upd = P.kind == KIND_UPDATE;
   float rhat = NAN;
   if (!upd) {
@@ -1082,10 +1091,12 @@ __global__ __launch_bounds__(512, 2) void k_mat_cols(Launch L) {
   __shared__ float2 sh_part[8][kRowsValu];
   const int b = blockIdx.x;
   const int pi = b >= L.nb0;
-  const Pass P = pi ? L.p[1] : L.p[0];
+  const Pass P = L.p[pi];
   int s, rb, nrows, ncols, c_fin, c_A;     // rows: target points, columns: source points
   SlotInfo si;
-  if (!place_item<1>(L, P, pi, pi ? b - L.nb0 : b, s, rb, nrows, ncols, si, c_fin, c_A)) return;
+  if (!place_item<1>(L, P, pass_blocks(L, pi), pi ? b - L.nb0 : b, s, rb, nrows, ncols, si, c_fin,
+                     c_A))
+    return;
   const bool upd = P.kind == KIND_UPDATE;
   float rhat = NAN;
   if (!upd) {
@@ -1273,6 +1284,27 @@ __global__ __launch_bounds__(1024) void k_offsets(SlotInfo* slot, int A, int row
 // Grid (chunks, A). Retired lanes are emitted in caller order from the
 // parity of their audited state; in a compaction the survivors are gathered
 // into the other bank at their new slots (every lane-indexed array).
+// The output-convention potential of one point of a state, exactly as the
+// emission writes it: f_i = (gam_i + |x~_i|^2 / 2) / kappa (likewise g_j), formed
+// in the precision of the state and rounded to float32; 0 for a removed point.
+__device__ __forceinline__ float export_potential(const float* gam, const float* rec, size_t e,
+                                                  int dp, int es, const SlotInfo& si) {
+  if (es == 2) {
+    const double gq = reinterpret_cast<const double*>(gam)[e];
+    if (gq == -(double)INFINITY) return 0.f;
+    const double* r = reinterpret_cast<const double*>(rec) + e * dp;
+    double nrm = 0.0;
+    for (int k = 0; k < dp; ++k) nrm = fma(r[k], r[k], nrm);
+    return (float)((gq + 0.5 * nrm) * (1.0 / si.kappa64));
+  }
+  const float gq = gam[e];
+  if (gq == -INFINITY) return 0.f;
+  const float* r = rec + e * dp;
+  float nrm = 0.f;
+  for (int k = 0; k < dp; ++k) nrm = fmaf(r[k], r[k], nrm);
+  return (gq + 0.5f * nrm) * (1.f / si.kappa);
+}
+
 __global__ __launch_bounds__(256) void k_move(MoveArgs p) {
   const int s = blockIdx.y;
   const int A = p.compact ? min(p.A, p.ctrl->A_prev) : min(p.A, p.ctrl->A);
@@ -1284,9 +1316,6 @@ __global__ __launch_bounds__(256) void k_move(MoveArgs p) {
   if (!emit && !copy) return;
   const int c0 = blockIdx.x * p.chunk;
   if (emit) {
-    // f_i = (gam_i + |x~_i|^2 / 2) / kappa, in the precision of the state
-    const float inv_k = 1.f / si.kappa;
-    const double inv_k64 = 1.0 / si.kappa64;
     const int par = p.emit_all ? p.final_par : (d.depth & 1);
     for (int side = 0; side < 2; ++side) {
       const int lim = side ? p.m_max : p.n_max;
@@ -1294,27 +1323,9 @@ __global__ __launch_bounds__(256) void k_move(MoveArgs p) {
       const int padn = p.pad[side];
       float* out = side ? p.g : p.f;
       for (int q = c0 + threadIdx.x; q < min(lim, c0 + p.chunk); q += blockDim.x) {
-        float v = 0.f;
-        if (q < cnt) {
-          const size_t e = (size_t)s * padn + q;
-          if (p.es == 2) {
-            const double gq = reinterpret_cast<const double*>(p.src.gam[side][par])[e];
-            if (gq != -(double)INFINITY) {
-              const double* rec = reinterpret_cast<const double*>(p.src.rec[side]) + e * p.dp;
-              double nrm = 0.0;
-              for (int k = 0; k < p.dp; ++k) nrm = fma(rec[k], rec[k], nrm);
-              v = (float)((gq + 0.5 * nrm) * inv_k64);
-            }
-          } else {
-            const float gq = p.src.gam[side][par][e];
-            if (gq != -INFINITY) {
-              const float* rec = p.src.rec[side] + e * p.dp;
-              float nrm = 0.f;
-              for (int k = 0; k < p.dp; ++k) nrm = fmaf(rec[k], rec[k], nrm);
-              v = (gq + 0.5f * nrm) * inv_k;
-            }
-          }
-        }
+        const float v = q < cnt ? export_potential(p.src.gam[side][par], p.src.rec[side],
+                                                   (size_t)s * padn + q, p.dp, p.es, si)
+                                : 0.f;
         out[(size_t)si.lane * lim + q] = v;
       }
     }
@@ -1362,6 +1373,162 @@ __global__ __launch_bounds__(256) void k_move(MoveArgs p) {
     }
   }
 }
+
+// ------------------------------------------- float64 verification (DS_F_GUARD)
+// One marginal of the audited state in float64, for one work item (rows rows of a
+// lane against all its columns) of a lane the float32 screen calls ready within
+// the guard margin -- or of every lane at the final audit. The potentials are the
+// float32 values the emission writes for that state, the cost is formed in
+// float64 from the caller's coordinates, the exponentials are float64: the
+// residual that decides a release is that of the potentials the caller receives
+// (eq:release-contract), to float64 rounding. Pass 0: row marginal (rows = x),
+// pass 1: column marginal (rows = y). Wave w takes rows w, w + nw, .. of the
+// item (nw waves); its lanes stride over the columns, whose exported potentials
+// are staged 256 at a time in LDS; a row's sum is a fixed-order butterfly over
+// the wave. Each block publishes its rows' sum of |marginal - mass| (row order);
+// the last block of the lane over both passes adds them in block order and takes
+// the decision. Launched between the f-half and the g-half of an audited cycle
+// (state k-1 is read-only there) and at the final audit.
+__device__ __forceinline__ double wave_sum64(double v) {
+#pragma unroll
+  for (int m = 32; m > 0; m >>= 1) v += __shfl_xor(v, m, 64);
+  return v;
+}
+
+constexpr int kGuardChunk = 256;
+
+__global__ __launch_bounds__(256) void k_check64(Launch L, GuardArgs G) {
+  __shared__ double sh_pot[kGuardChunk];
+  __shared__ double sh_row[64];
+  __shared__ int sh_bad[64];
+  const int b = blockIdx.x;
+  const int pi = b >= L.nb0;
+  const Pass& P = L.p[pi];
+  int s, rb, nrows, ncols, c_fin, c_A;
+  SlotInfo si;
+  if (!place_item<1>(L, P, pass_blocks(L, pi), pi ? b - L.nb0 : b, s, rb, nrows, ncols, si, c_fin,
+                     c_A))
+    return;
+  // the lane's float32 row screen of the audited state (same gate for both passes)
+  const int n_x = P.role ? ncols : nrows;
+  bool checked = true;
+  if (!P.final_audit) {
+    const LaneAgg g = lane_aggregate(P.agg_screen, s, L.rbmax, row_blocks(n_x, L.rows), false);
+    checked = P.verify_all || !isfinite(g.sum) || g.sum <= G.tau_guard;
+  }
+  if (!item_live(L, P, s, si, c_fin, c_A) || !checked) return;
+  const int lane_id = si.lane;
+  const int R = L.rows;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int nw = (int)blockDim.x >> 6;
+  const int d = G.d;
+  const double inv_eps = 1.0 / (double)G.eps[lane_id];
+  const float* wr = P.w_row + (size_t)lane_id * P.w_ld;
+  const float* wc = G.w_col[pi] + (size_t)lane_id * G.w_ld_col[pi];
+  // wave w: rows w, w + nw, .. of the item (the same number of row steps in
+  // every wave); per row step the block stages the exported potentials of 256
+  // columns at a time in LDS, and the wave's lanes stride over them
+  const int steps = (R + nw - 1) / nw;
+#pragma unroll 1
+  for (int q = 0; q < steps; ++q) {
+    const int r = wave + q * nw;
+    const int i = rb * R + r;
+    const bool live = r < R && i < nrows && wr[i] != 0.f;
+    const double fi = live ? (double)export_potential(P.gam_out, P.rec_row, (size_t)s * P.padr + i,
+                                                      L.dp, G.es, si)
+                           : 0.0;
+    const float* xi = G.xy_row[pi] + ((size_t)lane_id * G.ld_row[pi] + (live ? i : 0)) * d;
+    double acc = 0.0;
+#pragma unroll 1
+    for (int c0 = 0; c0 < ncols; c0 += kGuardChunk) {
+      __syncthreads();   // every wave is done with the previous chunk
+      if (tid < kGuardChunk) {
+        const int j = c0 + tid;
+        sh_pot[tid] = (j < ncols && wc[j] != 0.f)
+                          ? (double)export_potential(P.gam_col, P.rec_col, (size_t)s * P.padc + j,
+                                                     L.dp, G.es, si)
+                          : -(double)INFINITY;   // past the prefix or removed (zero mass)
+      }
+      __syncthreads();
+      if (!live) continue;
+#pragma unroll 1
+      for (int t = lane; t < kGuardChunk && c0 + t < ncols; t += 64) {
+        const double gj = sh_pot[t];
+        if (gj == -(double)INFINITY) continue;
+        const float* yj = G.xy_col[pi] + ((size_t)lane_id * G.ld_col[pi] + c0 + t) * d;
+        double C = 0.0;
+#pragma unroll 1
+        for (int k = 0; k < d; ++k) {
+          const double df = (double)xi[k] - (double)yj[k];
+          C = fma(df, df, C);
+        }
+        acc += exp((fi + gj - C) * inv_eps);
+      }
+    }
+    // row total (the same bits in every lane), |marginal - mass|
+    const double tot = wave_sum64(acc);
+    if (lane == 0 && r < R) {
+      sh_row[r] = live ? fabs(tot - (double)wr[i]) : 0.0;
+      sh_bad[r] = live && !isfinite(tot);
+    }
+  }
+  __syncthreads();
+  if (tid != 0) return;
+  double part = 0.0;
+  int bad = 0;
+  for (int r = 0; r < R; ++r) {
+    if (rb * R + r >= nrows) break;
+    part += sh_row[r];
+    bad |= sh_bad[r];
+  }
+  unsigned long long* dst =
+      reinterpret_cast<unsigned long long*>(G.agg64[P.role] + (size_t)s * L.rbmax + rb);
+  __hip_atomic_store(dst, (unsigned long long)__double_as_longlong(part), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(dst + 1, (unsigned long long)__double_as_longlong(bad ? 1.0 : 0.0),
+                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  wait_mem();
+  const int total = row_blocks(si.n, R) + row_blocks(si.m, R);   // the lane's blocks, both passes
+  const int prev = atomicAdd(&L.vcnt[lane_id], 1);
+  if (prev + 1 != total) return;
+  atomicExch(&L.vcnt[lane_id], 0);
+  // last block of the lane: both marginals' residuals, in block order
+  double rr[2] = {0.0, 0.0};
+  bool fin = true;
+  for (int side = 0; side < 2; ++side) {
+    const int nrb = row_blocks(side ? si.m : si.n, R);
+    unsigned long long* src =
+        reinterpret_cast<unsigned long long*>(G.agg64[side] + (size_t)s * L.rbmax);
+    for (int q = 0; q < nrb; ++q) {
+      rr[side] += __longlong_as_double((long long)__hip_atomic_load(
+          src + 2 * q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+      if (__longlong_as_double((long long)__hip_atomic_load(
+              src + 2 * q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) != 0.0)
+        fin = false;
+    }
+  }
+  const double rrow = rr[0], rcol = rr[1];
+  fin = fin && isfinite(rrow) && isfinite(rcol);
+  const double rmax = fmax(rrow, rcol);
+  atomicAdd(&L.nchk[lane_id], 2);   // both marginals evaluated
+  L.audit[s].rhat = (float)rrow;
+  L.audit[s].rcol = (float)rcol;
+  if (P.final_audit) {
+    if (L.mode == MODE_STATIC && si.passed) {
+      L.dec[s].res_row = (float)rrow;
+      L.dec[s].res_col = (float)rcol;
+      return;
+    }
+    retire_lane(L, P, s, si, !fin ? 2 : (rmax <= (double)L.tol ? 0 : 1), (float)rrow, (float)rcol);
+    return;
+  }
+  atomicAdd(&L.ctrl->screen_pos, 1);
+  if (!fin) retire_lane(L, P, s, si, 2, (float)rrow, (float)rcol);
+  else if (rmax <= (double)L.tol) retire_lane(L, P, s, si, 0, (float)rrow, (float)rcol);
+  else atomicAdd(&L.ctrl->check_fail, 1);
+}
+
 
 // Completion order: lanes sorted by (depth, lane id). rank_t counts the lanes
 // that precede t; one block, W <= 4096.
@@ -1680,6 +1847,11 @@ hipError_t launch_update_mat(const Launch& a, int blocks, hipStream_t st, hipEve
     hipExtLaunchKernelGGL(k_mat_rows, dim3(blocks), dim3(512), 0, st, e0, e1, 0, a);
   else
     hipExtLaunchKernelGGL(k_mat_cols, dim3(blocks), dim3(512), 0, st, e0, e1, 0, a);
+  return hipGetLastError();
+}
+hipError_t launch_check64(const Launch& a, const GuardArgs& g, int blocks, hipStream_t st) {
+  if (blocks <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_check64, dim3(blocks), dim3(256), 0, st, a, g);
   return hipGetLastError();
 }
 hipError_t launch_cost(const CostArgs& a, hipStream_t st) {

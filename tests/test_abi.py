@@ -137,3 +137,15 @@ def test_sub_batch_validation_and_size():
     auto = lambda W: _bytes(_problem(W=W), ds._options(1e-3, None, 100, 1, "active", 0, 0))[1]
     for W, k in ((64, 3), (40, 2), (16, 1)):
         assert auto(W) == _bytes(_problem(W=W), ds._options(1e-3, None, 100, 1, "active", 0, k))[1]
+
+
+def test_guarded_release_validation_and_size():
+    """DS_F_GUARD keeps two float64 partials per row block and lane, and
+    stages a lane's column potentials in LDS (at most 8192 points per side)."""
+    op = ds._options(1e-3, None, 100, 1, "active", 0, 1)
+    opg = ds._options(1e-3, None, 100, 1, "active", ds.F_GUARD, 1)
+    code, n0 = _bytes(_problem(W=4, n_max=256, m_max=256, d=8), op)
+    code2, n1 = _bytes(_problem(W=4, n_max=256, m_max=256, d=8), opg)
+    assert code == 0 and code2 == 0 and n1 > n0
+    assert _bytes(_problem(W=2, n_max=9000, m_max=100, d=3), opg)[0] == 4
+    assert _bytes(_problem(W=2, n_max=9000, m_max=100, d=3), op)[0] == 0
