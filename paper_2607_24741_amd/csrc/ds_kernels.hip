@@ -626,9 +626,14 @@ void k_update_mfma(Launch L) {
   if (fast) sweep(true); else sweep(false);
   __syncthreads();
   if (wave != 0) return;
-  // merge per row: half-waves, then groups, in order
+  // merge per row: half-waves, then groups, in order. Anchored sums carry a
+  // zero running maximum everywhere, so there every scale factor is exactly 1
+  // and the merge is the plain sum in the same order (the same bits).
   float Mt = 0.f, St = 0.f;
-  if (owner) {
+  if (owner && fast) {
+#pragma unroll
+    for (int g = 0; g < kGroups; ++g) St += sh_part[g][0][lane].y + sh_part[g][1][lane].y;
+  } else if (owner) {
     float Mg[kGroups], Sg[kGroups];
     float mx = -INFINITY;
 #pragma unroll
@@ -759,7 +764,10 @@ void k_update_valu(Launch L) {
   __syncthreads();
   if (wave != 0) return;
   float Mt = 0.f, St = 0.f;
-  if (owner) {
+  if (owner && fast) {   // anchored sums: every scale factor is exactly 1
+#pragma unroll
+    for (int g = 0; g < kGroups; ++g) St += sh_part[g][lane].y;
+  } else if (owner) {
     float mx = -INFINITY;
 #pragma unroll
     for (int g = 0; g < kGroups; ++g) mx = fmaxf(mx, sh_part[g][lane].x);
