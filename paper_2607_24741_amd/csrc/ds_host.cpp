@@ -426,15 +426,26 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
   for (int k = 1; k <= max_iter; ++k) {
     // bounded run-ahead: wait for the device only when too far behind
     // (block 0 of every update launch publishes the launch's sequence
-    // number; the stream is polled now and then so a failed launch surfaces
-    // as an error instead of a wait that never ends)
-    for (int spin = 0; seqno - hs->progress > 2 * kLag; ++spin) {
-      if ((spin & 1023) == 1023) {
-        const hipError_t qe = hipStreamQuery(st);
-        if (qe == hipSuccess) break;                  // idle: nothing left to wait for
-        if (qe != hipErrorNotReady) HIP_TRY(qe);
+    // number). Only when the word has not moved for a while is the stream
+    // queried, so that a failed launch surfaces as an error instead of a wait
+    // that never ends; frequent queries from several sub-batch threads would
+    // contend with their launches in the runtime.
+    if (seqno - hs->progress > 2 * kLag) {
+      int seen = hs->progress;
+      auto since = std::chrono::steady_clock::now();
+      while (seqno - hs->progress > 2 * kLag) {
+        const int now_seen = hs->progress;
+        if (now_seen != seen) {
+          seen = now_seen;
+          since = std::chrono::steady_clock::now();
+        } else if (std::chrono::steady_clock::now() - since > std::chrono::milliseconds(20)) {
+          const hipError_t qe = hipStreamQuery(st);
+          if (qe == hipSuccess) break;                // idle: nothing left to wait for
+          if (qe != hipErrorNotReady) HIP_TRY(qe);
+          since = std::chrono::steady_clock::now();
+        }
+        std::this_thread::yield();
       }
-      std::this_thread::yield();
     }
     const int s_fin = hs->finished, s_ep = hs->epoch, s_ret = hs->n_retired;
     const int s_cmp = hs->compacted, s_act = hs->n_active;
