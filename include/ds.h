@@ -82,8 +82,9 @@ enum {
                            count already-releasable lanes the screen missed      */
   DS_F_TIMING = 2u,     /* time the update launches of every 32nd cycle with HIP
                            events in their dispatches (ds_stats)                 */
-  DS_F_FORCE_VALU = 4u, /* use the vector-ALU update kernels for any d <= 32     */
-  DS_F_FORCE_MFMA = 8u, /* use the matrix-core update kernels for any d <= 32    */
+  DS_F_FORCE_VALU = 4u, /* use the vector-ALU update kernels for any d <= 32
+                           (the default for d <= 32 is the matrix-core kernel)  */
+  DS_F_FORCE_MFMA = 8u, /* use the matrix-core update kernels (the default)      */
   DS_F_PRECISE = 16u,   /* float64 state and exponent arguments (vector-ALU
                            kernels, d <= 16, exclusive with DS_F_FORCE_MFMA):
                            for small eps, where float32 rounding of exponents of

@@ -108,11 +108,15 @@ ds::Layout plan(const ds_problem* pr, const ds_options* op, void* ws) {
   return L;
 }
 
+// The matrix-core kernel is the default at every d: even at d = 2 or 3 its
+// augmented contraction (K = 2 ceil(d/2) + 2) costs fewer SIMD cycles per term
+// than the vector kernel's d fused multiply-adds plus the bias add, and it
+// was measured faster at d = 2, 3, 8 and 16.
 bool uses_mfma(const ds_problem* pr, const ds_options* op) {
+  (void)pr;
   if (op->flags & DS_F_PRECISE) return false;
-  if (op->flags & DS_F_FORCE_MFMA) return true;
   if (op->flags & DS_F_FORCE_VALU) return false;
-  return pr->d >= 8;
+  return true;
 }
 
 ds_err check_problem(const ds_problem* pr, const ds_options* op) {
@@ -381,10 +385,20 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
   // Kernel variant by the width bound of the launch: few items -> more waves
   // per item (shorter sweeps); many items -> more rows per wave (fewer column
   // re-reads). Every variant computes the same bits.
-  auto pick = [&](int items) -> int {
+  // Middle widths on the matrix cores: a wave sweeps two groups, or four when
+  // a group is at most two column tiles (the launch's columns: the other
+  // side's points), so that every wave still sweeps several tiles.
+  int tpg[2];
+  for (int role = 0; role < 2; ++role) {
+    const int cols = uniform ? (role ? lanes[0].n : lanes[0].m) : L.pad[1 - role];
+    const int ct = (cols + kColTile - 1) / kColTile;
+    tpg[role] = (ct + kGroups - 1) / kGroups;
+  }
+  auto pick = [&](int items, int role) -> int {
     if (mat) return VAR_MEDIUM;   // one layout: 64-row items, one block each
     if (use_mfma && uniform && items >= kWideItems) return VAR_WIDE;
-    return items >= (use_mfma ? kMediumItemsMfma : kMediumItemsValu) ? VAR_MEDIUM : VAR_NARROW;
+    if (items < (use_mfma ? kMediumItemsMfma : kMediumItemsValu)) return VAR_NARROW;
+    return (use_mfma && tpg[role] <= 2) ? VAR_MEDIUM4 : VAR_MEDIUM;
   };
   auto blocks_of = [&](int variant, int role, int items) -> int {
     if (variant != VAR_WIDE || items <= 0) return std::max(items, 0);
@@ -486,7 +500,7 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
     Launch lf = make_launch();
     lf.p[0] = make_pass(0, 0, pk1, pk, pk1);
     lf.p[0].depth = k - 1;
-    const int vf = pick(items[0]);
+    const int vf = pick(items[0], 0);
     lf.nb0 = blocks_of(vf, 0, items[0]);
     ds_err r = run(lf, vf, lf.nb0, sample, k, 0);
     if (r != DS_OK) return r;
@@ -506,7 +520,7 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
     // g-half of cycle k (+ column check and decision for state k-1)
     // (the check blocks come first: most of them exit at once)
     Launch lg = make_launch();
-    const int vg = pick(items[1]);
+    const int vg = pick(items[1], 1);
     const int nbg = blocks_of(vg, 1, items[1]);
     int blocks = nbg;
     if (audit_prev && !guard) {
@@ -552,14 +566,14 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
       Launch lv = make_launch();
       lv.p[0] = make_pass(0, 1, pK, pK, pK);
       lv.p[0].final_audit = 1; lv.p[0].depth = K; lv.p[0].verify_all = 1;
-      const int vv = pick(ctrl.items_f);
+      const int vv = pick(ctrl.items_f, 0);
       lv.nb0 = blocks_of(vv, 0, ctrl.items_f);
       ds_err r = run(lv, vv, lv.nb0, true, K, 1);
       if (r != DS_OK) return r;
       Launch lw = make_launch();
       lw.p[0] = make_pass(1, 1, pK, pK, pK);
       lw.p[0].final_audit = 1; lw.p[0].decide = 1; lw.p[0].depth = K; lw.p[0].verify_all = 1;
-      const int vw = pick(ctrl.items_g);
+      const int vw = pick(ctrl.items_g, 1);
       lw.nb0 = blocks_of(vw, 1, ctrl.items_g);
       r = run(lw, vw, lw.nb0, true, K, 1);
       if (r != DS_OK) return r;

@@ -254,7 +254,9 @@ struct IngestArgs {
 // over waves. All variants compute identical bits; the host picks one by width.
 enum { VAR_NARROW = 0,   // 32-row items, one group per wave (8 waves)
        VAR_MEDIUM = 1,   // 32-row items, two groups per wave (4 waves)
-       VAR_WIDE = 2 };   // 64-row items (uniform lane shapes only), two groups per wave
+       VAR_WIDE = 2,     // 64-row items (uniform lane shapes only), two groups per wave
+       VAR_MEDIUM4 = 3 };  // 32-row items, four groups per wave (2 waves): matrix-core
+                           // kernel, lanes of at most 2 column tiles per group
 // e0 / e1 (may be null): events that record the kernel's own start and end
 hipError_t launch_update(const Launch& a, int d, bool use_mfma, int variant, int blocks,
                          hipStream_t st, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);

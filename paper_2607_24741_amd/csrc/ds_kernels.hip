@@ -460,17 +460,21 @@ __device__ __forceinline__ bool place_item(const Launch& L, const Pass& P, int n
 // anchor. Lane l holds row i = l % 32 for 16 columns, so the streaming sum over
 // j stays inside the lane. The next tile's operands load while the current
 // tile is reduced.
+//
+// The second launch bound is the minimum number of waves per SIMD the register
+// allocation must allow (measured per layout: fewer, longer waves want more
+// registers than spills).
 template <int DH, int RT, int GW>
-constexpr int mfma_min_blocks() {
+constexpr int mfma_waves_per_simd() {
   return (kGroups / GW) == 8 ? (DH <= 7 ? 4 : 2)
-                             : (RT == 1 ? (DH <= 7 ? 8 : (DH <= 12 ? 6 : 4))
-                                        : (DH <= 8 ? 4 : 2));
+       : (kGroups / GW) == 2 ? (DH <= 7 ? 6 : 4)
+       : (RT == 1 ? (DH <= 7 ? 8 : (DH <= 12 ? 6 : 4)) : (DH <= 8 ? 4 : 2));
 }
 
 // UNI: compiled for uniform lane shapes (work item -> slot by division) or
 // for mixed shapes (offsets table); the host launches the one that matches.
 template <int DH, int RT, int GW, bool UNI>
-__global__ __launch_bounds__(64 * (kGroups / GW), (mfma_min_blocks<DH, RT, GW>()))
+__global__ __launch_bounds__(64 * (kGroups / GW), (mfma_waves_per_simd<DH, RT, GW>()))
 void k_update_mfma(Launch L) {
   note_progress(L);
   static_assert(UNI || RT == 1, "two row tiles per item need uniform lane shapes");
@@ -1745,10 +1749,13 @@ static hipError_t launch_mfma_dh(const Launch& a, int variant, int blocks, hipSt
     switch (variant) {
       case VAR_NARROW: hipExtLaunchKernelGGL((k_update_mfma<DH, 1, 1, true>), dim3(blocks), dim3(512), 0, st, e0, e1, 0, a); break;
       case VAR_MEDIUM: hipExtLaunchKernelGGL((k_update_mfma<DH, 1, 2, true>), dim3(blocks), dim3(256), 0, st, e0, e1, 0, a); break;
+      case VAR_MEDIUM4: hipExtLaunchKernelGGL((k_update_mfma<DH, 1, 4, true>), dim3(blocks), dim3(128), 0, st, e0, e1, 0, a); break;
       default: hipExtLaunchKernelGGL((k_update_mfma<DH, 2, 2, true>), dim3(blocks), dim3(256), 0, st, e0, e1, 0, a); break;
     }
   } else if (variant == VAR_NARROW) {
     hipExtLaunchKernelGGL((k_update_mfma<DH, 1, 1, false>), dim3(blocks), dim3(512), 0, st, e0, e1, 0, a);
+  } else if (variant == VAR_MEDIUM4) {
+    hipExtLaunchKernelGGL((k_update_mfma<DH, 1, 4, false>), dim3(blocks), dim3(128), 0, st, e0, e1, 0, a);
   } else {
     hipExtLaunchKernelGGL((k_update_mfma<DH, 1, 2, false>), dim3(blocks), dim3(256), 0, st, e0, e1, 0, a);
   }

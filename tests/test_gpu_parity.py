@@ -32,7 +32,7 @@ def _case(name, w, tol, flags=0, res_atol=None, **kw):
     return g, o, rep
 
 
-@pytest.mark.parametrize("flags", [0, F_FORCE_MFMA], ids=["valu", "mfma"])
+@pytest.mark.parametrize("flags", [F_FORCE_VALU, 0], ids=["valu", "mfma"])
 def test_toy_config_full(flags):
     w = wl.make("c1")
     _case("c1", w, 1e-3, flags=flags)
@@ -143,7 +143,7 @@ def test_precise_state_small_cases(name):
     assert rep["beyond_1e6"] == 0
 
 
-@pytest.mark.parametrize("flags", [0, F_FORCE_MFMA], ids=["valu", "mfma"])
+@pytest.mark.parametrize("flags", [F_FORCE_VALU, 0], ids=["valu", "mfma"])
 def test_heterogeneous_nan_padded(flags):
     w = wl.make("c5", W=8, n=400, m=360, hetero=(40, 400), pad_value=np.nan)
     _case("c5-hetero", w, 1e-3, flags=flags, max_iter=3000)
@@ -193,10 +193,31 @@ def test_full_size_mixture_fixed_work_and_residual_property():
         assert abs(max(rr, rc) - g["residual"][t]) <= 1e-5
 
 
+def _static_at_lmax(w, gs, fixed, pot_bar):
+    for t in range(w.W):
+        scale = max(np.abs(fixed["f"][t]).max(), np.abs(fixed["g"][t]).max(), float(w.eps[t]))
+        err = max(np.abs(gs["f"][t] - fixed["f"][t]).max(),
+                  np.abs(gs["g"][t] - fixed["g"][t]).max()) / scale
+        if pot_bar is not None:
+            assert err <= pot_bar, (t, err)
+        assert abs(gs["residual"][t] - fixed["residual"][t]) <= 1e-5
+        assert gs["residual"][t] <= 1e-3 + 1e-5
+
+
 def test_modes_agree_and_account_slots():
     """Logical masking returns exactly the active outputs (compaction does no
     arithmetic); static packing records the same first passing depths and
-    returns every lane's state at the common final boundary l_max."""
+    returns every lane's state at the common final boundary l_max: bit for bit
+    the state a fixed-work run of l_max cycles returns, and (float64 state)
+    the oracle's at l_max.
+
+    The float32 potentials of a lane run far past its own depth are compared
+    with the oracle through their residual only: near a fixed point every
+    cycle repeats nearly the same rounding errors, which add up along the
+    slowest-contracting direction. Lane 4 of this window (eps 0.133, depth
+    103, residual still 3e-5 at cycle 1022) drifts by 8e-5 (vector kernel) to
+    1.9e-4 (matrix-core kernel) relative over 919 extra cycles, while its
+    residual stays within 2e-7 of the oracle's."""
     w = wl.make("c1")
     log("[case] modes on c1")
     ga = run_gpu(w, 1e-3, mode="active")
@@ -212,14 +233,18 @@ def test_modes_agree_and_account_slots():
     assert gs["stats"].slots_update == w.W * lmax
     sc = oracle.slot_counts(ga["depth"])
     assert sc["active"] == ga["stats"].slots_update and sc["static"] == gs["stats"].slots_update
+    log(f"[case] modes on c1: fixed work {lmax} cycles")
+    gf = run_gpu(w, 1e-30, max_iter=lmax)
+    for k in ("f", "g", "residual"):
+        assert np.array_equal(gs[k], gf[k]), k
     fixed = oracle.solve(w.X, w.Y, w.a, w.b, w.eps, 1e-3, n=w.n, m=w.m, fixed_iters=lmax)
-    for t in range(w.W):
-        scale = max(np.abs(fixed["f"][t]).max(), np.abs(fixed["g"][t]).max(), float(w.eps[t]))
-        err = max(np.abs(gs["f"][t] - fixed["f"][t]).max(),
-                  np.abs(gs["g"][t] - fixed["g"][t]).max()) / scale
-        assert err <= 1e-4, (t, err)
-        assert abs(gs["residual"][t] - fixed["residual"][t]) <= 1e-5
-        assert gs["residual"][t] <= 1e-3 + 1e-5
+    _static_at_lmax(w, gs, fixed, None)
+    log("[case] modes on c1: static, float64 state")
+    gp = run_gpu(w, 1e-3, mode="static", flags=F_PRECISE)
+    lp = int(gp["depth"].max())
+    if lp != lmax:
+        fixed = oracle.solve(w.X, w.Y, w.a, w.b, w.eps, 1e-3, n=w.n, m=w.m, fixed_iters=lp)
+    _static_at_lmax(w, gp, fixed, 1e-4)
 
 
 def test_bitwise_lane_independence_and_determinism():
@@ -241,17 +266,20 @@ def test_bitwise_lane_independence_and_determinism():
 
 @pytest.mark.parametrize("flags", [0, F_FORCE_VALU, F_PRECISE, F_MATERIALIZE],
                          ids=["mfma", "valu", "precise", "materialised"])
-def test_launch_layouts_are_bitwise_identical(flags):
+@pytest.mark.parametrize("cfg", ["c2", "c3"])
+def test_launch_layouts_are_bitwise_identical(cfg, flags):
     """The host picks the update kernel's work layout (row tiles and column
-    groups per wave) from each launch's width; a lane's bits must not depend
-    on it. Fixed work on full c2 lanes: the whole window (widest layout),
-    twenty lanes (middle layout) and four lanes (narrowest layout)."""
-    w = wl.make("c2")
-    log(f"[case] layouts flags={flags}: W=64 fixed work 12 cycles")
-    g = run_gpu(w, 1e-9, max_iter=12, flags=flags)
-    for lanes in (list(range(20)), [5, 17, 33, 60]):
-        log(f"[case] layouts flags={flags}: lanes {lanes[:4]}... ({len(lanes)})")
-        gs = run_gpu(wl.make("c2", lanes=lanes), 1e-9, max_iter=12, flags=flags)
+    groups per wave) from each launch's width and column count; a lane's bits
+    must not depend on it. Fixed work on full lanes in one sub-batch: the whole
+    window (widest layout), a middle subset (two groups per wave for c2's 1024
+    columns, four for c3's 512) and four lanes (narrowest layout)."""
+    w = wl.make(cfg)
+    log(f"[case] layouts {cfg} flags={flags}: W={w.W} fixed work 12 cycles")
+    g = run_gpu(w, 1e-9, max_iter=12, flags=flags, streams=1)
+    middle = list(range(20)) if cfg == "c2" else list(range(3, 123, 3))
+    for lanes in (middle, [5, 17, 33, 60]):
+        log(f"[case] layouts {cfg} flags={flags}: lanes {lanes[:4]}... ({len(lanes)})")
+        gs = run_gpu(wl.make(cfg, lanes=lanes), 1e-9, max_iter=12, flags=flags, streams=1)
         for q, t in enumerate(lanes):
             assert np.array_equal(gs["f"][q], g["f"][t]), (t, "f")
             assert np.array_equal(gs["g"][q], g["g"][t]), (t, "g")
@@ -403,7 +431,7 @@ def _tiny_lanes():
     return wl.Workload("tiny", X, Y, a, b, eps, n, m, 1e-4, 5000)
 
 
-@pytest.mark.parametrize("flags", [0, F_FORCE_MFMA], ids=["valu", "mfma"])
+@pytest.mark.parametrize("flags", [F_FORCE_VALU, 0], ids=["valu", "mfma"])
 def test_edge_single_points_and_tiny_lanes(flags):
     w = _tiny_lanes()
     _case("tiny", w, 1e-4, flags=flags)
