@@ -131,6 +131,59 @@ def test_features_full_size_sampled():
     assert abs(max(rr, rc) - g["residual"][t]) <= 1e-5
 
 
+def test_lidar_full_size_sampled():
+    """Full LiDAR-shaped window (W=1024; n, m uniform on 256..8192, padded to
+    8192; d=3; per-lane eps on 0.005..0.1; tol 1e-3) in its benchmark launch
+    configuration (three sub-batches, mixed lane shapes): (i) fixed work, 8
+    cycles: the lane nearest 2048 x 2048 points against the oracle's state;
+    (ii) a real solve: the six smallest lanes against the oracle (depths,
+    potentials, residuals), the largest lane's returned potentials
+    re-evaluated in float64 (its residual equals the reported one), and the
+    batch properties (statuses, slot identity, width trace, completion order)."""
+    w = wl.make("c5")
+    area = w.n.astype(np.int64) * w.m
+    t_mid = int(np.argmin(np.abs(area - 2048 * 2048)))
+    log(f"[case] c5 full size fixed work 8 cycles (lane {t_mid}: {w.n[t_mid]} x {w.m[t_mid]})")
+    g = run_gpu(w, 1e-9, max_iter=8)
+    assert np.all(g["depth"] == 8) and np.all(g["status"] == oracle.MAX_ITER)
+    nt, mt = int(w.n[t_mid]), int(w.m[t_mid])
+    fw = oracle.solve_lane(w.X[t_mid, :nt], w.Y[t_mid, :mt], w.a[t_mid, :nt], w.b[t_mid, :mt],
+                           w.eps[t_mid], 1e-9, fixed_iters=8)
+    scale = max(np.abs(fw["f"]).max(), np.abs(fw["g"]).max(), float(w.eps[t_mid]))
+    err = max(np.abs(g["f"][t_mid, :nt] - fw["f"]).max(),
+              np.abs(g["g"][t_mid, :mt] - fw["g"]).max()) / scale
+    log(f"  lane {t_mid}: pot err {err:.2e}, res gpu {g['residual'][t_mid]:.6e} "
+        f"or {fw['residual']:.6e}")
+    assert err <= 1e-4
+    assert abs(g["residual"][t_mid] - fw["residual"]) <= 1e-5
+    log("[case] c5 full size tol 1e-3")
+    g = run_gpu(w, 1e-3)
+    st = g["stats"]
+    assert st.sub_batches == 3
+    conv = g["status"] == oracle.CONVERGED
+    assert np.all(conv | ((g["status"] == oracle.MAX_ITER) & (g["depth"] == 5000)))
+    assert np.all(g["residual"][conv] <= 1e-3)
+    assert st.slots_update == int(g["depth"].sum())
+    assert list(g["order"]) == sorted(range(w.W), key=lambda t: (g["depth"][t], t))
+    small = [int(t) for t in np.argsort(area, kind="stable")[:6]]
+    o = run_oracle(w, 1e-3, lanes=small)
+    rep = compare(w, g, o, 1e-3, lanes=small, check_order=False)
+    log(f"  lanes {small}: depths {[int(g['depth'][t]) for t in small]} oracle "
+        f"{[int(o['depth'][t]) for t in small]} max_pot_err={rep['max_pot_err']:.2e} "
+        f"max_res_err={rep['max_res_err']:.2e} near_threshold={rep['near_threshold']}")
+    t = int(np.argmax(area))
+    nt, mt = int(w.n[t]), int(w.m[t])
+    C = oracle.sq_euclidean_cost(w.X[t, :nt], w.Y[t, :mt])
+    rr, rc = oracle.marginal_residuals(C, g["f"][t, :nt], g["g"][t, :mt],
+                                       w.a[t, :nt].astype(np.float64),
+                                       w.b[t, :mt].astype(np.float64), float(w.eps[t]))
+    log(f"  lane {t} ({nt} x {mt}): depth {g['depth'][t]} status {g['status'][t]} f64 residual "
+        f"of gpu state {max(rr, rc):.6e} reported {g['residual'][t]:.6e}")
+    assert abs(max(rr, rc) - g["residual"][t]) <= 1e-5
+    if conv[t]:
+        assert max(rr, rc) <= 1e-3 + 1e-5
+
+
 @pytest.mark.parametrize("name", ["c1", "c5"])
 def test_precise_state_small_cases(name):
     """Float64 state on the toy window and on NaN-padded heterogeneous lanes
