@@ -1394,23 +1394,29 @@ __global__ __launch_bounds__(256) void k_move(MoveArgs p) {
 // float64 from the caller's coordinates, the exponentials are float64: the
 // residual that decides a release is that of the potentials the caller receives
 // (eq:release-contract), to float64 rounding. Pass 0: row marginal (rows = x),
-// pass 1: column marginal (rows = y). Wave w takes rows w, w + nw, .. of the
-// item (nw waves); its lanes stride over the columns, whose exported potentials
-// are staged 256 at a time in LDS; a row's sum is a fixed-order butterfly over
-// the wave. Each block publishes its rows' sum of |marginal - mass| (row order);
-// the last block of the lane over both passes adds them in block order and takes
-// the decision. Launched between the f-half and the g-half of an audited cycle
-// (state k-1 is read-only there) and at the final audit.
-__device__ __forceinline__ double wave_sum64(double v) {
-#pragma unroll
-  for (int m = 32; m > 0; m >>= 1) v += __shfl_xor(v, m, 64);
-  return v;
-}
+// pass 1: column marginal (rows = y).
+//
+// Thread (r, p) of the block owns row r of the item and column phase p (every
+// NPH-th column); it keeps the row's coordinates in registers (DR >= d of them,
+// zero-padded; DR = 0: d > 32, read from memory per term). The columns'
+// coordinates and exported potentials are staged CH at a time in LDS, where
+// the lanes of a wave read the same column (a broadcast). A row's sum is its
+// phases' partial sums added in phase order. Each block publishes its rows' sum
+// of |marginal - mass| (row order); the last block of the lane over both
+// passes adds them in block order and takes the decision. Launched between the
+// f-half and the g-half of an audited cycle (state k-1 is read-only there) and
+// at the final audit.
+constexpr int kGuardThreads = 256;
+template <int DR>
+constexpr int guard_chunk() { return DR == 0 ? 256 : (2048 / DR < 256 ? 2048 / DR : 256); }
 
-constexpr int kGuardChunk = 256;
-
-__global__ __launch_bounds__(256) void k_check64(Launch L, GuardArgs G) {
-  __shared__ double sh_pot[kGuardChunk];
+template <int DR>
+__global__ __launch_bounds__(kGuardThreads) void k_check64(Launch L, GuardArgs G) {
+  constexpr int CH = guard_chunk<DR>();
+  constexpr int DS = DR == 0 ? 1 : DR;                       // staged coordinates per column
+  __shared__ double sh_y[DR == 0 ? 1 : CH * DS];
+  __shared__ double sh_pot[CH];
+  __shared__ double sh_acc[kGuardThreads];
   __shared__ double sh_row[64];
   __shared__ int sh_bad[64];
   const int b = blockIdx.x;
@@ -1430,69 +1436,82 @@ __global__ __launch_bounds__(256) void k_check64(Launch L, GuardArgs G) {
   }
   if (!item_live(L, P, s, si, c_fin, c_A) || !checked) return;
   const int lane_id = si.lane;
-  const int R = L.rows;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int nw = (int)blockDim.x >> 6;
+  const int R = L.rows;                        // 32 or 64 rows per item
+  const int nph = kGuardThreads / R;           // column phases
+  const int tid = threadIdx.x;
+  const int r = tid % R, ph = tid / R;
   const int d = G.d;
   const double inv_eps = 1.0 / (double)G.eps[lane_id];
   const float* wr = P.w_row + (size_t)lane_id * P.w_ld;
   const float* wc = G.w_col[pi] + (size_t)lane_id * G.w_ld_col[pi];
-  // wave w: rows w, w + nw, .. of the item (the same number of row steps in
-  // every wave); per row step the block stages the exported potentials of 256
-  // columns at a time in LDS, and the wave's lanes stride over them
-  const int steps = (R + nw - 1) / nw;
+  const float* ycol = G.xy_col[pi] + (size_t)lane_id * G.ld_col[pi] * d;
+  const int i = rb * R + r;
+  const bool live = i < nrows && wr[i] != 0.f;
+  const double fi = live ? (double)export_potential(P.gam_out, P.rec_row, (size_t)s * P.padr + i,
+                                                    L.dp, G.es, si)
+                         : 0.0;
+  const float* xi = G.xy_row[pi] + ((size_t)lane_id * G.ld_row[pi] + (live ? i : 0)) * d;
+  double xr[DS];
+#pragma unroll
+  for (int k = 0; k < DS; ++k) xr[k] = (DR != 0 && k < d) ? (double)xi[k] : 0.0;
+  double acc = 0.0;
 #pragma unroll 1
-  for (int q = 0; q < steps; ++q) {
-    const int r = wave + q * nw;
-    const int i = rb * R + r;
-    const bool live = r < R && i < nrows && wr[i] != 0.f;
-    const double fi = live ? (double)export_potential(P.gam_out, P.rec_row, (size_t)s * P.padr + i,
-                                                      L.dp, G.es, si)
-                           : 0.0;
-    const float* xi = G.xy_row[pi] + ((size_t)lane_id * G.ld_row[pi] + (live ? i : 0)) * d;
-    double acc = 0.0;
-#pragma unroll 1
-    for (int c0 = 0; c0 < ncols; c0 += kGuardChunk) {
-      __syncthreads();   // every wave is done with the previous chunk
-      if (tid < kGuardChunk) {
-        const int j = c0 + tid;
-        sh_pot[tid] = (j < ncols && wc[j] != 0.f)
-                          ? (double)export_potential(P.gam_col, P.rec_col, (size_t)s * P.padc + j,
-                                                     L.dp, G.es, si)
-                          : -(double)INFINITY;   // past the prefix or removed (zero mass)
+  for (int c0 = 0; c0 < ncols; c0 += CH) {
+    __syncthreads();   // every thread is done with the previous chunk
+    for (int t = tid; t < CH; t += kGuardThreads) {
+      const int j = c0 + t;
+      sh_pot[t] = (j < ncols && wc[j] != 0.f)
+                      ? (double)export_potential(P.gam_col, P.rec_col, (size_t)s * P.padc + j,
+                                                 L.dp, G.es, si)
+                      : -(double)INFINITY;   // past the prefix or removed (zero mass)
+    }
+    if (DR != 0) {
+      for (int e = tid; e < CH * DS; e += kGuardThreads) {
+        const int t = e / DS, k = e % DS;
+        sh_y[e] = (c0 + t < ncols && k < d) ? (double)ycol[(size_t)(c0 + t) * d + k] : 0.0;
       }
-      __syncthreads();
-      if (!live) continue;
+    }
+    __syncthreads();
+    if (!live) continue;
 #pragma unroll 1
-      for (int t = lane; t < kGuardChunk && c0 + t < ncols; t += 64) {
-        const double gj = sh_pot[t];
-        if (gj == -(double)INFINITY) continue;
-        const float* yj = G.xy_col[pi] + ((size_t)lane_id * G.ld_col[pi] + c0 + t) * d;
-        double C = 0.0;
-#pragma unroll 1
+    for (int t = ph; t < CH && c0 + t < ncols; t += nph) {
+      const double gj = sh_pot[t];
+      if (gj == -(double)INFINITY) continue;
+      double C = 0.0;
+      if (DR != 0) {
+#pragma unroll
+        for (int k = 0; k < DS; ++k) {
+          const double df = xr[k] - sh_y[t * DS + k];
+          C = fma(df, df, C);
+        }
+      } else {
+        const float* yj = ycol + (size_t)(c0 + t) * d;
+#pragma unroll 4
         for (int k = 0; k < d; ++k) {
           const double df = (double)xi[k] - (double)yj[k];
           C = fma(df, df, C);
         }
-        acc += exp((fi + gj - C) * inv_eps);
       }
+      acc += exp((fi + gj - C) * inv_eps);
     }
-    // row total (the same bits in every lane), |marginal - mass|
-    const double tot = wave_sum64(acc);
-    if (lane == 0 && r < R) {
-      sh_row[r] = live ? fabs(tot - (double)wr[i]) : 0.0;
-      sh_bad[r] = live && !isfinite(tot);
-    }
+  }
+  // row totals: the phases' partial sums in phase order, |marginal - mass|
+  sh_acc[tid] = acc;
+  __syncthreads();
+  if (ph == 0 && r < 64) {
+    double tot = 0.0;
+    for (int q = 0; q < nph; ++q) tot += sh_acc[q * R + r];
+    sh_row[r] = live ? fabs(tot - (double)wr[i]) : 0.0;
+    sh_bad[r] = live && !isfinite(tot);
   }
   __syncthreads();
   if (tid != 0) return;
   double part = 0.0;
   int bad = 0;
-  for (int r = 0; r < R; ++r) {
-    if (rb * R + r >= nrows) break;
-    part += sh_row[r];
-    bad |= sh_bad[r];
+  for (int q = 0; q < R; ++q) {
+    if (rb * R + q >= nrows) break;
+    part += sh_row[q];
+    bad |= sh_bad[q];
   }
   unsigned long long* dst =
       reinterpret_cast<unsigned long long*>(G.agg64[P.role] + (size_t)s * L.rbmax + rb);
@@ -1866,7 +1885,13 @@ hipError_t launch_update_mat(const Launch& a, int blocks, hipStream_t st, hipEve
 }
 hipError_t launch_check64(const Launch& a, const GuardArgs& g, int blocks, hipStream_t st) {
   if (blocks <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_check64, dim3(blocks), dim3(256), 0, st, a, g);
+  if (a.rows != 32 && a.rows != 64) return hipErrorInvalidValue;   // rows per item
+  const dim3 grid(blocks), block(kGuardThreads);
+  if (g.d <= 4) hipLaunchKernelGGL(k_check64<4>, grid, block, 0, st, a, g);
+  else if (g.d <= 8) hipLaunchKernelGGL(k_check64<8>, grid, block, 0, st, a, g);
+  else if (g.d <= 16) hipLaunchKernelGGL(k_check64<16>, grid, block, 0, st, a, g);
+  else if (g.d <= 32) hipLaunchKernelGGL(k_check64<32>, grid, block, 0, st, a, g);
+  else hipLaunchKernelGGL(k_check64<0>, grid, block, 0, st, a, g);
   return hipGetLastError();
 }
 hipError_t launch_cost(const CostArgs& a, hipStream_t st) {
