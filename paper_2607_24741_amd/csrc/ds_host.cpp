@@ -518,17 +518,18 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
       HIP_TRY(launch_check64(lc, ga, lc.nb0 + std::max(items[1], 0), st));
     }
     // g-half of cycle k (+ column check and decision for state k-1)
-    // (the check blocks come first: most of them exit at once)
+    // (the check blocks come last: most of them exit at once, and at the front
+    // they would delay the update blocks' dispatch)
     Launch lg = make_launch();
     const int vg = pick(items[1], 1);
     const int nbg = blocks_of(vg, 1, items[1]);
     int blocks = nbg;
     if (audit_prev && !guard) {
-      lg.p[0] = make_pass(1, 1, pk1, pk1, pk1);   // column marginal of state k-1
-      lg.p[0].decide = 1;
-      lg.p[0].verify_all = shadow ? 1 : 0;
-      lg.p[0].depth = k - 1;
-      lg.p[1] = make_pass(1, 0, pk1, pk, pk);     // g-half of cycle k
+      lg.p[0] = make_pass(1, 0, pk1, pk, pk);     // g-half of cycle k
+      lg.p[1] = make_pass(1, 1, pk1, pk1, pk1);   // column marginal of state k-1
+      lg.p[1].decide = 1;
+      lg.p[1].verify_all = shadow ? 1 : 0;
+      lg.p[1].depth = k - 1;
       lg.nb0 = nbg;
       blocks += nbg;
     } else {
