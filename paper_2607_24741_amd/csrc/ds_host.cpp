@@ -9,11 +9,15 @@
 //           block of each checked lane takes its decision on the device
 //           (verifier-gated: the screen alone never retires a lane) and a
 //           retired lane's work items stop running at once.
-// The host never waits per cycle: a snapshot of the control block is copied
-// back every few cycles, and when one shows retirements the host launches the
-// compaction (scan + gather into the other bank, with emission of the retired
-// lanes) so later launches run at the survivor width. The host runs at most a
-// bounded number of cycles ahead of the device.
+// With guarded release a float64 verification launch between the two halves
+// takes the decision instead of the float32 column check.
+// The host never waits per cycle: the device publishes its control state
+// (retirements, survivor widths, a progress word) to pinned host memory, and
+// when it shows retirements the host launches the compaction (scan + gather
+// into the other bank, with emission of the retired lanes) so later launches
+// run at the survivor width. The host runs at most a bounded number of cycles
+// ahead of the device. A call may be split into sub-batches (contiguous lane
+// ranges), each with this loop on its own host thread and stream.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>

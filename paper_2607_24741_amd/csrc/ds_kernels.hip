@@ -1,22 +1,32 @@
 // gfx950 kernels of the active-set batched Sinkhorn path (wave64, CDNA4).
 //
-//  k_update_mfma<DH>  one half-step of eq:sinkhorn-cycle for every (slot, row
-//                     block, column split) work item, x~.y~ on the fp32 matrix
-//                     cores (v_mfma_f32_32x32x2_f32) with the column potential and
-//                     the row anchor folded into the contraction, streaming
-//                     base-2 log-sum-exp on the vector ALU, fused row screen.
-//  k_update_valu<D>   the same half-step for small d on the vector ALU with the
-//                     column data wave-uniform (scalar loads, SGPR operands).
-//  k_scan             one block: screen/check decisions, wave-ballot +
-//                     prefix-sum compaction map, completion ranks, new work
-//                     item offsets (Sec. 3.2, Fig. fig:active-loop).
+//  k_update_mfma<DH, RT, GW, UNI>
+//                     one half-step of eq:sinkhorn-cycle for every (slot, row
+//                     block) work item: x~.y~ on the fp32 matrix cores
+//                     (v_mfma_f32_32x32x2_f32) with the column potential and the
+//                     row anchor folded into the contraction, streaming base-2
+//                     log-sum-exp on the vector ALU over 8 fixed column groups,
+//                     fused row screen; with a second pass in the same launch,
+//                     the column check and release decision (the default path
+//                     for every d <= 32).
+//  k_update_valu<D>   the same half-step on the vector ALU, column data
+//                     wave-uniform (scalar loads, SGPR operands); on request.
+//  k_update_f64<D>    the same half-step with the state in float64.
+//  k_cost, k_mat_rows, k_mat_cols
+//                     the materialised cost: built once on the matrix cores,
+//                     then streamed from HBM by both half-steps (d > 32).
+//  k_check64<DR>      float64 verification of the exported potentials (guarded
+//                     release).
+//  k_scan             one block: compaction map (survivor ranks, new work item
+//                     offsets) from the device-side decisions (Sec. 3.2).
 //  k_move             retiree emission in caller lane order + survivor gather
 //                     into the other bank (physical compaction, Sec. 3.2).
-//  k_ingest_*         validation, centring/scaling, log masses, cold start.
+//  k_ingest_*         validation, centring/scaling, log masses, proposals.
 //
 // Determinism: every reduction runs in a fixed order (no float atomics); the
-// split count and tile order of a lane depend only on its (n, m), so a lane's
-// bits do not depend on the batch width, its slot or its co-lanes.
+// column groups and tile order of a lane depend only on its (n, m), so a lane's
+// bits do not depend on the batch width, the launch layout, its slot or its
+// co-lanes.
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <math.h>
