@@ -358,7 +358,8 @@ __device__ void finish_rows(const Launch& L, const Pass& P, int s, const SlotInf
 // N = 8q + r items: every XCD works through one contiguous range of items --
 // whole lanes -- and its L2 holds only those lanes' column operands. The map
 // is a bijection of [0, N), so it changes which block runs an item, never
-// what the item computes.
+// what the item computes. Used for uniform lane shapes, where every item is
+// the same work.
 __device__ __forceinline__ int xcd_item(int b, int N) {
   const int q = N >> 3, r = N & 7, x = b & 7;
   return x * q + min(x, r) + (b >> 3);
@@ -407,6 +408,11 @@ __device__ __forceinline__ bool item_uniform(const Pass& P, int nb, int b, int& 
 
 // Mixed lane shapes: the item comes from the offsets table of the device-side
 // layout (slot s, first row block rb0); false when the block has no work.
+// Items are taken in block order, so consecutive items go to different XCDs:
+// with lanes of very different sizes, whole-lane ranges per XCD left the XCDs'
+// work 7-21 % apart at full width (the slowest one ends the launch), while
+// interleaved items balance it at the price of every XCD reading every lane's
+// column operands.
 __device__ __forceinline__ bool locate_item(const Launch& L, const Pass& P, int b, int& s,
                                             int& rb0, SlotInfo& si) {
   const Ctrl* c = L.ctrl;
@@ -415,7 +421,7 @@ __device__ __forceinline__ bool locate_item(const Launch& L, const Pass& P, int 
   if (!P.final_audit && fin) return false;
   const int N = P.off[A];
   if (b >= N) return false;
-  const int item = xcd_item(b, N);
+  const int item = b;
   s = find_slot(P.off, A, item);
   rb0 = item - P.off[s];
   si = L.slot[s];
