@@ -339,6 +339,33 @@ def test_launch_layouts_are_bitwise_identical(cfg, flags):
             assert gs["residual"][q] == g["residual"][t], t
 
 
+def test_mixed_shape_layouts_are_bitwise_identical():
+    """Mixed lane shapes (offsets-table placement): the whole window runs the
+    four-groups-per-wave layout (at most 512 columns, over 512 work items per
+    launch), four lanes the narrowest one; a lane's bits must not change, and
+    fixed work matches the oracle on sampled lanes."""
+    w = wl.make("c5", W=64, n=512, m=480, hetero=(40, 512))
+    log("[case] mixed-shape layouts: W=64 fixed work 12 cycles")
+    g = run_gpu(w, 1e-9, max_iter=12, streams=1)
+    lanes = [2, 19, 40, 63]
+    log(f"[case] mixed-shape layouts: lanes {lanes}")
+    gs = run_gpu(wl.make("c5", lanes=lanes, n=512, m=480, hetero=(40, 512)), 1e-9, max_iter=12,
+                 streams=1)
+    for q, t in enumerate(lanes):
+        assert np.array_equal(gs["f"][q], g["f"][t]), (t, "f")
+        assert np.array_equal(gs["g"][q], g["g"][t]), (t, "g")
+        assert gs["residual"][q] == g["residual"][t], t
+    for t in lanes[:2]:
+        nt, mt = int(w.n[t]), int(w.m[t])
+        fw = oracle.solve_lane(w.X[t, :nt], w.Y[t, :mt], w.a[t, :nt], w.b[t, :mt], w.eps[t], 1e-9,
+                               fixed_iters=12)
+        scale = max(np.abs(fw["f"]).max(), np.abs(fw["g"]).max(), float(w.eps[t]))
+        err = max(np.abs(g["f"][t, :nt] - fw["f"]).max(),
+                  np.abs(g["g"][t, :mt] - fw["g"]).max()) / scale
+        assert err <= 1e-4, (t, err)
+        assert abs(g["residual"][t] - fw["residual"]) <= 1e-5
+
+
 @pytest.mark.parametrize("cfg", ["c2", "c5"])
 def test_sub_batches_are_bitwise_identical(cfg):
     """Sub-batches (concurrent lane ranges, each with its own control loop and
