@@ -198,3 +198,51 @@ def make(name, *, W=None, n=None, m=None, lanes=None, pad_value=0.0, seed=SEED,
     return Workload(name=name, X=X, Y=Y, a=A, b=B, eps=E, n=N, m=M, tol=cfg["tol"],
                     max_iter=cfg["max_iter"],
                     meta=dict(lanes=lanes, seed=seed, description=DESCRIPTIONS[name]))
+
+
+# ------------------------------------------------------- randomised windows
+def random_window(k, *, seed=SEED):
+    """Randomised small window number ``k`` for parity sweeps: W in 1..12,
+    padded sizes n_max, m_max in 1..320 with per-lane n_t, m_t in 1..n_max
+    (m_max), d in 1..40, point clouds that are Gaussian or uniform at a random
+    scale s (offsets ~ N(0, s^2 I)), Dirichlet(alpha) masses with alpha in
+    {0.3, 1, 5}, and per-lane eps = 2 d s^2 logU(0.02, 0.2) (mean costs of 10
+    to 100 eps). Also returns the run options drawn for the case: tol,
+    audit_every, flags and sub-batch count. NaN-padded."""
+    rng = np.random.default_rng(np.random.SeedSequence([seed, 900, k]))
+    W = int(rng.integers(1, 13))
+    n_max = int(rng.integers(1, 321))
+    m_max = int(rng.integers(1, 321))
+    d = int(rng.integers(1, 41))
+    X = np.full((W, n_max, d), np.nan, dtype=np.float32)
+    Y = np.full((W, m_max, d), np.nan, dtype=np.float32)
+    A = np.full((W, n_max), np.nan, dtype=np.float32)
+    B = np.full((W, m_max), np.nan, dtype=np.float32)
+    E = np.zeros(W, dtype=np.float32)
+    N = np.zeros(W, dtype=np.int32)
+    M = np.zeros(W, dtype=np.int32)
+    for t in range(W):
+        nt, mt = int(rng.integers(1, n_max + 1)), int(rng.integers(1, m_max + 1))
+        s = float(np.exp(rng.uniform(np.log(0.2), np.log(3.0))))
+        def cloud(cnt):   # unit-variance shape at scale s, offset ~ N(0, s^2 I)
+            if rng.random() < 0.5:
+                return s * (rng.standard_normal((cnt, d)) + rng.standard_normal(d))
+            return s * (rng.uniform(-1.7, 1.7, size=(cnt, d)) + rng.standard_normal(d))
+        alpha = float(rng.choice([0.3, 1.0, 5.0]))
+        X[t, :nt] = cloud(nt)
+        Y[t, :mt] = cloud(mt)
+        A[t, :nt] = _dirichlet(rng, alpha, nt)
+        B[t, :mt] = _dirichlet(rng, alpha, mt)
+        E[t] = 2.0 * d * s * s * float(np.exp(rng.uniform(np.log(0.02), np.log(0.2))))
+        N[t], M[t] = nt, mt
+    tol = float(rng.choice([1e-2, 1e-3]))
+    audit_every = int(rng.integers(1, 4))
+    flags = int(rng.choice([0, 0, 4, 16, 32, 64]))   # default, vector ALU, float64, materialised, guarded
+    if d > 32:
+        flags = 0 if flags != 64 else 64               # d > 32 is always materialised
+    if d > 16 and flags == 16:
+        flags = 0                                      # the float64 state supports d <= 16
+    streams = int(rng.choice([0, 1, 2])) if W >= 2 else 0
+    w = Workload(name=f"random{k}", X=X, Y=Y, a=A, b=B, eps=E, n=N, m=M, tol=tol, max_iter=2000,
+                 meta=dict(seed=seed, description="randomised small window"))
+    return w, dict(tol=tol, audit_every=audit_every, flags=flags, streams=streams)

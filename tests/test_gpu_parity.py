@@ -475,6 +475,22 @@ def test_guarded_release_mixed_shapes_and_final_audit():
     _certified(w, g, 1e-3, range(w.W))
 
 
+@pytest.mark.parametrize("k", range(24))
+def test_randomised_windows(k):
+    """Seeded random small windows (W 1..12, sizes 1..320 per lane, d 1..40,
+    Gaussian or uniform clouds, Dirichlet(0.3 / 1 / 5) masses, tol 1e-2 or
+    1e-3, audit every 1-3 cycles, default / vector-ALU / float64 /
+    materialised / guarded paths, 0-2 sub-batches) against the oracle."""
+    w, opt = wl.random_window(k)
+    flags, streams = opt["flags"], opt["streams"]
+    res_atol = GUARD_RES_ATOL if flags == F_GUARD else None
+    g, o, rep = _case(f"random{k}", w, opt["tol"], flags=flags, res_atol=res_atol,
+                      audit_every=opt["audit_every"], max_iter=w.max_iter, streams=streams)
+    assert np.all(g["status"] == oracle.CONVERGED)
+    if flags == F_GUARD:
+        _certified(w, g, opt["tol"], range(w.W))
+
+
 def test_padding_isolation():
     log("[case] NaN vs zero padding")
     wn = wl.make("c5", W=6, n=300, m=300, hetero=(30, 300), pad_value=np.nan)

@@ -48,3 +48,25 @@ def test_heterogeneous_sizes_and_nan_padding():
         assert np.all(np.isnan(w.X[t, w.n[t]:])) and np.all(np.isfinite(w.X[t, :w.n[t]]))
         assert np.all(np.isnan(w.a[t, w.n[t]:]))
     assert np.all((w.eps >= 0.005 - 1e-7) & (w.eps <= 0.1 + 1e-7))
+
+
+def test_random_windows_are_seeded_and_well_formed():
+    for k in range(24):
+        w, opt = wl.random_window(k)
+        w2, opt2 = wl.random_window(k)
+        assert opt == opt2
+        for f in ("X", "Y", "a", "b", "eps", "n", "m"):
+            assert np.array_equal(getattr(w, f), getattr(w2, f), equal_nan=True)
+        assert 1 <= w.W <= 12 and 1 <= w.d <= 40
+        assert opt["flags"] in (0, 4, 16, 32, 64) and opt["audit_every"] in (1, 2, 3)
+        if w.d > 16:
+            assert opt["flags"] != 16
+        if w.d > 32:
+            assert opt["flags"] in (0, 64)
+        for t in range(w.W):
+            nt, mt = int(w.n[t]), int(w.m[t])
+            assert 1 <= nt <= w.X.shape[1] and 1 <= mt <= w.Y.shape[1]
+            assert abs(w.a[t, :nt].astype(np.float64).sum() - 1) < 1e-5
+            assert abs(w.b[t, :mt].astype(np.float64).sum() - 1) < 1e-5
+            assert np.all(np.isfinite(w.X[t, :nt])) and np.all(np.isnan(w.X[t, nt:]))
+            assert np.all(np.isnan(w.b[t, mt:])) and w.eps[t] > 0
