@@ -257,8 +257,10 @@ struct PartOut {
   size_t ws_bytes = 0;
 };
 
+// lane_base: the caller's index of this sub-batch's first lane (error messages
+// name lanes by the caller's index)
 ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* res, void* ws,
-                  hipStream_t st, DeviceRes* R, PartOut& out) {
+                  hipStream_t st, DeviceRes* R, PartOut& out, int lane_base) {
   using namespace ds;
   Layout L = plan(pr, op, ws);
   const int W = pr->W, d = pr->d;
@@ -300,7 +302,7 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
     const char* what = ctrl.err_code == 1 ? "n out of range [1, n_max]"
                      : ctrl.err_code == 2 ? "m out of range [1, m_max]"
                                           : "eps not finite and > 0";
-    return fail(DS_E_INVALID, "lane " + std::to_string(ctrl.err_lane) + ": " + what);
+    return fail(DS_E_INVALID, "lane " + std::to_string(lane_base + ctrl.err_lane) + ": " + what);
   }
   if (mat) {
     CostArgs ca;
@@ -748,7 +750,7 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
     const ds_problem sp = sub_problem(pr, lo, hi);
     const ds_result sr = sub_result(pr, res, lo);
     hipStream_t s = p == 0 ? st : Rs[p]->stream;
-    errs[p] = solve_part(&sp, op, &sr, static_cast<char*>(ws) + off[p], s, Rs[p], outs[p]);
+    errs[p] = solve_part(&sp, op, &sr, static_cast<char*>(ws) + off[p], s, Rs[p], outs[p], lo);
     if (errs[p] != DS_OK) msgs[p] = g_last_error;
     if (p > 0 && errs[p] == DS_OK) {
       const hipError_t he = hipEventRecord(Rs[p]->join_ev, s);
@@ -761,8 +763,14 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
     work(0);
     for (auto& t : th) t.join();
   }
-  for (int p = 0; p < parts; ++p)
-    if (errs[p] != DS_OK) return fail(errs[p], msgs[p]);
+  for (int p = 0; p < parts; ++p) {
+    if (errs[p] == DS_OK) continue;
+    // drain every sub-batch's stream before its resources go back to the pool
+    // (the outputs are undefined after an error, the workspace must be idle)
+    (void)hipStreamSynchronize(st);
+    for (int q = 1; q < parts; ++q) (void)hipStreamSynchronize(Rs[q]->stream);
+    return fail(errs[p], msgs[p]);
+  }
   for (int p = 1; p < parts; ++p) HIP_TRY(hipStreamWaitEvent(st, Rs[p]->join_ev, 0));
   if (res->order) HIP_TRY(launch_order(res->depth, W, res->order, st));
   std::vector<int32_t> depth(W), status(W);

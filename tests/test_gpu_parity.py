@@ -577,3 +577,13 @@ def test_invalid_lane_data_is_a_call_error():
     with pytest.raises(ds.DSError) as ei:
         run_gpu(w, 1e-4)
     assert ei.value.code == 1 and "lane 4" in str(ei.value)
+    # in the second of two sub-batches: named by the caller's lane index, and
+    # the library stays usable afterwards
+    log("[case] invalid eps in a second sub-batch")
+    w = _tiny_lanes()
+    w.eps[3] = float("nan")
+    with pytest.raises(ds.DSError) as ei:
+        run_gpu(w, 1e-4, streams=2)
+    assert ei.value.code == 1 and "lane 3" in str(ei.value)
+    g = run_gpu(_tiny_lanes(), 1e-4, streams=2)
+    assert g["stats"].sub_batches == 2 and np.all(g["status"] == oracle.CONVERGED)
