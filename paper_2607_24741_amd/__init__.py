@@ -208,6 +208,9 @@ def solve(X, Y, a, b, eps, tol, *, n=None, m=None, g0=None, max_iter=5000, audit
     _check(lib, lib.ds_workspace_bytes(ctypes.byref(pr), ctypes.byref(op), ctypes.byref(need)))
     if workspace is None:
         workspace = torch.empty(int(need.value) + 256, dtype=torch.uint8, device=dev)
+    elif (workspace.dtype != torch.uint8 or not workspace.is_contiguous()
+          or workspace.device != dev):
+        raise ValueError(f"workspace must be a contiguous uint8 tensor on {dev}")
     base = workspace.data_ptr()
     shift = (-base) % 256
     ws_ptr, ws_bytes = base + shift, workspace.numel() - shift
