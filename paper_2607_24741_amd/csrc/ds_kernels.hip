@@ -478,13 +478,16 @@ __device__ __forceinline__ bool place_item(const Launch& L, const Pass& P, int n
 // tile is reduced.
 //
 // The second launch bound is the minimum number of waves per SIMD the register
-// allocation must allow (measured per layout: fewer, longer waves want more
-// registers than spills).
+// allocation must allow, chosen per layout and dh so that no variant spills
+// vector registers to scratch and the scalar spills stay at the few every
+// variant has: at 8 waves (64 registers) the two-group layout spilled 79
+// scalar registers into vector lanes, some 250 extra lane read/write
+// instructions per wave (c2 3 % slower than at 6 waves).
 template <int DH, int RT, int GW>
 constexpr int mfma_waves_per_simd() {
   return (kGroups / GW) == 8 ? (DH <= 7 ? 4 : 2)
-       : (kGroups / GW) == 2 ? (DH <= 7 ? 6 : 4)
-       : (RT == 1 ? (DH <= 7 ? 8 : (DH <= 12 ? 6 : 4)) : (DH <= 8 ? 4 : 2));
+       : (kGroups / GW) == 2 ? (DH <= 7 ? 5 : 4)
+       : (RT == 1 ? (DH <= 5 ? 6 : (DH <= 10 ? 5 : 4)) : (DH <= 8 ? 4 : 2));
 }
 
 // UNI: compiled for uniform lane shapes (work item -> slot by division) or
@@ -624,7 +627,7 @@ void k_update_mfma(Launch L) {
   auto sweep = [&](bool anchored) {
     bool have = ta < tb;
     int t = ta;
-#pragma unroll
+#pragma unroll (GW > 2 ? 1 : GW)   // four groups unrolled: 25 scalar spills
     for (int u = 0; u < GW; ++u) {
       const int t1 = min(ct, (g0 + u + 1) * tpg);
       reset();
