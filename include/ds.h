@@ -143,8 +143,9 @@ typedef struct {
  * independent, so every output is bit-identical to the one-batch solve; the
  * launch latencies of one sub-batch overlap the work of the others. Automatic:
  * one sub-batch below 32 lanes, in the static and logical modes (they share
- * one final cycle across the window) and with the materialised cost; two
- * from 32 lanes; three from 48. ds_workspace_bytes accounts for the split. */
+ * one final cycle across the window) and with the materialised cost;
+ * otherwise three when W * n_max * m_max * (2 ceil(d/2) + 2) >= 8e8, else
+ * two. ds_workspace_bytes accounts for the split. */
 
 /* Outputs, in caller lane order. Device pointers. */
 typedef struct {
