@@ -491,6 +491,29 @@ def test_randomised_windows(k):
         _certified(w, g, opt["tol"], range(w.W))
 
 
+@pytest.mark.parametrize("flags", [F_FORCE_VALU, 0], ids=["valu", "mfma"])
+@pytest.mark.parametrize("d", [1, 2])
+def test_low_dimensional_lanes(d, flags):
+    """d = 1 and 2 (a contraction of K = 4 on the matrix cores, the smallest
+    augmented vectors): ragged lanes against the oracle."""
+    rng = np.random.default_rng(11 + d)
+    W, n_max, m_max = 5, 150, 130
+    n = np.array([150, 37, 1, 90, 64], dtype=np.int32)
+    m = np.array([130, 1, 41, 77, 128], dtype=np.int32)
+    X = np.full((W, n_max, d), np.nan, np.float32)
+    Y = np.full((W, m_max, d), np.nan, np.float32)
+    a = np.full((W, n_max), np.nan, np.float32)
+    b = np.full((W, m_max), np.nan, np.float32)
+    for t in range(W):
+        X[t, :n[t]] = rng.standard_normal((n[t], d))
+        Y[t, :m[t]] = rng.standard_normal((m[t], d)) * 1.5 + 0.7
+        aa = rng.gamma(1.0, size=n[t]); a[t, :n[t]] = aa / aa.sum()
+        bb = rng.gamma(1.0, size=m[t]); b[t, :m[t]] = bb / bb.sum()
+    eps = np.array([0.1, 0.3, 0.05, 0.2, 0.08], np.float32)
+    w = wl.Workload(f"d{d}", X, Y, a, b, eps, n, m, 1e-3, 5000)
+    _case(f"d{d}", w, 1e-3, flags=flags)
+
+
 def test_padding_isolation():
     log("[case] NaN vs zero padding")
     wn = wl.make("c5", W=6, n=300, m=300, hetero=(30, 300), pad_value=np.nan)
