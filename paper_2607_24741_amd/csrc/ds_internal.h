@@ -42,7 +42,7 @@ constexpr float kFastRangePrecise = 1.f;  // the same for the float64 state
 constexpr int kMaxTimed = 4096;     // timed launches per sub-batch (DS_F_TIMING)
 // launch-variant thresholds (work items of the launch, see launch_update)
 constexpr int kWideItems = 1536;
-constexpr int kMediumItemsMfma = 512;
+constexpr int kMediumItemsMfma = 384;
 constexpr int kMediumItemsValu = 256;
 
 // Per physical slot lane descriptor; moved by compaction with the rest of the
