@@ -402,15 +402,10 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
   }
   auto pick = [&](int items, int role) -> int {
     if (mat) return VAR_MEDIUM;   // one layout: 64-row items, one block each
-    if (use_mfma && uniform && items >= kWideItems) return VAR_WIDE;
     if (items < (use_mfma ? kMediumItemsMfma : kMediumItemsValu)) return VAR_NARROW;
     return (use_mfma && tpg[role] <= 2) ? VAR_MEDIUM4 : VAR_MEDIUM;
   };
-  auto blocks_of = [&](int variant, int role, int items) -> int {
-    if (variant != VAR_WIDE || items <= 0) return std::max(items, 0);
-    const int lanes_ub = (items + ipl[role] - 1) / ipl[role];
-    return lanes_ub * ((ipl[role] + 1) / 2);
-  };
+  auto blocks_of = [&](int items) -> int { return std::max(items, 0); };
   int seqno = 0;   // update launches issued (see HostSnap::progress)
   auto run = [&](Launch l, int variant, int blocks, bool sample, int cycle, int kind) -> ds_err {
     l.seqno = ++seqno;
@@ -507,7 +502,7 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
     lf.p[0] = make_pass(0, 0, pk1, pk, pk1);
     lf.p[0].depth = k - 1;
     const int vf = pick(items[0], 0);
-    lf.nb0 = blocks_of(vf, 0, items[0]);
+    lf.nb0 = blocks_of(items[0]);
     ds_err r = run(lf, vf, lf.nb0, sample, k, 0);
     if (r != DS_OK) return r;
     if (audit_prev && guard) {
@@ -528,7 +523,7 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
     // they would delay the update blocks' dispatch)
     Launch lg = make_launch();
     const int vg = pick(items[1], 1);
-    const int nbg = blocks_of(vg, 1, items[1]);
+    const int nbg = blocks_of(items[1]);
     int blocks = nbg;
     if (audit_prev && !guard) {
       lg.p[0] = make_pass(1, 0, pk1, pk, pk);     // g-half of cycle k
@@ -574,14 +569,14 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
       lv.p[0] = make_pass(0, 1, pK, pK, pK);
       lv.p[0].final_audit = 1; lv.p[0].depth = K; lv.p[0].verify_all = 1;
       const int vv = pick(ctrl.items_f, 0);
-      lv.nb0 = blocks_of(vv, 0, ctrl.items_f);
+      lv.nb0 = blocks_of(ctrl.items_f);
       ds_err r = run(lv, vv, lv.nb0, true, K, 1);
       if (r != DS_OK) return r;
       Launch lw = make_launch();
       lw.p[0] = make_pass(1, 1, pK, pK, pK);
       lw.p[0].final_audit = 1; lw.p[0].decide = 1; lw.p[0].depth = K; lw.p[0].verify_all = 1;
       const int vw = pick(ctrl.items_g, 1);
-      lw.nb0 = blocks_of(vw, 1, ctrl.items_g);
+      lw.nb0 = blocks_of(ctrl.items_g);
       r = run(lw, vw, lw.nb0, true, K, 1);
       if (r != DS_OK) return r;
     }

@@ -41,7 +41,6 @@ constexpr float kFastRange = 64.f;  // max spread of the bound (log2 units) for 
 constexpr float kFastRangePrecise = 1.f;  // the same for the float64 state
 constexpr int kMaxTimed = 4096;     // timed launches per sub-batch (DS_F_TIMING)
 // launch-variant thresholds (work items of the launch, see launch_update)
-constexpr int kWideItems = 1536;
 constexpr int kMediumItemsMfma = 384;
 constexpr int kMediumItemsValu = 256;
 
@@ -254,7 +253,6 @@ struct IngestArgs {
 // over waves. All variants compute identical bits; the host picks one by width.
 enum { VAR_NARROW = 0,   // 32-row items, one group per wave (8 waves)
        VAR_MEDIUM = 1,   // 32-row items, two groups per wave (4 waves)
-       VAR_WIDE = 2,     // 64-row items (uniform lane shapes only), two groups per wave
        VAR_MEDIUM4 = 3 };  // 32-row items, four groups per wave (2 waves): matrix-core
                            // kernel, lanes of at most 2 column tiles per group
 // e0 / e1 (may be null): events that record the kernel's own start and end

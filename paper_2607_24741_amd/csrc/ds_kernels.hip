@@ -1782,13 +1782,12 @@ template <int DH>
 static hipError_t launch_mfma_dh(const Launch& a, int variant, int blocks, hipStream_t st,
                                  hipEvent_t e0, hipEvent_t e1) {
   const bool uni = a.p[0].ipl > 0;   // both passes of a launch share the shapes
-  if (variant == VAR_WIDE && !uni) return hipErrorInvalidValue;
   if (uni) {
     switch (variant) {
       case VAR_NARROW: hipExtLaunchKernelGGL((k_update_mfma<DH, 1, 1, true>), dim3(blocks), dim3(512), 0, st, e0, e1, 0, a); break;
       case VAR_MEDIUM: hipExtLaunchKernelGGL((k_update_mfma<DH, 1, 2, true>), dim3(blocks), dim3(256), 0, st, e0, e1, 0, a); break;
       case VAR_MEDIUM4: hipExtLaunchKernelGGL((k_update_mfma<DH, 1, 4, true>), dim3(blocks), dim3(128), 0, st, e0, e1, 0, a); break;
-      default: hipExtLaunchKernelGGL((k_update_mfma<DH, 2, 2, true>), dim3(blocks), dim3(256), 0, st, e0, e1, 0, a); break;
+      default: return hipErrorInvalidValue;
     }
   } else if (variant == VAR_NARROW) {
     hipExtLaunchKernelGGL((k_update_mfma<DH, 1, 1, false>), dim3(blocks), dim3(512), 0, st, e0, e1, 0, a);

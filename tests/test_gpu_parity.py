@@ -324,8 +324,8 @@ def test_launch_layouts_are_bitwise_identical(cfg, flags):
     """The host picks the update kernel's work layout (row tiles and column
     groups per wave) from each launch's width and column count; a lane's bits
     must not depend on it. Fixed work on full lanes in one sub-batch: the whole
-    window (widest layout), a middle subset (two groups per wave for c2's 1024
-    columns, four for c3's 512) and four lanes (narrowest layout)."""
+    window and a middle subset (two groups per wave for c2's 1024 columns, four
+    for c3's 512) against four lanes (one group per wave)."""
     w = wl.make(cfg)
     log(f"[case] layouts {cfg} flags={flags}: W={w.W} fixed work 12 cycles")
     g = run_gpu(w, 1e-9, max_iter=12, flags=flags, streams=1)
