@@ -432,7 +432,6 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
   hs->items_act_f = items[0]; hs->items_act_g = items[1];
   hs->progress = 0;
   int epoch = 0;
-  bool finished = false;
   int launched = 0;
   int compactions = 0;
   int64_t bytes_compacted = 0;  // upper bound: survivors x per-lane state bytes
@@ -465,7 +464,7 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
     const int s_fin = hs->finished, s_ep = hs->epoch, s_ret = hs->n_retired;
     const int s_cmp = hs->compacted, s_act = hs->n_active;
     const int s_itf = hs->items_act_f, s_itg = hs->items_act_g;
-    if (s_fin) { finished = true; break; }
+    if (s_fin) break;
     if (active && s_ep == epoch && s_ret > s_cmp) {
       // physical compaction: survivors gathered into the other bank
       epoch++;
@@ -493,7 +492,7 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
       items[1] = std::min(items[1], s_itg);
       compactions++;
     }
-    if (A <= 0) { finished = true; break; }
+    if (A <= 0) break;
     const int pk = k & 1, pk1 = (k - 1) & 1;
     const bool sample = (k % kSampleEvery) == 0;
     const bool audit_prev = (k - 1 >= 1) && ((k - 1) % ae == 0);

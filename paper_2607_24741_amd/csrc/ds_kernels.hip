@@ -497,8 +497,8 @@ __global__ __launch_bounds__(64 * (kGroups / GW), (mfma_waves_per_simd<DH, RT, G
 void k_update_mfma(Launch L) {
   note_progress(L);
   static_assert(UNI || RT == 1, "two row tiles per item need uniform lane shapes");
-  constexpr int NW = kGroups / GW;
   constexpr int ROWS = 32 * RT;
+  constexpr int kUnrollGroups = GW > 2 ? 1 : GW;   // four groups unrolled: 25 scalar spills
   constexpr int DP = 2 * DH;
   __shared__ float2 sh_part[kGroups][2][ROWS];
   const int b = blockIdx.x;
@@ -627,7 +627,7 @@ void k_update_mfma(Launch L) {
   auto sweep = [&](bool anchored) {
     bool have = ta < tb;
     int t = ta;
-#pragma unroll (GW > 2 ? 1 : GW)   // four groups unrolled: 25 scalar spills
+#pragma unroll kUnrollGroups
     for (int u = 0; u < GW; ++u) {
       const int t1 = min(ct, (g0 + u + 1) * tpg);
       reset();
@@ -809,7 +809,7 @@ void k_update_valu(Launch L) {
 // v_exp_f32, and the sums run in float64. Anchored sums are used only when
 // the bound's spread is at most kFastRangePrecise.
 template <int D, int GW>
-__global__ __launch_bounds__(64 * (kGroups / GW), (kGroups / GW == 8 ? 2 : 4))
+__global__ __launch_bounds__(64 * (kGroups / GW), (kGroups / GW == 8 ? 2 : (D >= 15 ? 3 : 4)))
 void k_update_f64(Launch L) {
   note_progress(L);
   constexpr int DPc = D + (D & 1);
