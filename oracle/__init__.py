@@ -21,8 +21,8 @@ What it computes (DrainSinkhorn, arxiv 2607.24741):
 * eq:slot-identity / eq:removable-slots (Sec. 4.1, Prop. 1) -- the slot
   accounting of static versus shrinking active execution.
 
-Readings of points the paper leaves open are listed in the design doc; each one is
-restated at the function that takes it.
+Each reading of a point the paper leaves open is stated at the function that
+takes it.
 
 Parity status: every public function here is pinned by tests in
 ``tests/test_oracle_pins.py`` against closed forms, brute-force dense scaling,

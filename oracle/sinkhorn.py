@@ -94,7 +94,7 @@ def solve_lane(x, y, a, b, eps, tol, *, max_iter=5000, audit_every=1,
     """Solve one lane from a proposal (cold by default) and stop on the
     two-sided audit.
 
-    Readings taken (each listed in the design doc):
+    Readings taken:
       * cold proposal f = g = 0 (all formal runs use cold proposals, Sec. 5 /
         tab:workload-configs); f is updated first (eq:sinkhorn-cycle), which
         fixes the gauge (f + c, g - c) of Sec. 4.2 -- no normalisation applied;

@@ -12,8 +12,8 @@ those same float32 bytes.
 
 The paper's datasets (MetroPT-3 telemetry, Packer19 scRNA, ImageNet-32 PCA500
 features, A2D2 LiDAR) are not available; the recipes below are stand-ins with
-the shapes, sizes and value structure of those workloads (see the design doc for the
-recipe table and the readings taken where the shape description is open).
+the shapes, sizes and value structure of those workloads; where the paper's
+description of a workload is open, the choice is stated in the recipe's docstring.
 """
 
 from __future__ import annotations

@@ -1,7 +1,7 @@
 """Helpers for the GPU parity tests: run a seeded workload through the C ABI
 and compare with the float64 oracle on the same float32 bytes.
 
-Parity bar (readings of the stated tolerances; see DESIGN.md):
+Parity bar (readings of the stated tolerances):
   * potentials: max_i |f_gpu - f_or| / max(||f_or||_inf, ||g_or||_inf, eps) <= 1e-4
     (likewise for g);
   * residuals: |r_gpu - r_or| <= 1e-5 absolute;
@@ -11,8 +11,8 @@ Parity bar (readings of the stated tolerances):
     bound (every audit at which the GPU continued has r_or >= tol - 1e-5, and
     the audit at which it stopped has r_or <= tol + 1e-5); such a lane is then
     compared at fixed work (the oracle's state at the GPU's depth). Lanes whose
-    margin exceeds 1e-6 are counted (fp32 cannot resolve residuals to 1e-6;
-    the design doc states this reading).
+    margin exceeds 1e-6 are counted (fp32 cannot resolve residuals to 1e-6,
+    so the 1e-6 band is reported rather than enforced).
 """
 
 from __future__ import annotations
