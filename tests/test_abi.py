@@ -55,6 +55,7 @@ def test_workspace_query_and_validation():
     for bad in (dict(W=0), dict(n_max=0), dict(m_max=-1), dict(d=0), dict(d=513)):
         assert _bytes(_problem(**bad), op)[0] == 1, bad
     assert _bytes(_problem(W=5000), op)[0] == 4
+    assert _bytes(_problem(W=4096), op)[0] == 0 and _bytes(_problem(W=4097), op)[0] == 4
     for tol, mi, ae, mode in ((0.0, 10, 1, 0), (1e-3, 0, 1, 0), (1e-3, 10, 0, 0), (1e-3, 10, 1, 7)):
         o = ds._Options(tol=tol, screen_tol=0.0, max_iter=mi, audit_every=ae, mode=mode, flags=0)
         assert _bytes(_problem(), o)[0] == 1

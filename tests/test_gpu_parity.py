@@ -573,6 +573,51 @@ def test_edge_max_iter_and_single_lane():
     _case("w1", one, 1e-3)
 
 
+def _max_width_lanes(eps_lo, eps_hi, max_iter, W=4096, seed=11):
+    """The widest call the library accepts (4096 lanes): small ragged lanes
+    (1 to 48 points a side, some with a single point), d = 3, eps per lane
+    log-uniform in [eps_lo, eps_hi]."""
+    rng = np.random.default_rng(seed)
+    n_max = m_max = 48
+    d = 3
+    X = rng.standard_normal((W, n_max, d)).astype(np.float32)
+    Y = (rng.standard_normal((W, m_max, d)) + 0.5).astype(np.float32)
+    n = rng.integers(1, n_max + 1, size=W).astype(np.int32)
+    m = rng.integers(1, m_max + 1, size=W).astype(np.int32)
+    n[-1], m[-1] = n_max, m_max
+    a = np.zeros((W, n_max), np.float32)
+    b = np.zeros((W, m_max), np.float32)
+    for t in range(W):
+        aa = rng.gamma(1.0, size=n[t]); a[t, :n[t]] = aa / aa.sum()
+        bb = rng.gamma(1.0, size=m[t]); b[t, :m[t]] = bb / bb.sum()
+    eps = np.exp(rng.uniform(np.log(eps_lo), np.log(eps_hi), size=W)).astype(np.float32)
+    return wl.Workload("max-width", X, Y, a, b, eps, n, m, 1e-3, max_iter)
+
+
+def test_edge_max_width():
+    # every lane against the oracle at the width limit, with the automatic
+    # sub-batch split; eps in [0.25, 1] lets every lane complete within the cap
+    w = _max_width_lanes(0.25, 1.0, 1000)
+    g, o, rep = _case("max-width", w, 1e-3, max_iter=1000)
+    assert g["stats"].sub_batches >= 2
+    assert np.all(g["status"] == oracle.CONVERGED)
+
+
+def test_edge_max_width_capped_lanes_float64_state():
+    # Smaller eps leaves a few hundred of the 4096 lanes at the 400-cycle cap,
+    # some of them half-way through the escape from a residual plateau (n = 14,
+    # m = 3, eps = 0.065: 0.085 for 300 cycles, then 0.060 at the cap). There
+    # the residual moves by about 5e-4 per cycle, and the float32 state's
+    # rounding, a fraction of a cycle of that motion, moved it by 4.4e-5 from
+    # the oracle's at equal depth (potentials within 1e-4). The float64 state
+    # follows the oracle's trajectory: every lane, capped or not, meets the
+    # parity bar.
+    w = _max_width_lanes(0.05, 0.5, 400)
+    g, o, rep = _case("max-width float64 state", w, 1e-3, flags=F_PRECISE, max_iter=400)
+    assert g["stats"].sub_batches >= 2
+    assert int((g["status"] == oracle.MAX_ITER).sum()) > 100
+
+
 def test_edge_nonfinite_and_zero_mass():
     w = _tiny_lanes()
     w.X[2, 3, 1] = np.nan           # lane 2 non-finite
