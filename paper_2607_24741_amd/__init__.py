@@ -169,6 +169,37 @@ def _ptr(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
+_OUT_REQUIRED = ("f", "g", "depth", "residual", "status")
+_OUT_OPTIONAL = ("row_residual", "col_residual", "order")
+
+
+def _check_out(out, W, n_max, m_max, dev):
+    """Validates caller-provided output tensors (the library writes through
+    their raw pointers): f [W, n_max] and g [W, m_max] float32, depth and
+    status int32 [W], residual float32 [W]; row_residual / col_residual
+    (float32 [W]) and order (int32 [W]) may be absent or None."""
+    import torch
+    spec = dict(f=(torch.float32, (W, n_max)), g=(torch.float32, (W, m_max)),
+                depth=(torch.int32, (W,)), residual=(torch.float32, (W,)),
+                row_residual=(torch.float32, (W,)), col_residual=(torch.float32, (W,)),
+                status=(torch.int32, (W,)), order=(torch.int32, (W,)))
+    unknown = set(out) - set(spec)
+    if unknown:
+        raise ValueError(f"unknown output(s) {sorted(unknown)}")
+    checked = {}
+    for k, (dt, shape) in spec.items():
+        t = out.get(k)
+        if t is None:
+            if k in _OUT_REQUIRED:
+                raise ValueError(f"output {k} is required")
+            checked[k] = None
+            continue
+        if t.dtype != dt or not t.is_contiguous() or t.device != dev or tuple(t.shape) != shape:
+            raise ValueError(f"output {k} must be a contiguous {dt} tensor of shape {shape} on {dev}")
+        checked[k] = t
+    return checked
+
+
 def solve(X, Y, a, b, eps, tol, *, n=None, m=None, g0=None, max_iter=5000, audit_every=1,
           mode="active", screen_tol=None, flags=0, streams=0, return_stats=False,
           workspace=None, trace_len=0, out=None):
@@ -223,6 +254,8 @@ def solve(X, Y, a, b, eps, tol, *, n=None, m=None, g0=None, max_iter=5000, audit
                    col_residual=torch.empty(W, dtype=torch.float32, device=dev),
                    status=torch.empty(W, dtype=torch.int32, device=dev),
                    order=torch.empty(W, dtype=torch.int32, device=dev))
+    else:
+        out = _check_out(out, W, n_max, m_max, dev)
     res = _Result(**{k: _ptr(v) for k, v in out.items()})
     st = _Stats()
     trace_buf = None

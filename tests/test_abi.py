@@ -156,3 +156,22 @@ def test_guarded_release_validation_and_size():
     assert code == 0 and code2 == 0 and n1 > n0
     assert _bytes(_problem(W=2, n_max=9000, m_max=100, d=3), opg)[0] == 4
     assert _bytes(_problem(W=2, n_max=9000, m_max=100, d=3), op)[0] == 0
+
+
+def test_caller_outputs_are_validated():
+    # the library writes through raw pointers: wrong dtype, shape or a missing
+    # required output must be refused before the call
+    import torch
+    dev = torch.device("cpu")
+    W, n_max, m_max = 3, 5, 4
+    ok = dict(f=torch.empty((W, n_max)), g=torch.empty((W, m_max)),
+              depth=torch.empty(W, dtype=torch.int32), residual=torch.empty(W),
+              status=torch.empty(W, dtype=torch.int32))
+    got = ds._check_out(ok, W, n_max, m_max, dev)
+    assert got["order"] is None and got["row_residual"] is None and got["f"] is ok["f"]
+    bad = [dict(ok, f=torch.empty((W, m_max))), dict(ok, depth=torch.empty(W)),
+           dict(ok, g=torch.empty((m_max, W)).t()), dict(ok, extra=torch.empty(W)),
+           {k: v for k, v in ok.items() if k != "status"}]
+    for o in bad:
+        with pytest.raises(ValueError):
+            ds._check_out(o, W, n_max, m_max, dev)

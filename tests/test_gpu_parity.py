@@ -655,3 +655,30 @@ def test_invalid_lane_data_is_a_call_error():
     assert ei.value.code == 1 and "lane 3" in str(ei.value)
     g = run_gpu(_tiny_lanes(), 1e-4, streams=2)
     assert g["stats"].sub_batches == 2 and np.all(g["status"] == oracle.CONVERGED)
+
+
+def test_caller_outputs_and_workspace_reuse():
+    # caller-provided outputs without the optional ones (the library gets NULL
+    # for them) and one workspace reused across calls give the default call's
+    # bits
+    import torch
+    import paper_2607_24741_amd as ds
+    from tests.gpu_support import to_device
+    w = wl.make("c1")
+    log("[case] caller outputs + workspace reuse (c1)")
+    dv = to_device(w)
+    args = (dv["X"], dv["Y"], dv["a"], dv["b"], dv["eps"], 1e-3)
+    ref = ds.solve(*args, n=dv["n"], m=dv["m"])
+    need = ds.workspace_bytes(w.W, w.X.shape[1], w.Y.shape[1], w.d, tol=1e-3)
+    ws = torch.empty(need + 256, dtype=torch.uint8, device="cuda:0")
+    for _ in range(2):
+        out = dict(f=torch.full((w.W, w.X.shape[1]), 7.0, device="cuda:0"),
+                   g=torch.full((w.W, w.Y.shape[1]), 7.0, device="cuda:0"),
+                   depth=torch.zeros(w.W, dtype=torch.int32, device="cuda:0"),
+                   residual=torch.zeros(w.W, device="cuda:0"),
+                   status=torch.full((w.W,), 9, dtype=torch.int32, device="cuda:0"))
+        got = ds.solve(*args, n=dv["n"], m=dv["m"], workspace=ws, out=out)
+        torch.cuda.synchronize()
+        assert got[5] is None
+        for a_, b_ in zip(got[:5], ref[:5]):
+            assert torch.equal(a_, b_)
