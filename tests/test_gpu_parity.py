@@ -682,3 +682,48 @@ def test_caller_outputs_and_workspace_reuse():
         assert got[5] is None
         for a_, b_ in zip(got[:5], ref[:5]):
             assert torch.equal(a_, b_)
+
+
+def test_concurrent_calls_from_host_threads():
+    # distinct workspaces used at once from two host threads, each on a stream
+    # of its own (one call split into two sub-batches): the library's per-device
+    # resource pool hands each call its own resources, and every result equals
+    # the sequential call's bits
+    import threading
+    import torch
+    import paper_2607_24741_amd as ds
+    from tests.gpu_support import to_device
+    log("[case] concurrent calls from two host threads (c1 with two sub-batches, tiny lanes)")
+    jobs = [(to_device(wl.make("c1")), 1e-3, 2), (to_device(_tiny_lanes()), 1e-4, 0)]
+
+    def call(dv, tol, streams):
+        return ds.solve(dv["X"], dv["Y"], dv["a"], dv["b"], dv["eps"], tol, n=dv["n"], m=dv["m"],
+                        streams=streams)
+
+    ref = [call(*j) for j in jobs]
+    torch.cuda.synchronize()
+    got = [[None] * 3 for _ in jobs]
+    errors = []
+
+    def worker(i):
+        try:
+            s = torch.cuda.Stream()
+            with torch.cuda.stream(s):
+                for r in range(3):
+                    got[i][r] = call(*jobs[i])
+            s.synchronize()
+        except Exception as e:  # pragma: no cover - reported below
+            errors.append(e)
+
+    th = [threading.Thread(target=worker, args=(i,)) for i in range(len(jobs))]
+    for t in th:
+        t.start()
+    for t in th:
+        t.join(timeout=120)
+    assert not any(t.is_alive() for t in th)
+    assert not errors, errors
+    torch.cuda.synchronize()
+    for i in range(len(jobs)):
+        for r in range(3):
+            for a_, b_ in zip(got[i][r], ref[i]):
+                assert torch.equal(a_, b_)
