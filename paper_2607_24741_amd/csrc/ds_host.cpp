@@ -192,15 +192,22 @@ hipError_t acquire_res(DeviceRes** out) {
   for (auto& r : g_pool[dev])
     if (!r->busy) { r->busy = true; *out = r.get(); return hipSuccess; }
   auto r = std::make_unique<DeviceRes>();
+  // a set that cannot be completed is released again, so a failed call leaks nothing
+  auto undo = [&](hipError_t err) {
+    if (r->stream) (void)hipStreamDestroy(r->stream);
+    if (r->join_ev) (void)hipEventDestroy(r->join_ev);
+    if (r->snap) (void)hipHostFree(r->snap);
+    return err;
+  };
   e = hipHostMalloc(reinterpret_cast<void**>(&r->snap), sizeof(ds::HostSnap),
                     hipHostMallocMapped | hipHostMallocCoherent);
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess) return undo(e);
   e = hipHostGetDevicePointer(reinterpret_cast<void**>(&r->snap_dev), r->snap, 0);
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess) return undo(e);
   e = hipEventCreateWithFlags(&r->join_ev, hipEventDisableTiming);
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess) return undo(e);
   e = hipStreamCreateWithFlags(&r->stream, hipStreamNonBlocking);
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess) return undo(e);
   r->busy = true;
   *out = r.get();
   g_pool[dev].push_back(std::move(r));
