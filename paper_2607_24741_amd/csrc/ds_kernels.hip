@@ -209,11 +209,23 @@ __device__ __forceinline__ LaneAgg lane_aggregate(const float4* agg, int s, int 
 // Update: lse_new - lse_old lies in [min_j dgam_j, max_j dgam_j], dgam being
 // the latest change of the column operand (= -(change of the column lse)), so
 // anchored (max-free) sums are safe when that spread is small; M = -min dgam.
+//
+// Two wave reductions instead of three: a block with a non-finite change
+// enters the maximum as +inf, which fails the spread test exactly as the
+// separate flag did (inf - dmin is +inf or NaN).
 __device__ __forceinline__ void update_facts(const Launch& L, const Pass& P, int s, int ncols,
                                              bool& fast, float& M, float range = kFastRange) {
-  const LaneAgg g = lane_aggregate(P.agg_bound, s, L.rbmax, row_blocks(ncols, L.rows), false);
-  fast = !g.bad && g.dmin <= g.dmax && (g.dmax - g.dmin) <= range;
-  M = -g.dmin;
+  float t1 = INFINITY, t2 = -INFINITY;
+  const float4* base = P.agg_bound + (size_t)s * L.rbmax;
+  const int nrb = row_blocks(ncols, L.rows);
+  for (int q = (int)(threadIdx.x & 63); q < nrb; q += 64) {
+    const float4 v = base[q];
+    t1 = fminf(t1, v.y);
+    t2 = fmaxf(t2, v.w != 0.f ? INFINITY : v.z);
+  }
+  const float dmin = wave64(t1, OpMin()), dmax = wave64(t2, OpMax());
+  fast = dmin <= dmax && (dmax - dmin) <= range;
+  M = -dmin;
 }
 // Check: whether this lane is checked at all (screen-positive, non-finite
 // screen, or every lane), and the row screen of the audited state (n_x: the
