@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define DS_API_VERSION 2
+#define DS_API_VERSION 3
 
 typedef enum {
   DS_OK = 0,
@@ -82,18 +82,18 @@ enum {
                            count already-releasable lanes the screen missed      */
   DS_F_TIMING = 2u,     /* time the update launches of every 32nd cycle with HIP
                            events in their dispatches (ds_stats)                 */
-  DS_F_FORCE_VALU = 4u, /* use the vector-ALU update kernels for any d <= 32
-                           (the default for d <= 32 is the matrix-core kernel)  */
-  DS_F_FORCE_MFMA = 8u, /* use the matrix-core update kernels (the default)      */
-  DS_F_PRECISE = 16u,   /* float64 state and exponent arguments (vector-ALU
-                           kernels, d <= 16, exclusive with DS_F_FORCE_MFMA):
-                           for small eps, where float32 rounding of exponents of
-                           size C/eps reaches the tolerance bands; the outputs
-                           stay float32                                         */
+  DS_F_FORCE_VALU = 4u, /* float32 state on the vector-ALU update kernels (d <= 16) */
+  DS_F_FORCE_MFMA = 8u, /* float32 state on the matrix-core update kernels
+                           (d <= 32; the default for 16 < d <= 32)             */
+  DS_F_PRECISE = 16u,   /* float64 state and exponent arguments (d <= 16). This
+                           is the default for d <= 16 unless DS_F_FAST32 or a
+                           FORCE flag is given; the flag is kept so a caller can
+                           require it (an error where it is unavailable). The
+                           outputs stay float32.                                */
   DS_F_MATERIALIZE = 32u, /* build the cost C (base-2 units, float32) once per call
                            in the workspace and stream it from HBM in every
                            half-step; always on for d > 32 (n_max, m_max <= 8192) */
-  DS_F_GUARD = 64u      /* guarded release (eq:release-contract in float64): a lane
+  DS_F_GUARD = 64u,     /* guarded release (eq:release-contract in float64): a lane
                            whose float32 row screen is within the guard margin
                            (r^ <= (1 + 1/64) tau_screen, or non-finite) is verified by a
                            float64 evaluation of both marginals of exactly the
@@ -101,6 +101,12 @@ enum {
                            in float64 from the caller's coordinates); that residual
                            decides the release and is the one reported. One extra
                            launch per audit cycle; n_max, m_max <= 8192.         */
+  DS_F_FAST32 = 128u    /* float32 state on the matrix-core kernels for d <= 16:
+                           about 1.5-2.5x faster, but float32 rounding of the
+                           scaled coordinates and potentials (exponents of size
+                           C/eps) moves residuals by 1e-6..1e-5, so completion
+                           depths of lanes within that distance of tol can
+                           differ by a cycle from the float64 trajectory's      */
 };
 
 /* One window of W lanes. Device pointers. */

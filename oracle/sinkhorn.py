@@ -90,7 +90,7 @@ def dual_objective(C, f, g, a, b, eps):
 
 # --------------------------------------------------------------------- one lane
 def solve_lane(x, y, a, b, eps, tol, *, max_iter=5000, audit_every=1,
-               fixed_iters=None, precision="f64", history=False, g0=None):
+               fixed_iters=None, history=False, g0=None):
     """Solve one lane from a proposal (cold by default) and stop on the
     two-sided audit.
 
@@ -117,12 +117,8 @@ def solve_lane(x, y, a, b, eps, tol, *, max_iter=5000, audit_every=1,
     ``fixed_iters=k`` runs exactly k cycles with no stopping test and reports
     the residual of the final state (fixed-work parity, Sec. 3.2).
 
-    ``precision="fp32"`` runs the same steps with every half-step and residual
-    evaluated in float32 (cost, exponentials, sums, stored potentials). It is
-    an estimate of the error floor of a plain fp32 trajectory, not a model of
-    any particular GPU kernel.
     """
-    dt = np.float32 if precision == "fp32" else np.float64
+    dt = np.float64
     x = np.asarray(x, dtype=np.float64)
     y = np.asarray(y, dtype=np.float64)
     a = np.asarray(a, dtype=np.float64)
@@ -136,12 +132,7 @@ def solve_lane(x, y, a, b, eps, tol, *, max_iter=5000, audit_every=1,
     xs, ys = x[row_live], y[col_live]
     av, bv = a[row_live], b[col_live]
 
-    if precision == "fp32":
-        C = sq_euclidean_cost(xs.astype(np.float32).astype(np.float64),
-                              ys.astype(np.float32).astype(np.float64))
-        C = C.astype(np.float32)
-    else:
-        C = sq_euclidean_cost(xs, ys)
+    C = sq_euclidean_cost(xs, ys)
     with np.errstate(divide="ignore", invalid="ignore"):
         log_a = np.log(av).astype(dt)
         log_b = np.log(bv).astype(dt)
@@ -200,7 +191,7 @@ def _lane_job(args):
 
 
 def solve(X, Y, a, b, eps, tol, *, n=None, m=None, max_iter=5000, audit_every=1,
-          fixed_iters=None, precision="f64", history=False, lanes=None,
+          fixed_iters=None, history=False, lanes=None,
           processes=None, g0=None):
     """Solve a window of W independent lanes (candidate-axis packing).
 
@@ -228,7 +219,7 @@ def solve(X, Y, a, b, eps, tol, *, n=None, m=None, max_iter=5000, audit_every=1,
     m = np.full(W, m_max, dtype=np.int64) if m is None else np.asarray(m)
     lanes = list(range(W)) if lanes is None else [int(t) for t in lanes]
     kw = dict(max_iter=max_iter, audit_every=audit_every, fixed_iters=fixed_iters,
-              precision=precision, history=history)
+              history=history)
     jobs = [((X[t, :n[t]], Y[t, :m[t]], a[t, :n[t]], b[t, :m[t]], eps[t], tol),
              dict(kw, g0=None if g0 is None else np.asarray(g0)[t, :m[t]]))
             for t in lanes]

@@ -23,15 +23,16 @@ from dataclasses import dataclass
 __all__ = ["solve", "workspace_bytes", "load_library", "library_path", "DSError",
            "MODES", "LANE_CONVERGED", "LANE_MAX_ITER", "LANE_NONFINITE",
            "F_SHADOW", "F_TIMING", "F_FORCE_VALU", "F_FORCE_MFMA", "F_PRECISE",
-           "F_MATERIALIZE", "F_GUARD"]
+           "F_MATERIALIZE", "F_GUARD", "F_FAST32"]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 _LIBPATH = os.path.join(_PKG, "_lib", "libdrainsinkhorn.so")
-API_VERSION = 2   # the structs below mirror include/ds.h at this version
+API_VERSION = 3   # the structs below mirror include/ds.h at this version
 
 MODES = {"active": 0, "static": 1, "logical": 2}
 LANE_CONVERGED, LANE_MAX_ITER, LANE_NONFINITE = 0, 1, 2
 F_SHADOW, F_TIMING, F_FORCE_VALU, F_FORCE_MFMA, F_PRECISE, F_MATERIALIZE, F_GUARD = 1, 2, 4, 8, 16, 32, 64
+F_FAST32 = 128   # float32 state on the matrix cores (d <= 16); default: float64 state
 
 _ERRS = {0: "DS_OK", 1: "DS_E_INVALID", 2: "DS_E_WORKSPACE", 3: "DS_E_HIP",
          4: "DS_E_UNSUPPORTED", 5: "DS_E_INTERNAL"}
@@ -244,6 +245,9 @@ def solve(X, Y, a, b, eps, tol, *, n=None, m=None, g0=None, max_iter=5000, audit
         raise ValueError(f"workspace must be a contiguous uint8 tensor on {dev}")
     base = workspace.data_ptr()
     shift = (-base) % 256
+    if workspace.numel() - shift < int(need.value):
+        raise ValueError(f"workspace holds {workspace.numel()} bytes ({shift} of them before the "
+                         f"first 256-byte boundary); the call needs {int(need.value)} from there")
     ws_ptr, ws_bytes = base + shift, workspace.numel() - shift
     if out is None:
         out = dict(f=torch.empty((W, n_max), dtype=torch.float32, device=dev),

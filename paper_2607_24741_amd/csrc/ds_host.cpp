@@ -51,6 +51,17 @@ bool uses_mfma(const ds_problem* pr, const ds_options* op);
 bool uses_mat(const ds_problem* pr, const ds_options* op) {
   return pr->d > ds::kMaxDSmall || (op->flags & DS_F_MATERIALIZE) != 0;
 }
+// The float64 state is the default wherever its kernels exist (matrix-free,
+// d <= 16): rounding the scaled coordinates or the potentials to float32
+// perturbs exponents of size C/eps by ~C/eps * 2^-24, which moves the residual
+// trajectory by 1e-6..1e-5 and with it the completion depths of near-threshold
+// lanes. DS_F_FAST32 or a FORCE flag selects the float32 kernels instead.
+bool uses_f64(const ds_problem* pr, const ds_options* op) {
+  if (uses_mat(pr, op)) return false;
+  if (op->flags & DS_F_PRECISE) return true;
+  if (op->flags & (DS_F_FAST32 | DS_F_FORCE_VALU | DS_F_FORCE_MFMA)) return false;
+  return pr->d <= ds::kMaxDF64;
+}
 
 struct Carver {
   char* base;
@@ -77,7 +88,7 @@ ds::Layout plan(const ds_problem* pr, const ds_options* op, void* ws) {
   L.pad[1] = (int)align_up((size_t)pr->m_max, ds::kPad);
   L.mat = uses_mat(pr, op) ? 1 : 0;
   L.rows = (!L.mat && uses_mfma(pr, op)) ? ds::kRowsMfma : ds::kRowsValu;
-  L.es = (op->flags & DS_F_PRECISE) ? 2 : 1;
+  L.es = uses_f64(pr, op) ? 2 : 1;
   if (L.mat) L.dp = 0;   // no point records: the cost is materialised
   L.rbmax = std::max(L.pad[0], L.pad[1]) / L.rows;
   const size_t W = (size_t)pr->W;
@@ -117,8 +128,7 @@ ds::Layout plan(const ds_problem* pr, const ds_options* op, void* ws) {
 // than the vector kernel's d fused multiply-adds plus the bias add, and it
 // was measured faster at d = 2, 3, 8 and 16.
 bool uses_mfma(const ds_problem* pr, const ds_options* op) {
-  (void)pr;
-  if (op->flags & DS_F_PRECISE) return false;
+  if (uses_f64(pr, op)) return false;
   if (op->flags & DS_F_FORCE_VALU) return false;
   return true;
 }
@@ -130,9 +140,9 @@ ds_err check_problem(const ds_problem* pr, const ds_options* op) {
   if (pr->W > ds::kMaxW) return fail(DS_E_UNSUPPORTED, "W above 4096 is not supported");
   if (pr->d > 512) return fail(DS_E_INVALID, "d must be <= 512");
   if (uses_mat(pr, op)) {
-    if (op->flags & (DS_F_PRECISE | DS_F_FORCE_VALU | DS_F_FORCE_MFMA))
+    if (op->flags & (DS_F_PRECISE | DS_F_FAST32 | DS_F_FORCE_VALU | DS_F_FORCE_MFMA))
       return fail(DS_E_UNSUPPORTED, "the materialised cost (d > 32 or DS_F_MATERIALIZE) runs "
-                                    "in float32 with its own kernels: no PRECISE / FORCE flags");
+                                    "in float32 with its own kernels: no PRECISE / FAST32 / FORCE flags");
     if (pr->n_max > ds::kMatMaxPts || pr->m_max > ds::kMatMaxPts)
       return fail(DS_E_UNSUPPORTED, "the materialised cost supports at most 8192 points per side");
   }
@@ -149,8 +159,9 @@ ds_err check_problem(const ds_problem* pr, const ds_options* op) {
     return fail(DS_E_INVALID, "DS_F_FORCE_VALU and DS_F_FORCE_MFMA are exclusive");
   if ((op->flags & DS_F_FORCE_VALU) && pr->d > 16)
     return fail(DS_E_UNSUPPORTED, "the vector-ALU kernels support d <= 16");
-  if ((op->flags & DS_F_PRECISE) && (op->flags & DS_F_FORCE_MFMA))
-    return fail(DS_E_INVALID, "DS_F_PRECISE runs on the vector ALU: DS_F_FORCE_MFMA is exclusive");
+  if ((op->flags & DS_F_PRECISE) && (op->flags & (DS_F_FORCE_MFMA | DS_F_FORCE_VALU | DS_F_FAST32)))
+    return fail(DS_E_INVALID, "DS_F_PRECISE (float64 state) excludes DS_F_FAST32 and the FORCE flags, "
+                              "which select float32 kernels");
   if ((op->flags & DS_F_PRECISE) && pr->d > 16)
     return fail(DS_E_UNSUPPORTED, "the float64 state supports d <= 16");
   // sizes that keep every 32-bit index in range
@@ -276,7 +287,7 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
   const bool shadow = (op->flags & DS_F_SHADOW) != 0;
   const bool guard = (op->flags & DS_F_GUARD) != 0;
   const bool use_mfma = uses_mfma(pr, op);
-  const bool precise = (op->flags & DS_F_PRECISE) != 0;
+  const bool precise = uses_f64(pr, op);
   const bool mat = L.mat != 0;
   const int maxpad = std::max(L.pad[0], L.pad[1]);
 

@@ -36,9 +36,13 @@ constexpr int kRowsMfma = 32;    // rows per work item, matrix-core kernel
 constexpr int kRowsValu = 64;    // rows per work item, vector-ALU kernel
 constexpr int kMaxW = 4096;
 constexpr int kMaxDSmall = 32;   // matrix-free kernels
+constexpr int kMaxDF64 = 16;     // matrix-free float64-state kernels
 constexpr int kMatMaxPts = 8192; // materialised cost: points per lane side (LDS staging)
 constexpr float kFastRange = 64.f;  // max spread of the bound (log2 units) for anchored sums
-constexpr float kFastRangePrecise = 1.f;  // the same for the float64 state
+// The same for the float64 state: there the anchored exponent (at most this
+// far above the true row maximum) is rounded once to float32 for v_exp_f32,
+// a relative error of at most 64 * 2^-24 * ln 2 ~ 2.6e-6 per term.
+constexpr float kFastRangePrecise = 64.f;
 constexpr int kMaxTimed = 4096;     // timed launches per sub-batch (DS_F_TIMING)
 // launch-variant thresholds (work items of the launch, see launch_update)
 constexpr int kMediumItemsMfma = 384;

@@ -923,6 +923,7 @@ void k_update_f64(Launch L) {
       const bool more = t + 1 < tB;
       if (more) DS_F64_FETCH(t + 1);
       if (fast) {
+        float tacc[2] = {0.f, 0.f};
         for (int c = 0; c < kColTile; c += 2) {
 #pragma unroll
           for (int v = 0; v < 2; ++v) {
@@ -930,9 +931,10 @@ void k_update_f64(Launch L) {
             double z = cur[TREC + c + v] + bias;
 #pragma unroll
             for (int k = 0; k < D; ++k) z = fma(xr[k], cj[k], z);
-            sacc[v] += (double)ex2((float)z);
+            tacc[v] += ex2((float)z);
           }
         }
+        sacc[0] += (double)(tacc[0] + tacc[1]);   // the tile's sum, added in float64
       } else {
         for (int c = 0; c < kColTile; c += 4) {
           double z[4];
@@ -960,7 +962,7 @@ void k_update_f64(Launch L) {
 #undef DS_F64_STASH
 #undef DS_F64_LD
 #undef DS_F64_ST
-    if (fast) srun = sacc[0] + sacc[1];
+    if (fast) srun = sacc[0];
     sh_part[g][lane] = make_double2(mrun, srun);   // (-inf, 0) for an empty group
   }
   __syncthreads();

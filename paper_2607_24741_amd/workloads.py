@@ -237,7 +237,9 @@ def random_window(k, *, seed=SEED):
         N[t], M[t] = nt, mt
     tol = float(rng.choice([1e-2, 1e-3]))
     audit_every = int(rng.integers(1, 4))
-    flags = int(rng.choice([0, 0, 4, 16, 32, 64]))   # default, vector ALU, float64, materialised, guarded
+    # default, float32 matrix cores, float32 vector ALU, float64 (explicit),
+    # materialised, guarded
+    flags = int(rng.choice([0, 128, 4, 16, 32, 64]))
     if d > 32:
         flags = 0 if flags != 64 else 64               # d > 32 is always materialised
     if d > 16 and flags == 16:

@@ -5,14 +5,20 @@ Parity bar (readings of the stated tolerances):
   * potentials: max_i |f_gpu - f_or| / max(||f_or||_inf, ||g_or||_inf, eps) <= 1e-4
     (likewise for g);
   * residuals: |r_gpu - r_or| <= 1e-5 absolute;
-  * depths, statuses and completion order exact, except for near-threshold
-    lanes: a differing depth is accepted only when the GPU's stop decision is
-    consistent with the oracle's own residual trajectory within the residual
-    bound (every audit at which the GPU continued has r_or >= tol - 1e-5, and
-    the audit at which it stopped has r_or <= tol + 1e-5); such a lane is then
-    compared at fixed work (the oracle's state at the GPU's depth). Lanes whose
-    margin exceeds 1e-6 are counted (fp32 cannot resolve residuals to 1e-6,
-    so the 1e-6 band is reported rather than enforced).
+  * depths, statuses and completion order exact, except for lanes whose
+    residual lies within 1e-6 of tol: a differing depth or status is accepted
+    only when the oracle's own residual trajectory is within EXEMPT_BAND of tol
+    at every audit where the two decisions differ (every audit at which the
+    GPU continued has r_or >= tol - 1e-6, and the audit at which it stopped has
+    r_or <= tol + 1e-6); such a lane is then compared at fixed work (the
+    oracle's state at the GPU's depth), and every such margin is printed.
+
+The 1e-6 band is the contract of the default path (the float64 state for
+d <= 16, the materialised cost above 32). The opt-in float32 kernels
+(DS_F_FAST32, DS_F_FORCE_VALU, DS_F_FORCE_MFMA, DS_F_MATERIALIZE at small d)
+round the scaled coordinates and potentials to float32, which moves residual
+trajectories by 1e-6..1e-5; their tests pass band=FP32_BAND and still count
+the lanes outside the 1e-6 band (report["beyond_1e6"]).
 """
 
 from __future__ import annotations
@@ -27,6 +33,7 @@ import oracle
 POT_RTOL = 1e-4
 RES_ATOL = 1e-5
 EXEMPT_BAND = 1e-6
+FP32_BAND = 1e-5     # depth-decision band of the opt-in float32 kernels (outside the contract)
 
 
 def log(msg):
@@ -75,7 +82,7 @@ def pot_err(fg, fo, gg, go, eps):
     return max(np.abs(fg - fo).max(), np.abs(gg - go).max()) / scale
 
 
-def decision_consistent(w, t, tol, depth_gpu, status_gpu, audit_every, band=RES_ATOL):
+def decision_consistent(w, t, tol, depth_gpu, status_gpu, audit_every, band=EXEMPT_BAND):
     """Is the GPU's stop decision for lane t consistent with the oracle's own
     residual trajectory within `band`? Every audit at which the GPU kept going
     must have r_or >= tol - band, and the audit at which it stopped (if it
@@ -96,15 +103,15 @@ def decision_consistent(w, t, tol, depth_gpu, status_gpu, audit_every, band=RES_
 
 
 def compare(w, g, o, tol, *, audit_every=1, max_iter=5000, lanes=None, check_order=True,
-            res_atol=RES_ATOL):
+            res_atol=RES_ATOL, band=EXEMPT_BAND):
     """Assert the parity bar lane by lane; returns a report dict.
 
     Depth or status mismatches are accepted only when the GPU's decision is
-    consistent with the oracle's residual trajectory within the residual
-    parity bound (RES_ATOL); such lanes are compared at fixed work (the
-    oracle's state at the GPU's depth) and listed in report["near_threshold"]
-    with their margin; report["beyond_1e6"] counts those whose margin exceeds
-    the 1e-6 band.
+    consistent with the oracle's residual trajectory within `band` (1e-6 on
+    the default path); such lanes are compared at fixed work (the oracle's
+    state at the GPU's depth) and listed in report["near_threshold"] with
+    their margin; report["beyond_1e6"] counts those whose margin exceeds the
+    1e-6 band (nonzero only where a test passes the wider FP32_BAND).
     """
     lanes = range(w.W) if lanes is None else lanes
     report = dict(max_pot_err=0.0, max_res_err=0.0, near_threshold=[], beyond_1e6=0)
@@ -114,12 +121,12 @@ def compare(w, g, o, tol, *, audit_every=1, max_iter=5000, lanes=None, check_ord
         sg, so = int(g["status"][t]), int(o["status"][t])
         ref_f, ref_g, ref_r = o["f"][t, :nt], o["g"][t, :mt], o["residual"][t]
         if dg != do or sg != so:
-            ok, margin, fw = decision_consistent(w, t, tol, dg, sg, audit_every, band=res_atol)
+            ok, margin, fw = decision_consistent(w, t, tol, dg, sg, audit_every, band=band)
             report["near_threshold"].append((t, dg, do, margin))
             if margin > EXEMPT_BAND:
                 report["beyond_1e6"] += 1
-            assert ok, (f"lane {t}: gpu depth/status ({dg},{sg}) vs oracle ({do},{so}) is not "
-                        f"explained by the residual tolerance (margin {margin:.3e})")
+            assert ok, (f"lane {t}: gpu depth/status ({dg},{sg}) vs oracle ({do},{so}): the "
+                        f"oracle's residual is {margin:.3e} from tol, outside the {band:.0e} band")
             ref_f, ref_g, ref_r = fw["f"], fw["g"], fw["residual"]
         e = pot_err(g["f"][t, :nt], ref_f, g["g"][t, :mt], ref_g, float(w.eps[t]))
         report["max_pot_err"] = max(report["max_pot_err"], e)

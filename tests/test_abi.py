@@ -28,7 +28,7 @@ def test_library_exports_every_declared_function():
                           "ds_last_error_message"}
     for nm in names:
         assert hasattr(lib, nm), nm
-    assert lib.ds_api_version() == 2
+    assert lib.ds_api_version() == 3
     for code in range(6):
         assert lib.ds_error_string(code).decode()
 
@@ -64,17 +64,26 @@ def test_workspace_query_and_validation():
     assert ds.load_library().ds_last_error_message().decode()
 
 
-def test_precise_state_validation_and_size():
-    """The float64 state runs on the vector-ALU kernels only (d <= 16) and
-    doubles the per-point state of the workspace."""
+def test_precise_state_default_validation_and_size():
+    """The float64 state is the default for d <= 16 (DS_F_PRECISE states it
+    explicitly, with the same workspace); DS_F_FAST32 selects the float32
+    state, whose per-point state is half the size. DS_F_PRECISE excludes the
+    float32 selectors and d > 16; above 16 the default is the float32 state."""
     op = ds._options(1e-3, None, 100, 1, "active", 0)
     opp = ds._options(1e-3, None, 100, 1, "active", ds.F_PRECISE)
-    code, n32 = _bytes(_problem(W=4, d=8), op)
+    opf = ds._options(1e-3, None, 100, 1, "active", ds.F_FAST32)
+    code, n_def = _bytes(_problem(W=4, d=8), op)
     code2, n64 = _bytes(_problem(W=4, d=8), opp)
-    assert code == 0 and code2 == 0 and n64 > 1.5 * n32
-    bad = ds._options(1e-3, None, 100, 1, "active", ds.F_PRECISE | ds.F_FORCE_MFMA)
-    assert _bytes(_problem(d=8), bad)[0] == 1
+    code3, n32 = _bytes(_problem(W=4, d=8), opf)
+    assert code == code2 == code3 == 0
+    assert n_def == n64 and n64 > 1.5 * n32
+    for fl in (ds.F_FORCE_MFMA, ds.F_FORCE_VALU, ds.F_FAST32):
+        bad = ds._options(1e-3, None, 100, 1, "active", ds.F_PRECISE | fl)
+        assert _bytes(_problem(d=8), bad)[0] == 1
     assert _bytes(_problem(d=17), opp)[0] == 4
+    code, n17 = _bytes(_problem(W=4, d=17), op)
+    code2, n17f = _bytes(_problem(W=4, d=17), opf)
+    assert code == code2 == 0 and n17 == n17f
 
 
 def test_materialised_cost_validation_and_size():
@@ -87,7 +96,7 @@ def test_materialised_cost_validation_and_size():
     opm = ds._options(1e-3, None, 100, 1, "active", ds.F_MATERIALIZE)
     code, nm = _bytes(_problem(W=2, n_max=256, m_max=200, d=3), opm)
     assert code == 0 and nm >= 2 * 256 * 256 * 4
-    for fl in (ds.F_PRECISE, ds.F_FORCE_VALU, ds.F_FORCE_MFMA):
+    for fl in (ds.F_PRECISE, ds.F_FAST32, ds.F_FORCE_VALU, ds.F_FORCE_MFMA):
         o = ds._options(1e-3, None, 100, 1, "active", fl)
         assert _bytes(_problem(d=64), o)[0] == 4
     assert _bytes(_problem(n_max=9000, d=64), op)[0] == 4

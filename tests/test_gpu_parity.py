@@ -9,20 +9,35 @@ import pytest
 
 import oracle
 from paper_2607_24741_amd import workloads as wl
-from tests.gpu_support import compare, log, procs, run_gpu, run_oracle
+from tests.gpu_support import EXEMPT_BAND, FP32_BAND, compare, log, procs, run_gpu, run_oracle
 
 pytestmark = pytest.mark.gpu
 
 F_SHADOW, F_FORCE_VALU, F_FORCE_MFMA, F_PRECISE, F_MATERIALIZE, F_GUARD = 1, 4, 8, 16, 32, 64
+F_FAST32 = 128
+# opt-in float32 kernels: outside the 1e-6 depth contract (see tests/gpu_support.py)
+FP32_FLAGS = F_FAST32 | F_FORCE_VALU | F_FORCE_MFMA | F_MATERIALIZE
+
+
+def band_for(flags, d):
+    """Depth-decision band: the contract's 1e-6 on the default path, FP32_BAND
+    for the opt-in float32 kernels (and for the float32 matrix-core default of
+    16 < d <= 32, where no float64-state kernel exists)."""
+    if flags & FP32_FLAGS:
+        return FP32_BAND
+    if 16 < d <= 32 and not flags & F_PRECISE:
+        return FP32_BAND
+    return EXEMPT_BAND
 
 
 def _case(name, w, tol, flags=0, res_atol=None, **kw):
+    band = band_for(flags, w.d)
     log(f"[case] {name}: W={w.W} n_max={w.X.shape[1]} m_max={w.Y.shape[1]} d={w.d} tol={tol} "
-        f"flags={flags} {kw}")
+        f"flags={flags} band={band:.0e} {kw}")
     g = run_gpu(w, tol, flags=flags, **kw)
     o = run_oracle(w, tol, **{k: v for k, v in kw.items() if k in ("max_iter", "audit_every")})
     extra = {} if res_atol is None else {"res_atol": res_atol}
-    rep = compare(w, g, o, tol, audit_every=kw.get("audit_every", 1), **extra)
+    rep = compare(w, g, o, tol, audit_every=kw.get("audit_every", 1), band=band, **extra)
     log(f"[case] {name}: depths {g['depth'].tolist()} max_pot_err={rep['max_pot_err']:.2e} "
         f"max_res_err={rep['max_res_err']:.2e} near_threshold={rep['near_threshold']} "
         f"beyond_1e-6_band={rep['beyond_1e6']}")
@@ -32,54 +47,56 @@ def _case(name, w, tol, flags=0, res_atol=None, **kw):
     return g, o, rep
 
 
-@pytest.mark.parametrize("flags", [F_FORCE_VALU, 0], ids=["valu", "mfma"])
+@pytest.mark.parametrize("flags", [0, F_FAST32, F_FORCE_VALU], ids=["default", "fast32", "valu"])
 def test_toy_config_full(flags):
     w = wl.make("c1")
     _case("c1", w, 1e-3, flags=flags)
 
 
-@pytest.mark.parametrize("flags", [0, F_FORCE_VALU], ids=["mfma", "valu"])
+@pytest.mark.parametrize("flags", [0, F_FAST32, F_FORCE_VALU], ids=["default", "fast32", "valu"])
 def test_mixture_reduced_ragged(flags):
     w = wl.make("c2", W=6, n=200, m=176)
     _case("c2-reduced", w, 1e-2, flags=flags)
 
 
-@pytest.mark.xfail(strict=False, reason=(
-    "fp32 floor: at eps=0.01 with C/eps ~ 3e3 the float32 trajectory drifts from the "
-    "float64 one by about one cycle of convergence near the threshold (residual slope "
-    "~9e-6 per cycle), which is of the order of the 1e-5 residual bar"))
 def test_telemetry_reduced():
+    """MetroPT-shaped case (eps = 0.01, C/eps ~ 3e3) on the default float64
+    state: depths, potentials and residuals meet the bar with no lane outside
+    the 1e-6 exemption band."""
     w = wl.make("c3", W=4, n=160, m=224)
-    _case("c3-reduced", w, 1e-2, max_iter=4000)
-
-
-def test_telemetry_reduced_precise():
-    """Float64 state on the same MetroPT-shaped case: depths, potentials and
-    residuals meet the bar with no lane outside the 1e-6 exemption band."""
-    w = wl.make("c3", W=4, n=160, m=224)
-    g, o, rep = _case("c3-reduced-precise", w, 1e-2, flags=F_PRECISE, max_iter=4000)
+    g, o, rep = _case("c3-reduced", w, 1e-2, max_iter=4000)
     assert rep["beyond_1e6"] == 0
+
+
+@pytest.mark.xfail(strict=False, reason=(
+    "opt-in float32 state: at eps=0.01 with C/eps ~ 3e3 the float32 trajectory drifts from "
+    "the float64 one by about one cycle near the threshold (residual slope ~9e-6 per cycle); "
+    "the fixed-work residual then differs by 1.01e-5, just over the 1e-5 residual bar"))
+def test_telemetry_reduced_fast32():
+    w = wl.make("c3", W=4, n=160, m=224)
+    _case("c3-reduced-fast32", w, 1e-2, flags=F_FAST32, max_iter=4000)
 
 
 def test_telemetry_full_size_sampled():
     """Full MetroPT-shaped window (W=256, n=m=512, d=16, eps=0.01, tol 1e-3) in
     its benchmark launch configuration, sampled lanes against the oracle:
-    float64 state strictly (no lane outside the 1e-6 band), float32 state
-    within the residual bound (its near-threshold lanes are printed)."""
+    the default float64 state strictly (no lane outside the 1e-6 band), the
+    opt-in float32 state within FP32_BAND (its near-threshold lanes are
+    printed)."""
     w = wl.make("c3")
     lanes = [1, 2]
     o = run_oracle(w, 1e-3, lanes=lanes)
-    for flags in (F_PRECISE, 0):
+    for flags in (0, F_FAST32):
         log(f"[case] c3 full size flags={flags}")
         g = run_gpu(w, 1e-3, flags=flags)
         st = g["stats"]
         assert st.slots_update == int(g["depth"].sum())
         assert list(g["order"]) == sorted(range(w.W), key=lambda t: (g["depth"][t], t))
-        rep = compare(w, g, o, 1e-3, lanes=lanes, check_order=False)
+        rep = compare(w, g, o, 1e-3, lanes=lanes, check_order=False, band=band_for(flags, w.d))
         log(f"[case] c3 full flags={flags}: depths {[int(g['depth'][t]) for t in lanes]} "
             f"oracle {[int(o['depth'][t]) for t in lanes]} max_pot_err={rep['max_pot_err']:.2e} "
             f"max_res_err={rep['max_res_err']:.2e} near_threshold={rep['near_threshold']}")
-        if flags == F_PRECISE:
+        if flags == 0:
             assert rep["beyond_1e6"] == 0
 
 
@@ -167,7 +184,7 @@ def test_lidar_full_size_sampled():
     assert list(g["order"]) == sorted(range(w.W), key=lambda t: (g["depth"][t], t))
     small = [int(t) for t in np.argsort(area, kind="stable")[:6]]
     o = run_oracle(w, 1e-3, lanes=small)
-    rep = compare(w, g, o, 1e-3, lanes=small, check_order=False)
+    rep = compare(w, g, o, 1e-3, lanes=small, check_order=False, band=band_for(0, w.d))
     log(f"  lanes {small}: depths {[int(g['depth'][t]) for t in small]} oracle "
         f"{[int(o['depth'][t]) for t in small]} max_pot_err={rep['max_pot_err']:.2e} "
         f"max_res_err={rep['max_res_err']:.2e} near_threshold={rep['near_threshold']}")
@@ -196,7 +213,7 @@ def test_precise_state_small_cases(name):
     assert rep["beyond_1e6"] == 0
 
 
-@pytest.mark.parametrize("flags", [F_FORCE_VALU, 0], ids=["valu", "mfma"])
+@pytest.mark.parametrize("flags", [0, F_FAST32, F_FORCE_VALU], ids=["default", "fast32", "valu"])
 def test_heterogeneous_nan_padded(flags):
     w = wl.make("c5", W=8, n=400, m=360, hetero=(40, 400), pad_value=np.nan)
     _case("c5-hetero", w, 1e-3, flags=flags, max_iter=3000)
@@ -262,15 +279,12 @@ def test_modes_agree_and_account_slots():
     arithmetic); static packing records the same first passing depths and
     returns every lane's state at the common final boundary l_max: bit for bit
     the state a fixed-work run of l_max cycles returns, and (float64 state)
-    the oracle's at l_max.
-
-    The float32 potentials of a lane run far past its own depth are compared
-    with the oracle through their residual only: near a fixed point every
-    cycle repeats nearly the same rounding errors, which add up along the
-    slowest-contracting direction. Lane 4 of this window (eps 0.133, depth
-    103, residual still 3e-5 at cycle 1022) drifts by 8e-5 (vector kernel) to
-    1.9e-4 (matrix-core kernel) relative over 919 extra cycles, while its
-    residual stays within 2e-7 of the oracle's."""
+    the oracle's at l_max (float64 state; the float32 state is compared
+    through its residual only: near a fixed point every cycle repeats nearly
+    the same rounding errors, which add up along the slowest-contracting
+    direction -- lane 4 of this window, eps 0.133, depth 103, residual still
+    3e-5 at cycle 1022, drifts by up to 1.9e-4 relative over 919 extra
+    cycles while its residual stays within 2e-7 of the oracle's)."""
     w = wl.make("c1")
     log("[case] modes on c1")
     ga = run_gpu(w, 1e-3, mode="active")
@@ -291,13 +305,13 @@ def test_modes_agree_and_account_slots():
     for k in ("f", "g", "residual"):
         assert np.array_equal(gs[k], gf[k]), k
     fixed = oracle.solve(w.X, w.Y, w.a, w.b, w.eps, 1e-3, n=w.n, m=w.m, fixed_iters=lmax)
-    _static_at_lmax(w, gs, fixed, None)
-    log("[case] modes on c1: static, float64 state")
-    gp = run_gpu(w, 1e-3, mode="static", flags=F_PRECISE)
+    _static_at_lmax(w, gs, fixed, 1e-4)
+    log("[case] modes on c1: static, float32 state")
+    gp = run_gpu(w, 1e-3, mode="static", flags=F_FAST32)
     lp = int(gp["depth"].max())
     if lp != lmax:
         fixed = oracle.solve(w.X, w.Y, w.a, w.b, w.eps, 1e-3, n=w.n, m=w.m, fixed_iters=lp)
-    _static_at_lmax(w, gp, fixed, 1e-4)
+    _static_at_lmax(w, gp, fixed, None)
 
 
 def test_bitwise_lane_independence_and_determinism():
@@ -317,8 +331,8 @@ def test_bitwise_lane_independence_and_determinism():
     assert solo["depth"][0] == g["depth"][3]
 
 
-@pytest.mark.parametrize("flags", [0, F_FORCE_VALU, F_PRECISE, F_MATERIALIZE],
-                         ids=["mfma", "valu", "precise", "materialised"])
+@pytest.mark.parametrize("flags", [0, F_FAST32, F_FORCE_VALU, F_MATERIALIZE],
+                         ids=["default", "fast32", "valu", "materialised"])
 @pytest.mark.parametrize("cfg", ["c2", "c3"])
 def test_launch_layouts_are_bitwise_identical(cfg, flags):
     """The host picks the update kernel's work layout (row tiles and column
@@ -390,8 +404,8 @@ def test_sub_batches_are_bitwise_identical(cfg):
             assert getattr(g["stats"], k) == getattr(base["stats"], k), (s, k)
 
 
-@pytest.mark.parametrize("flags", [0, F_FORCE_VALU, F_PRECISE, F_MATERIALIZE],
-                         ids=["mfma", "valu", "precise", "materialised"])
+@pytest.mark.parametrize("flags", [0, F_FAST32, F_FORCE_VALU, F_MATERIALIZE],
+                         ids=["default", "fast32", "valu", "materialised"])
 def test_proposal_parity(flags):
     """A proposal g0 (Sec. 2: a carried or warm-started target potential)
     replaces the cold start and the GPU follows the oracle's trajectory from
@@ -444,8 +458,8 @@ def _certified(w, g, tol, lanes):
     return worst
 
 
-@pytest.mark.parametrize("flags", [0, F_FORCE_VALU, F_PRECISE, F_MATERIALIZE],
-                         ids=["mfma", "valu", "precise", "materialised"])
+@pytest.mark.parametrize("flags", [0, F_FAST32, F_FORCE_VALU, F_MATERIALIZE],
+                         ids=["default", "fast32", "valu", "materialised"])
 def test_guarded_release_certifies_returned_potentials(flags):
     """DS_F_GUARD: screen-ready lanes are verified by a float64 evaluation of
     both marginals of the float32 potentials the caller receives; the release
@@ -491,7 +505,7 @@ def test_randomised_windows(k):
         _certified(w, g, opt["tol"], range(w.W))
 
 
-@pytest.mark.parametrize("flags", [F_FORCE_VALU, 0], ids=["valu", "mfma"])
+@pytest.mark.parametrize("flags", [0, F_FAST32, F_FORCE_VALU], ids=["default", "fast32", "valu"])
 @pytest.mark.parametrize("d", [1, 2])
 def test_low_dimensional_lanes(d, flags):
     """d = 1 and 2 (a contraction of K = 4 on the matrix cores, the smallest
@@ -550,7 +564,7 @@ def _tiny_lanes():
     return wl.Workload("tiny", X, Y, a, b, eps, n, m, 1e-4, 5000)
 
 
-@pytest.mark.parametrize("flags", [F_FORCE_VALU, 0], ids=["valu", "mfma"])
+@pytest.mark.parametrize("flags", [0, F_FAST32, F_FORCE_VALU], ids=["default", "fast32", "valu"])
 def test_edge_single_points_and_tiny_lanes(flags):
     w = _tiny_lanes()
     _case("tiny", w, 1e-4, flags=flags)

@@ -58,7 +58,7 @@ def test_random_windows_are_seeded_and_well_formed():
         for f in ("X", "Y", "a", "b", "eps", "n", "m"):
             assert np.array_equal(getattr(w, f), getattr(w2, f), equal_nan=True)
         assert 1 <= w.W <= 12 and 1 <= w.d <= 40
-        assert opt["flags"] in (0, 4, 16, 32, 64) and opt["audit_every"] in (1, 2, 3)
+        assert opt["flags"] in (0, 4, 16, 32, 64, 128) and opt["audit_every"] in (1, 2, 3)
         if w.d > 16:
             assert opt["flags"] != 16
         if w.d > 32:
