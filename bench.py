@@ -1,12 +1,16 @@
 #!/usr/bin/env python3
 """Benchmark of the active-set batched Sinkhorn hot path on one MI355X.
 
-One step = one complete solve of the mixture workload window (W=64 lanes,
-n=m=1024 points in d=8, Dirichlet(1) marginals, eps=0.05, two-sided L1
-tolerance 1e-3, audit after every cycle, active mode): ingest, packed f/g
-half-steps, fused row screen, two-sided check, retirement, physical compaction
-and output emission -- with the inputs already resident in HBM. Other windows
-(`--config c1..c5`, `--precise`, `--materialize`) are available for study.
+One step = one complete solve of the largest workload window, the
+LiDAR-shaped heterogeneous batch (W=1024 lanes, n_t, m_t ~ U{256..8192} padded
+to 8192, d=3, Dirichlet(0.5) marginals, eps_t ~ logU(0.005, 0.1), two-sided L1
+tolerance 1e-3, audit after every cycle, active mode, default float64 state):
+ingest, packed f/g half-steps, fused row screen, two-sided check, retirement,
+physical compaction and output emission -- with the inputs already resident in
+HBM. The headline runs as one sub-batch (one stream), so that every update
+launch has the chip to itself and its duration is the kernel's own. Other
+windows (`--config c1..c5`), `--fast32`, `--materialize` and `--streams` are
+available for study.
 
 Prints one JSON line:
   value        candidate-update slots per second (sum_t l_t per solve / solve time)
@@ -14,14 +18,17 @@ Prints one JSON line:
   roofline     the update kernel (the dominant kernel): algorithmic work of the
                timed launches (every 32nd cycle's two launches and the final
                audit, timed by events attached to the kernel dispatches) over
-               their summed duration, against the peak of the unit that bounds
-               the path: fp32 matrix cores (2 d flops per (i, j) term) for
-               d >= 8, HBM (4 bytes of cost per term) for the materialised cost,
-               the vector ALU (2 d + 2 flops per term) for smaller d, where the
-               exponentials and sums outweigh the matrix-core contraction;
-               `vector_view` prices the same launches by the vector-unit model
-               of a matrix-free small-d half-step (d + 4 lane operations and one
-               exponential per term)
+               their summed duration. Matrix-free small d: the vector-unit
+               model t_pe = max((d + 4) / R_v, 1 / R_e) per (i, j) term, with
+               R_v = 3.93e13 lane operations/s (256 CUs x 4 SIMDs x 16 lanes x
+               2.4 GHz: the float64 and non-packed float32 issue rate) and
+               R_e = 1.97e13 exponentials/s (8 lanes/clk per SIMD); `achieved`
+               counts each lane operation as one multiply-add (2 flops) against
+               the float64 vector peak 78.6 TFLOP/s, so `frac` is the model's
+               fraction. Materialised cost: HBM, 4 bytes per term.
+  mixture_modes      the mixture window's static and logical modes over its active
+               mode, all three at one sub-batch
+  mixture_tol_sweep  the mixture window's end-to-end batch time at each swept tol
   cpu_baseline the float64 oracle on a bounded sample, on this host's cores
 
 `--study` instead measures the execution surface of eq:time-accounting on the
@@ -43,19 +50,17 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-MFMA_FP32_PEAK_TFLOPS = 157.3
 HBM_PEAK_GBS = 8000.0
-# vector fp32 without packed-math instructions (not generated by this build):
-# 256 CUs x 4 SIMDs x 16 lanes x 2 flops (FMA) x 2.4 GHz
-VALU_FP32_PEAK_TFLOPS = 78.6
-# The vector-unit view of a small-d matrix-free half-step, t_pe = max((d + 4) /
-# R_v, 1 / R_e) per (i, j) term: d multiply-adds of the dot product plus the
-# scale, maximum, shift and add, against the published 157.3 TFLOP/s fp32
-# vector figure (packed math: 7.86e13 lane operations/s), and one exponential
-# against 256 CUs x 4 SIMDs x 8 lanes/clk x 2.4 GHz of transcendental issue
-# (the published quarter rate, 9.8e12/s, is below what gfx950 was measured to
-# sustain, 1.83e13/s, so it would inflate the fraction).
-VECTOR_LANE_OPS_PEAK = 157.3e12 / 2.0
+# float64 vector peak (and non-packed float32: this build generates no packed
+# float32 instructions): 256 CUs x 4 SIMDs x 16 lanes x 2 flops (FMA) x 2.4 GHz
+VALU_PEAK_TFLOPS = 78.6
+# The vector-unit model of a small-d matrix-free half-step, t_pe = max((d + 4)
+# / R_v, 1 / R_e) per (i, j) term: d multiply-adds of the dot product plus the
+# scale, maximum, shift and add, at R_v = 3.93e13 lane operations/s, and one
+# exponential at 256 CUs x 4 SIMDs x 8 lanes/clk x 2.4 GHz of transcendental
+# issue (the published quarter rate, 9.8e12/s, is below what gfx950 was
+# measured to sustain, 1.83e13/s, so it would inflate the fraction).
+VECTOR_LANE_OPS_PEAK = VALU_PEAK_TFLOPS * 1e12 / 2.0
 EXP_PEAK = 256 * 4 * 8 * 2.4e9
 
 
@@ -66,12 +71,13 @@ def _cores():
         return os.cpu_count() or 1
 
 
-def measured_traffic():
+def measured_traffic(name):
     """HBM bytes per update launch from the committed FETCH_SIZE / WRITE_SIZE
-    summary, or None once the library source (kernels and the host runtime that
-    picks their layouts and sub-batches) has changed since it was taken."""
+    summary `profiles/<name>`, or None once the library source (kernels and the
+    host runtime that picks their layouts and sub-batches) has changed since it
+    was taken."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", "k_update_mfma_c2_traffic.md")
+    path = os.path.join(ROOT, "profiles", name)
     csrc = os.path.join(ROOT, "paper_2607_24741_amd", "csrc")
     try:
         fields = dict(line.split(": ", 1) for line in open(path).read().splitlines()
@@ -167,25 +173,112 @@ def study(args):
     print(json.dumps(rec), flush=True)
 
 
-def cpu_baseline(w, tol, cycles=600, lanes=None):
+def cpu_baseline(w, tol):
     """Oracle as it stands (test infrastructure, float64, not tuned) on a
-    bounded sample: the first `lanes` lanes of the window, each run for a fixed
-    `cycles` cycles with the two-sided audit after every cycle (the same work
-    per slot as the solver), one process per core."""
+    bounded sample of the window, each lane run for a fixed number of cycles
+    with the two-sided audit after every cycle (the same work per slot as the
+    solver), one process per core (at most 16). Mixed-size windows take 16
+    lanes at evenly spaced ranks of n_t m_t for 4 cycles; uniform ones their
+    first 16 lanes for 600 cycles."""
     import numpy as np
     import oracle
-    n_proc = min(16, _cores())
-    lanes = n_proc if lanes is None else lanes
-    sel = list(range(min(lanes, w.W)))
+    host = _cores()
+    n_proc = min(16, host)
+    area = w.n.astype(np.int64) * w.m
+    if len(set(area.tolist())) > 1:
+        order = np.argsort(area, kind="stable")
+        sel = [int(t) for t in order[np.linspace(0, w.W - 1, min(16, w.W)).round().astype(int)]]
+        cycles, what = 4, "lanes at evenly spaced ranks of n_t m_t"
+    else:
+        sel, cycles, what = list(range(min(16, w.W))), 600, "first lanes"
     t0 = time.perf_counter()
     oracle.solve(w.X, w.Y, w.a, w.b, w.eps, 1e-30, n=w.n, m=w.m, max_iter=cycles, lanes=sel,
                  processes=n_proc)
     dt = time.perf_counter() - t0
     slots = cycles * len(sel)
-    return {"value": slots / dt, "unit": "slots/s", "cores": n_proc, "kind": "oracle",
-            "sample": f"{len(sel)} lanes of the same window, {cycles} cycles each with a two-sided "
-                      f"audit after every cycle (float64 numpy, {n_proc} worker processes, "
-                      f"{dt:.1f} s wall)"}
+    pairs = 2.0 * cycles * float(area[sel].sum())
+    return {"value": slots / dt, "unit": "slots/s", "cores": n_proc, "host_cores": host,
+            "kind": "oracle", "pair_evals_per_s": pairs / dt,
+            "sample": f"{len(sel)} {what} of the same window, {cycles} cycles each with a "
+                      f"two-sided audit after every cycle (float64 numpy, {n_proc} worker "
+                      f"processes on a host with {host} cores, {dt:.1f} s wall)"}
+
+
+def roofline(w, args, stats, T, traffic_summary):
+    """The dominant kernel's roofline record (see the module docstring)."""
+    tpairs = sum(s.timed_pair_evals for s in stats)
+    ms_upd = sum(s.ms_update for s in stats)
+    launches = sum(s.update_launches for s in stats)
+    kept_pairs = sum(s.pair_evals for s in stats)
+    mat = args.materialize or w.d > 32
+    rec = {}
+    if mat:
+        per_pair, unit, peak, bound = 4.0, "GB/s", HBM_PEAK_GBS, "hbm"
+        algo = "4 bytes of materialised cost per valid (i,j) term"
+        kname = "k_mat_rows / k_mat_cols (f- and g-half-steps)"
+        scale = 1e9
+    else:
+        # FMA-equivalent flops of the vector-unit model: 2 (d + 4) per term
+        per_pair, unit, peak, bound = 2.0 * (w.d + 4), "TFLOP/s", VALU_PEAK_TFLOPS, "alu"
+        algo = ("(d + 4) lane operations per valid (i,j) term (the vector-unit model), "
+                "counted as multiply-adds (2 flops each)")
+        f64 = not (args.fast32 or args.force_valu) and w.d <= 16
+        kname = ("k_update_f64 (float64 state)" if f64 else
+                 "k_update_valu (float32 state)" if args.force_valu else
+                 "k_update_mfma (float32 state)") + " (f- and g-half-steps)"
+        scale = 1e12
+        rec["exp_bound_frac"] = (1.0 / EXP_PEAK) / ((w.d + 4) / VECTOR_LANE_OPS_PEAK)
+    achieved = per_pair * tpairs / (ms_upd * 1e-3) / scale
+    out = {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
+           "frac": achieved / peak, "traffic": measured_traffic(traffic_summary),
+           "kernel": kname, "avg_launch_us": 1e3 * ms_upd / max(1, launches),
+           "algorithmic": algo + ", lanes running at each launch's cycle",
+           "timed_pair_evals": tpairs, "timed_ms": ms_upd, "timed_launches": launches,
+           "device_frac_lb": per_pair * kept_pairs / T / scale / peak}
+    out.update(rec)
+    return out
+
+
+def mixture_extras(args, flags):
+    """The mixture window (W=64, n=m=1024, d=8): its execution modes at one
+    sub-batch each (static packing runs every lane to the common boundary,
+    logical masking keeps the full width) and its end-to-end batch time at
+    each tolerance of the sweep (automatic sub-batches)."""
+    import numpy as np
+    import torch
+    import paper_2607_24741_amd as ds
+    from paper_2607_24741_amd import workloads as wl
+    dev = torch.device("cuda:0")
+    w = wl.make("c2")
+    t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(dev)
+    X, Y, a, b, eps, n, m = (t(w.X), t(w.Y), t(w.a), t(w.b), t(w.eps), t(w.n), t(w.m))
+
+    def once(mode, tol, streams):
+        kw = dict(n=n, m=m, max_iter=w.max_iter, mode=mode, flags=flags, streams=streams,
+                  return_stats=True)
+        ds.solve(X, Y, a, b, eps, tol, **kw)   # warm
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        r = ds.solve(X, Y, a, b, eps, tol, **kw)
+        torch.cuda.synchronize()
+        return time.perf_counter() - t1, r
+
+    modes = {}
+    ta, _ = once("active", 1e-3, 1)
+    modes["active_ms"] = 1e3 * ta
+    for mname in ("static", "logical"):
+        dt, _ = once(mname, 1e-3, 1)
+        modes[mname + "_ms"] = 1e3 * dt
+        modes[mname + "_over_active"] = dt / ta
+    modes["sub_batches"] = 1
+    sweep = []
+    for tol in wl.TOL_SWEEP:
+        dt, r = once("active", tol, 0)
+        st = r[-1]
+        sweep.append({"tol": tol, "ms": 1e3 * dt, "slots_per_s": st.slots_update / dt,
+                      "slots": st.slots_update, "l_max": st.l_max, "sub_batches": st.sub_batches,
+                      "lanes_max_iter": int((r[4].cpu().numpy() == 1).sum())})
+    return modes, sweep
 
 
 def main():
@@ -195,17 +288,19 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--tol", type=float, default=1e-3)
     ap.add_argument("--mode", default="active", choices=["active", "static", "logical"])
-    ap.add_argument("--config", default="c2")
+    ap.add_argument("--config", default="c5")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--study", action="store_true",
                     help="measure the width-cost curve, width sweep and grouping instead")
-    ap.add_argument("--streams", type=int, default=0,
+    ap.add_argument("--streams", type=int, default=1,
                     help="concurrent sub-batches (0: the library's automatic choice)")
-    ap.add_argument("--precise", action="store_true", help="float64 state (DS_F_PRECISE)")
+    ap.add_argument("--fast32", action="store_true", help="float32 state (DS_F_FAST32)")
+    ap.add_argument("--force-valu", action="store_true",
+                    help="float32 state on the vector-ALU kernels (DS_F_FORCE_VALU)")
     ap.add_argument("--materialize", action="store_true", help="materialised cost (DS_F_MATERIALIZE)")
     ap.add_argument("--guard", action="store_true", help="guarded release (DS_F_GUARD)")
     ap.add_argument("--no-tol-sweep", action="store_true",
-                    help="skip the end-to-end batch times at the swept tolerances")
+                    help="skip the mixture window's modes and tolerance sweep")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on exactly one GPU: lanes are independent problems and the "
@@ -225,18 +320,17 @@ def main():
     w = wl.make(args.config)
     t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(dev)
     X, Y, a, b, eps, n, m = (t(w.X), t(w.Y), t(w.a), t(w.b), t(w.eps), t(w.n), t(w.m))
-    base_flags = ((ds.F_PRECISE if args.precise else 0) | (ds.F_MATERIALIZE if args.materialize else 0)
-                  | (ds.F_GUARD if args.guard else 0))
+    base_flags = ((ds.F_FAST32 if args.fast32 else 0) | (ds.F_FORCE_VALU if args.force_valu else 0)
+                  | (ds.F_MATERIALIZE if args.materialize else 0) | (ds.F_GUARD if args.guard else 0))
     need = ds.workspace_bytes(w.W, w.X.shape[1], w.Y.shape[1], w.d, tol=args.tol,
                               max_iter=w.max_iter, mode=args.mode, flags=base_flags,
                               streams=args.streams)
     ws = torch.empty(need + 256, dtype=torch.uint8, device=dev)
 
     def step(flags):
-        r = ds.solve(X, Y, a, b, eps, args.tol, n=n, m=m, max_iter=w.max_iter, mode=args.mode,
-                     flags=flags | base_flags, streams=args.streams, return_stats=True,
-                     workspace=ws)
-        return r
+        return ds.solve(X, Y, a, b, eps, args.tol, n=n, m=m, max_iter=w.max_iter, mode=args.mode,
+                        flags=flags | base_flags, streams=args.streams, return_stats=True,
+                        workspace=ws)
 
     for _ in range(args.warmup):
         step(0)
@@ -251,36 +345,8 @@ def main():
     status = last[4].cpu().numpy()
     slots = sum(s.slots_update for s in stats)
     pairs = sum(s.pair_evals + s.check_pair_evals for s in stats)
-    # roofline: the timed (sampled) launches of the update kernel -- both
-    # launches of every 32nd cycle of every sub-batch -- carry HIP events in
-    # their own dispatch, on the stream they run on. With concurrent
-    # sub-batches a launch shares the chip with the others' launches, so the
-    # per-launch figure understates the chip's rate; device_frac_lb is the
-    # algorithmic work of all kept half-steps over the whole step's wall time
-    # (a lower bound: it also charges the gaps and the other kernels).
-    tpairs = sum(s.timed_pair_evals for s in stats)
-    ms_upd = sum(s.ms_update for s in stats)
-    launches = sum(s.update_launches for s in stats)
-    kept_pairs = sum(s.pair_evals for s in stats)
-    # the roofline of the path the library takes for this shape
-    mat = args.materialize or w.d > 32
-    if mat:
-        # one float32 of cost streamed from HBM per (i, j) term
-        bound, unit, peak = "hbm", "GB/s", HBM_PEAK_GBS
-        per_pair, algo = 4.0, "4 bytes of materialised cost per valid (i,j) term"
-        kname = "k_mat_rows / k_mat_cols (f- and g-half-steps)"
-        achieved = per_pair * tpairs / (ms_upd * 1e-3) / 1e9
-    elif w.d >= 8 and not args.precise:
-        bound, unit, peak = "mfma", "TFLOP/s", MFMA_FP32_PEAK_TFLOPS
-        per_pair, algo = 2.0 * w.d, "2*d flops per valid (i,j) term"
-        kname = "k_update_mfma (f- and g-half-steps)"
-        achieved = per_pair * tpairs / (ms_upd * 1e-3) / 1e12
-    else:
-        bound, unit, peak = "alu", "TFLOP/s", VALU_FP32_PEAK_TFLOPS
-        per_pair, algo = 2.0 * w.d + 2.0, "2*d + 2 flops (dot, exp, add) per valid (i,j) term"
-        kname = ("k_update_f64 (f- and g-half-steps)" if args.precise else
-                 "k_update_mfma (f- and g-half-steps; the exponentials and sums bound it at small d)")
-        achieved = per_pair * tpairs / (ms_upd * 1e-3) / 1e12
+    f64 = not (args.fast32 or args.force_valu or args.materialize) and w.d <= 16
+    traffic_summary = f"k_update_{'f64' if f64 else 'mfma'}_{args.config}_traffic.md"
     rec = {
         "metric": "candidate-update slots/sec (end-to-end batch solve at tol 1e-3)",
         "value": slots / T,
@@ -292,7 +358,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f64" if args.precise else "f32",
+        "dtype": "f64" if f64 else "f32",
         "guarded_release": bool(args.guard),
         "data": "synthetic (seeded generator shaped like the paper's workload; no dataset)",
         "config": {"workload": wl.DESCRIPTIONS[args.config], "name": args.config, "W": w.W,
@@ -305,57 +371,11 @@ def main():
         "lanes_converged": int((status == 0).sum()),
         "lanes_max_iter": int((status == 1).sum()),
         "compactions": stats[-1].compactions,
-        "timed_update_launches_per_step": launches // args.steps,
-        "roofline": {"bound": bound, "achieved": achieved, "peak": peak,
-                     "unit": unit, "frac": achieved / peak,
-                     "traffic": measured_traffic() if (args.config == "c2" and bound == "mfma") else None,
-                     "kernel": kname,
-                     "avg_launch_us": 1e3 * ms_upd / max(1, launches),
-                     "algorithmic": algo + ", lanes running at each launch's cycle",
-                     "timed_pair_evals": tpairs, "timed_ms": ms_upd, "timed_launches": launches,
-                     "device_frac_lb": per_pair * kept_pairs / T / (1e9 if unit == "GB/s" else 1e12) / peak},
+        "timed_update_launches_per_step": sum(s.update_launches for s in stats) // args.steps,
+        "roofline": roofline(w, args, stats, T, traffic_summary),
     }
-    if not mat:
-        # the same launches priced by the vector-unit model of a matrix-free
-        # small-d half-step (what a kernel without matrix cores is bound by)
-        t_pe = max((w.d + 4) / VECTOR_LANE_OPS_PEAK, 1.0 / EXP_PEAK)
-        rec["roofline"]["vector_view"] = {
-            "model": "t_pe = max((d + 4) / R_v, 1 / R_e) seconds per valid (i,j) term",
-            "R_v_lane_ops_per_s": VECTOR_LANE_OPS_PEAK, "R_e_exp_per_s": EXP_PEAK,
-            "bound": "valu" if (w.d + 4) / VECTOR_LANE_OPS_PEAK >= 1.0 / EXP_PEAK else "exp",
-            "frac": t_pe * tpairs / (ms_upd * 1e-3),
-            "device_frac_lb": t_pe * kept_pairs / T}
-    if args.config == "c2" and not args.no_tol_sweep:
-        # the execution modes of the same window: static packing runs every lane
-        # to the common boundary, logical masking keeps the full width
-        modes = {}
-        for mname in ("static", "logical"):
-            ds.solve(X, Y, a, b, eps, args.tol, n=n, m=m, max_iter=w.max_iter, mode=mname,
-                     flags=base_flags, workspace=ws)   # warm
-            torch.cuda.synchronize()
-            t1 = time.perf_counter()
-            ds.solve(X, Y, a, b, eps, args.tol, n=n, m=m, max_iter=w.max_iter, mode=mname,
-                     flags=base_flags, workspace=ws)
-            torch.cuda.synchronize()
-            modes[mname + "_ms"] = 1e3 * (time.perf_counter() - t1)
-            modes[mname + "_over_active"] = modes[mname + "_ms"] / (1e3 * T / args.steps)
-        rec["modes"] = modes
-        # end-to-end batch time of one solve at each tolerance of the sweep
-        sweep = []
-        for tol in wl.TOL_SWEEP:
-            r = ds.solve(X, Y, a, b, eps, tol, n=n, m=m, max_iter=w.max_iter, mode=args.mode,
-                         flags=base_flags, return_stats=True, workspace=ws)   # warm
-            torch.cuda.synchronize()
-            t1 = time.perf_counter()
-            r = ds.solve(X, Y, a, b, eps, tol, n=n, m=m, max_iter=w.max_iter, mode=args.mode,
-                         flags=base_flags, return_stats=True, workspace=ws)
-            torch.cuda.synchronize()
-            dt = time.perf_counter() - t1
-            st = r[-1]
-            sweep.append({"tol": tol, "ms": 1e3 * dt, "slots_per_s": st.slots_update / dt,
-                          "slots": st.slots_update, "l_max": st.l_max,
-                          "lanes_max_iter": int((r[4].cpu().numpy() == 1).sum())})
-        rec["tol_sweep"] = sweep
+    if not args.no_tol_sweep:
+        rec["mixture_modes"], rec["mixture_tol_sweep"] = mixture_extras(args, base_flags)
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(w, args.tol)
     print(json.dumps(rec), flush=True)

@@ -87,7 +87,9 @@ ds::Layout plan(const ds_problem* pr, const ds_options* op, void* ws) {
   L.pad[0] = (int)align_up((size_t)pr->n_max, ds::kPad);
   L.pad[1] = (int)align_up((size_t)pr->m_max, ds::kPad);
   L.mat = uses_mat(pr, op) ? 1 : 0;
-  L.rows = (!L.mat && uses_mfma(pr, op)) ? ds::kRowsMfma : ds::kRowsValu;
+  L.rows = L.mat ? ds::kRowsValu
+                 : uses_f64(pr, op) ? ds::rows_f64(pr->d)
+                 : uses_mfma(pr, op) ? ds::kRowsMfma : ds::kRowsValu;
   L.es = uses_f64(pr, op) ? 2 : 1;
   if (L.mat) L.dp = 0;   // no point records: the cost is materialised
   L.rbmax = std::max(L.pad[0], L.pad[1]) / L.rows;
@@ -420,7 +422,10 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
   }
   auto pick = [&](int items, int role) -> int {
     if (mat) return VAR_MEDIUM;   // one layout: 64-row items, one block each
-    if (items < (use_mfma ? kMediumItemsMfma : kMediumItemsValu)) return VAR_NARROW;
+    // (the float64 kernel's items are 128 rows up to d = 12: half as many items per width)
+    const int medium = use_mfma ? kMediumItemsMfma
+                       : (precise && L.rows == 128) ? kMediumItemsF64 : kMediumItemsValu;
+    if (items < medium) return VAR_NARROW;
     return (use_mfma && tpg[role] <= 2) ? VAR_MEDIUM4 : VAR_MEDIUM;
   };
   auto blocks_of = [&](int items) -> int { return std::max(items, 0); };

@@ -47,6 +47,7 @@ constexpr int kMaxTimed = 4096;     // timed launches per sub-batch (DS_F_TIMING
 // launch-variant thresholds (work items of the launch, see launch_update)
 constexpr int kMediumItemsMfma = 384;
 constexpr int kMediumItemsValu = 256;
+constexpr int kMediumItemsF64 = 128;
 
 // Per physical slot lane descriptor; moved by compaction with the rest of the
 // lane-indexed state.
@@ -146,6 +147,9 @@ struct Layout {
   int guard;
   size_t bytes;
 };
+
+// rows per work item of the float64-state kernel: two per lane up to d = 12
+__host__ __device__ constexpr int rows_f64(int d) { return d <= 12 ? 128 : 64; }
 
 // work items of one lane-side: one per block of `rows` rows (all columns)
 __host__ __device__ inline int row_blocks(int nrows, int rows) { return (nrows + rows - 1) / rows; }

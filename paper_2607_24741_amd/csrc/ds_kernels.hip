@@ -243,7 +243,8 @@ __device__ __forceinline__ bool check_facts(const Launch& L, const Pass& P, int 
 
 // ----------------------------------------------------------- item epilogue
 // Finish of one work item by wave 0 alone, after the column groups were merged.
-// Lane l owns row rb0 * UNIT + l when `owner` (merged (Mt, St) of that row).
+// Lane l owns rows rb0 * UNIT + 64 r + l (r < R) when `owner[r]` (merged
+// (Mt, St) of that row; R > 1 only with one aggregate per item, UNIT = 64 R).
 // Writes the new lse / gam (update kind), one aggregate per UNIT-row block
 // (NU of them), and -- for the deciding column check -- takes the lane's
 // retirement decision in the last arriving item of the lane.
@@ -252,37 +253,44 @@ __device__ __forceinline__ double log2_t(double x) { return log2(x); }
 __device__ __forceinline__ float exp2_t(float x) { return ex2(x); }
 __device__ __forceinline__ double exp2_t(double x) { return exp2(x); }
 
-template <int UNIT, int NU, typename T>
-__device__ void finish_rows(const Launch& L, const Pass& P, int s, const SlotInfo& si, int rb0,
-                            bool owner, bool live, bool fast, float Mf, T lse_old, T lm,
-                            float w, T Mt, T St, float rhat) {
-  static_assert(UNIT * NU <= 64, "one wave owns the rows of an item");
+template <int UNIT, int NU, int R, typename T>
+__device__ void finish_rows_r(const Launch& L, const Pass& P, int s, const SlotInfo& si, int rb0,
+                              const bool (&owner)[R], const bool (&live)[R], bool fast, float Mf,
+                              const T (&lse_old)[R], const T (&lm)[R], const float (&w)[R],
+                              const T (&Mt)[R], const T (&St)[R], float rhat) {
+  static_assert(UNIT * NU <= 64 * R, "one wave owns the rows of an item");
+  static_assert(R == 1 || (NU == 1 && UNIT == 64 * R), "several rows per lane: one aggregate");
   const int lane = threadIdx.x & 63;
   const int nrows = P.role ? si.m : si.n;
   const int nrb = row_blocks(nrows, UNIT);
   const bool frozen = (L.mode == MODE_LOGICAL) && si.done;
   const T M = (T)Mf;
   float rho = 0.f, dmin = INFINITY, dmax = -INFINITY, bad = 0.f;
-  T lse_new = (T)INFINITY, gam_new = -(T)INFINITY;
-  if (owner) {
+  T lse_new[R], gam_new[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    lse_new[r] = (T)INFINITY;
+    gam_new[r] = -(T)INFINITY;
+    if (!owner[r]) continue;
     if (P.kind == KIND_UPDATE) {
-      if (live) {
-        const T anchor = fast ? lse_old + M : (T)0;   // the sweep's row anchor
-        lse_new = anchor + (Mt + log2_t(St));
-        gam_new = lm - lse_new;
-        const float dl = (float)(lse_new - lse_old);
-        if (isfinite(dl)) { dmin = dl; dmax = dl; } else { bad = 1.f; }
+      if (live[r]) {
+        const T anchor = fast ? lse_old[r] + M : (T)0;   // the sweep's row anchor
+        lse_new[r] = anchor + (Mt[r] + log2_t(St[r]));
+        gam_new[r] = lm[r] - lse_new[r];
+        const float dl = (float)(lse_new[r] - lse_old[r]);
+        if (isfinite(dl)) { dmin = fminf(dmin, dl); dmax = fmaxf(dmax, dl); } else { bad = 1.f; }
         if (P.role == 0) {
           // R_i / a_i of the input state = 2^(lse_new - lse_old), formed so the
           // large terms cancel exactly before rounding
-          const T ratio = fast ? St * exp2_t(anchor - lse_old) : St * exp2_t(Mt - lse_old);
-          rho = w * fabsf((float)(ratio - (T)1));
+          const T ratio = fast ? St[r] * exp2_t(anchor - lse_old[r])
+                               : St[r] * exp2_t(Mt[r] - lse_old[r]);
+          rho += w[r] * fabsf((float)(ratio - (T)1));
         }
       }
-    } else if (live) {
+    } else if (live[r]) {
       // check: terms were pi_ij / 2^lm_i, so St * 2^Mt = R_i / a_i
-      const T ratio = St * exp2_t(Mt);
-      rho = w * fabsf((float)(ratio - (T)1));
+      const T ratio = St[r] * exp2_t(Mt[r]);
+      rho += w[r] * fabsf((float)(ratio - (T)1));
     }
   }
   // one aggregate per UNIT-row block: {sum rho, min, max of the lse change, bad}
@@ -309,10 +317,14 @@ __device__ void finish_rows(const Launch& L, const Pass& P, int s, const SlotInf
       for (int u = 0; u < nu; ++u) dst[u] = ag[u];
     // the new state goes out last: nothing after it reuses its registers, so
     // the wave ends without waiting for the stores
-    if (owner && P.kind == KIND_UPDATE && !frozen) {
-      const size_t idx = (size_t)s * P.padr + rb0 * UNIT + lane;
-      reinterpret_cast<T*>(P.lse_out)[idx] = lse_new;
-      reinterpret_cast<T*>(P.gam_out)[idx] = gam_new;
+    if (P.kind == KIND_UPDATE && !frozen) {
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        if (!owner[r]) continue;
+        const size_t idx = (size_t)s * P.padr + rb0 * UNIT + 64 * r + lane;
+        reinterpret_cast<T*>(P.lse_out)[idx] = lse_new[r];
+        reinterpret_cast<T*>(P.gam_out)[idx] = gam_new[r];
+      }
     }
     return;
   }
@@ -363,6 +375,18 @@ __device__ void finish_rows(const Launch& L, const Pass& P, int s, const SlotInf
   } else if (finite && r <= L.tol) {
     atomicAdd(&L.ctrl->missed_ready, 1);   // shadow replay: the screen missed it
   }
+}
+
+// One row per lane.
+template <int UNIT, int NU, typename T>
+__device__ __forceinline__ void finish_rows(const Launch& L, const Pass& P, int s,
+                                            const SlotInfo& si, int rb0, bool owner, bool live,
+                                            bool fast, float Mf, T lse_old, T lm, float w, T Mt,
+                                            T St, float rhat) {
+  const bool o[1] = {owner}, lv[1] = {live};
+  const T lo[1] = {lse_old}, l2[1] = {lm}, mt[1] = {Mt}, st[1] = {St};
+  const float ww[1] = {w};
+  finish_rows_r<UNIT, NU, 1, T>(L, P, s, si, rb0, o, lv, fast, Mf, lo, l2, ww, mt, st, rhat);
 }
 
 // XCD-aware item order. Consecutive workgroups are dispatched to the 8 XCDs
@@ -816,17 +840,35 @@ void k_update_valu(Launch L) {
 
 // ------------------------------------------------- float64 (precise) half-step
 // The vector-ALU half-step with the state (records, log masses, lse, gam) in
-// float64 and every exponent formed in float64; only the final, anchored
-// exponent (|z| small for the terms that matter) is rounded to float32 for
-// v_exp_f32, and the sums run in float64. Anchored sums are used only when
-// the bound's spread is at most kFastRangePrecise.
+// float64 and every exponent formed in float64 -- d fused multiply-adds and one
+// add -- before it is rounded once to float32 for v_exp_f32 (anchored sums are
+// used while the bound's spread is at most kFastRangePrecise). The terms of one
+// 32-column tile are summed in float32 and each tile's sum is added in float64.
+//
+// A work item is 64 R rows (rows_f64(D): R = 2 up to d = 12, above which the
+// two rows' coordinates no longer fit in registers beside a column's): lane l
+// owns rows l + 64 r (r < R), so every column value read from LDS serves R
+// terms. Column data is the same for
+// every lane; each wave stages its tiles in its own LDS double buffer
+// (coalesced loads: records, then the column operand gam written into slot D
+// of each column -- the record's padding double when D is odd) and reads them
+// back as broadcasts. Only the wave itself touches its buffer, so no block
+// barrier is needed (a wave's LDS operations complete in order).
+// The second launch bound (minimum waves per SIMD) lets the allocator keep the
+// two rows' coordinates and the prefetched tile in registers without spilling.
+template <int D>
+constexpr int f64_waves_per_simd() { return D <= 4 ? 4 : (D <= 7 ? 3 : (D <= 12 ? 2 : 3)); }
+
 template <int D, int GW>
-__global__ __launch_bounds__(64 * (kGroups / GW), (kGroups / GW == 8 ? 2 : (D >= 15 ? 3 : 4)))
+__global__ __launch_bounds__(64 * (kGroups / GW), (f64_waves_per_simd<D>()))
 void k_update_f64(Launch L) {
   note_progress(L);
-  constexpr int DPc = D + (D & 1);
-  __shared__ double2 sh_part[kGroups][kRowsValu];
-  __shared__ __align__(16) double sh_tile[kGroups / GW][2][kColTile * DPc + kColTile];
+  constexpr int ROWS = rows_f64(D);
+  constexpr int R = ROWS / 64;
+  constexpr int DP = D + (D & 1);        // record stride in HBM (doubles)
+  constexpr int DG = (D + 2) & ~1;       // column stride in LDS: coordinates, gam, (pad)
+  __shared__ double2 sh_part[kGroups][ROWS];
+  __shared__ __align__(16) double sh_tile[kGroups / GW][2][kColTile * DG];
   const int b = blockIdx.x;
   const int pi = b >= L.nb0;
   const Pass P = L.p[pi];
@@ -843,50 +885,57 @@ void k_update_f64(Launch L) {
   }
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform (SGPR)
-  const int i = rb * kRowsValu + lane;
-  constexpr int DP = D + (D & 1);
-  const size_t ridx = (size_t)s * P.padr + i;
-  const double lse_old = reinterpret_cast<const double*>(P.lse_in)[ridx];
-  const bool in_prefix = i < nrows;
-  const bool owner = wave == 0 && in_prefix;
-  double lm = 0.0;
-  float w = 0.f;
-  if (owner) lm = reinterpret_cast<const double*>(P.lm_row)[ridx];
-  double xr[D];
-  const double* rrow = reinterpret_cast<const double*>(P.rec_row) + ridx * DP;
+  double lse_old[R], lm[R], xr[R][D];
+  bool in_prefix[R], owner[R];
+  float w[R];
 #pragma unroll
-  for (int k = 0; k < D; ++k) xr[k] = rrow[k];
+  for (int r = 0; r < R; ++r) {
+    const int i = rb * ROWS + 64 * r + lane;
+    const size_t ridx = (size_t)s * P.padr + i;
+    lse_old[r] = reinterpret_cast<const double*>(P.lse_in)[ridx];
+    in_prefix[r] = i < nrows;
+    owner[r] = wave == 0 && in_prefix[r];
+    lm[r] = 0.0;
+    w[r] = 0.f;
+    if (owner[r]) lm[r] = reinterpret_cast<const double*>(P.lm_row)[ridx];
+    const double* rrow = reinterpret_cast<const double*>(P.rec_row) + ridx * DP;
+#pragma unroll
+    for (int k = 0; k < D; ++k) xr[r][k] = rrow[k];
+  }
   bool fast = false;
   float M = 0.f;
   if (upd) {
     update_facts(L, P, s, ncols, fast, M, kFastRangePrecise);
     if (!item_live(L, P, s, si, c_fin, c_A)) return;
   }
-  if (owner) w = P.w_row[(size_t)si.lane * P.w_ld + i];   // caller masses, by lane id
-  const bool live = in_prefix && (lse_old != (double)INFINITY);
-  double bias = 0.0;
-  if (live) {
-    if (!upd) bias = -lse_old;
-    else if (fast) bias = -(lse_old + (double)M);
+  bool live[R];
+  double bias[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int i = rb * ROWS + 64 * r + lane;
+    if (owner[r]) w[r] = P.w_row[(size_t)si.lane * P.w_ld + i];   // caller masses, by lane id
+    live[r] = in_prefix[r] && (lse_old[r] != (double)INFINITY);
+    bias[r] = 0.0;
+    if (live[r]) {
+      if (!upd) bias[r] = -lse_old[r];
+      else if (fast) bias[r] = -(lse_old[r] + (double)M);
+    }
   }
 
   const int ct = (ncols + kColTile - 1) / kColTile;
   const int tpg = (ct + kGroups - 1) / kGroups;
-  // Column data is the same for every lane, and in float64 one column is up
-  // to 2 (d + 1) dwords. Each wave stages its tiles in its own LDS double
-  // buffer (records, then gam) with coalesced loads and reads them back as
-  // broadcasts; only the wave itself touches its buffer, so no block barrier
-  // is needed (a wave's LDS operations complete in order).
-  constexpr int TREC = kColTile * DP;   // doubles of records per tile
+  constexpr int TREC = kColTile * DP;   // doubles of records per tile in HBM
   constexpr int NV2 = TREC / 2;         // double2 per tile
   constexpr int PER = (NV2 + 63) / 64;  // double2 per lane
+  static_assert(PER <= 4, "a float64 tile is at most 4 double2 per lane");
   double* buf0 = sh_tile[wave][0];
   double* buf1 = sh_tile[wave][1];
   const double* rec_lane = reinterpret_cast<const double*>(P.rec_col) + (size_t)s * P.padc * DP;
   const double* gam_lane = reinterpret_cast<const double*>(P.gam_col) + (size_t)s * P.padc;
   // lane l moves double2 number q * 64 + l of a tile (clamped: the last lanes
-  // of a partial round repeat an in-range element, harmlessly)
-  static_assert(PER <= 4, "a float64 tile is at most 4 double2 per lane");
+  // of a partial round repeat an in-range element, harmlessly); double2 e of
+  // the HBM tile is pair e % (DP / 2) of column e / (DP / 2), which lands at
+  // double2 (e / (DP / 2)) * (DG / 2) + e % (DP / 2) of the LDS tile
 #define DS_F64_LD(q) ((q) < PER ? src_[min((q) * 64 + lane, NV2 - 1)] : make_double2(0.0, 0.0))
 #define DS_F64_FETCH(t)                                                                    \
   do {                                                                                     \
@@ -894,21 +943,25 @@ void k_update_f64(Launch L) {
     pv0 = DS_F64_LD(0); pv1 = DS_F64_LD(1); pv2 = DS_F64_LD(2); pv3 = DS_F64_LD(3);        \
     pg = gam_lane[(t) * kColTile + (lane & (kColTile - 1))];                               \
   } while (0)
-#define DS_F64_ST(q, v) \
-  if ((q) < PER) reinterpret_cast<double2*>(dst_)[min((q) * 64 + lane, NV2 - 1)] = (v)
+#define DS_F64_ST(q, v)                                                                    \
+  if ((q) < PER) {                                                                         \
+    const int e_ = min((q) * 64 + lane, NV2 - 1);                                          \
+    reinterpret_cast<double2*>(dst_)[(e_ / (DP / 2)) * (DG / 2) + e_ % (DP / 2)] = (v);    \
+  }
 #define DS_F64_STASH(dst)                                                                  \
   do {                                                                                     \
     double* dst_ = (dst);                                                                  \
     DS_F64_ST(0, pv0); DS_F64_ST(1, pv1); DS_F64_ST(2, pv2); DS_F64_ST(3, pv3);             \
-    if (lane < kColTile) dst_[TREC + lane] = pg;                                           \
+    if (lane < kColTile) dst_[lane * DG + D] = pg;                                         \
     __builtin_amdgcn_wave_barrier();                                                       \
   } while (0)
 #pragma unroll
   for (int u = 0; u < GW; ++u) {
     const int g = wave * GW + u;
     const int tA = min(ct, g * tpg), tB = min(ct, g * tpg + tpg);
-    double mrun = fast ? 0.0 : -(double)INFINITY, srun = 0.0;
-    double sacc[2] = {0.0, 0.0};
+    double mrun[R], srun[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) { mrun[r] = fast ? 0.0 : -(double)INFINITY; srun[r] = 0.0; }
     if (tA < tB) {
       double2 pv0, pv1, pv2, pv3;
       double pg;
@@ -923,61 +976,85 @@ void k_update_f64(Launch L) {
       const bool more = t + 1 < tB;
       if (more) DS_F64_FETCH(t + 1);
       if (fast) {
-        float tacc[2] = {0.f, 0.f};
+        // CV columns per step (one at large D, where the column values of
+        // two steps would not fit in registers beside the rows')
+        constexpr int CV = D <= 8 ? 2 : 1;
+        float tacc[R][2];
+#pragma unroll
+        for (int r = 0; r < R; ++r) tacc[r][0] = tacc[r][1] = 0.f;
         for (int c = 0; c < kColTile; c += 2) {
-#pragma unroll
+#pragma unroll CV
           for (int v = 0; v < 2; ++v) {
-            const double* cj = cur + (c + v) * DP;
-            double z = cur[TREC + c + v] + bias;
+            double cj[D + 1];
 #pragma unroll
-            for (int k = 0; k < D; ++k) z = fma(xr[k], cj[k], z);
-            tacc[v] += ex2((float)z);
+            for (int k = 0; k <= D; ++k) cj[k] = cur[(c + v) * DG + k];
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+              double z = cj[D] + bias[r];
+#pragma unroll
+              for (int k = 0; k < D; ++k) z = fma(xr[r][k], cj[k], z);
+              tacc[r][v] += ex2((float)z);
+            }
           }
         }
-        sacc[0] += (double)(tacc[0] + tacc[1]);   // the tile's sum, added in float64
+#pragma unroll
+        for (int r = 0; r < R; ++r) srun[r] += (double)(tacc[r][0] + tacc[r][1]);
       } else {
         for (int c = 0; c < kColTile; c += 4) {
-          double z[4];
 #pragma unroll
-          for (int v = 0; v < 4; ++v) {
-            const double* cj = cur + (c + v) * DP;
-            double zz = cur[TREC + c + v] + bias;
+          for (int r = 0; r < R; ++r) {
+            double z[4];
 #pragma unroll
-            for (int k = 0; k < D; ++k) zz = fma(xr[k], cj[k], zz);
-            z[v] = zz;
+            for (int v = 0; v < 4; ++v) {
+              const double* cj = cur + (c + v) * DG;
+              double zz = cj[D] + bias[r];
+#pragma unroll
+              for (int k = 0; k < D; ++k) zz = fma(xr[r][k], cj[k], zz);
+              z[v] = zz;
+            }
+            const double tm = fmax(fmax(z[0], z[1]), fmax(z[2], z[3]));
+            const double mn = fmax(mrun[r], tm);
+            const double mref = (mn == -(double)INFINITY) ? 0.0 : mn;
+            const double ts =
+                ((double)ex2((float)(z[0] - mref)) + (double)ex2((float)(z[1] - mref))) +
+                ((double)ex2((float)(z[2] - mref)) + (double)ex2((float)(z[3] - mref)));
+            srun[r] = srun[r] * (double)ex2((float)(mrun[r] - mref)) + ts;
+            mrun[r] = mn;
           }
-          const double tm = fmax(fmax(z[0], z[1]), fmax(z[2], z[3]));
-          const double mn = fmax(mrun, tm);
-          const double mref = (mn == -(double)INFINITY) ? 0.0 : mn;
-          const double ts = ((double)ex2((float)(z[0] - mref)) + (double)ex2((float)(z[1] - mref))) +
-                            ((double)ex2((float)(z[2] - mref)) + (double)ex2((float)(z[3] - mref)));
-          srun = srun * (double)ex2((float)(mrun - mref)) + ts;
-          mrun = mn;
         }
       }
       __builtin_amdgcn_wave_barrier();
       if (more) DS_F64_STASH(nxt);
     }
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+      sh_part[g][64 * r + lane] = make_double2(mrun[r], srun[r]);   // (-inf, 0) if empty
+  }
 #undef DS_F64_FETCH
 #undef DS_F64_STASH
 #undef DS_F64_LD
 #undef DS_F64_ST
-    if (fast) srun = sacc[0];
-    sh_part[g][lane] = make_double2(mrun, srun);   // (-inf, 0) for an empty group
-  }
   __syncthreads();
   if (wave != 0) return;
-  double Mt = 0.0, St = 0.0;
-  if (owner) {
+  double Mt[R], St[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    Mt[r] = 0.0;
+    St[r] = 0.0;
+    if (!owner[r]) continue;
     double mx = -(double)INFINITY;
 #pragma unroll
-    for (int g = 0; g < kGroups; ++g) mx = fmax(mx, sh_part[g][lane].x);
-    Mt = (mx == -(double)INFINITY) ? 0.0 : mx;
+    for (int g = 0; g < kGroups; ++g) mx = fmax(mx, sh_part[g][64 * r + lane].x);
+    Mt[r] = (mx == -(double)INFINITY) ? 0.0 : mx;
 #pragma unroll
-    for (int g = 0; g < kGroups; ++g) St += sh_part[g][lane].y * (double)ex2((float)(sh_part[g][lane].x - Mt));
+    for (int g = 0; g < kGroups; ++g)
+      St[r] += sh_part[g][64 * r + lane].y * (double)ex2((float)(sh_part[g][64 * r + lane].x - Mt[r]));
   }
-  finish_rows<kRowsValu, 1, double>(L, P, s, si, rb, owner, live && owner, fast, M, lse_old, lm, w,
-                                    Mt, St, rhat);
+  bool lo[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) lo[r] = live[r] && owner[r];
+  finish_rows_r<ROWS, 1, R, double>(L, P, s, si, rb, owner, lo, fast, M, lse_old, lm, w, Mt, St,
+                                    rhat);
 }
 
 // ----------------------------------------------- materialised-cost half-steps
@@ -1450,8 +1527,8 @@ __global__ __launch_bounds__(kGuardThreads) void k_check64(Launch L, GuardArgs G
   __shared__ double sh_y[DR == 0 ? 1 : CH * DS];
   __shared__ double sh_pot[CH];
   __shared__ double sh_acc[kGuardThreads];
-  __shared__ double sh_row[64];
-  __shared__ int sh_bad[64];
+  __shared__ double sh_row[128];
+  __shared__ int sh_bad[128];
   const int b = blockIdx.x;
   const int pi = b >= L.nb0;
   const Pass& P = L.p[pi];
@@ -1469,7 +1546,7 @@ __global__ __launch_bounds__(kGuardThreads) void k_check64(Launch L, GuardArgs G
   }
   if (!item_live(L, P, s, si, c_fin, c_A) || !checked) return;
   const int lane_id = si.lane;
-  const int R = L.rows;                        // 32 or 64 rows per item
+  const int R = L.rows;                        // 32, 64 or 128 rows per item
   const int nph = kGuardThreads / R;           // column phases
   const int tid = threadIdx.x;
   const int r = tid % R, ph = tid / R;
@@ -1531,7 +1608,7 @@ __global__ __launch_bounds__(kGuardThreads) void k_check64(Launch L, GuardArgs G
   // row totals: the phases' partial sums in phase order, |marginal - mass|
   sh_acc[tid] = acc;
   __syncthreads();
-  if (ph == 0 && r < 64) {
+  if (ph == 0) {
     double tot = 0.0;
     for (int q = 0; q < nph; ++q) tot += sh_acc[q * R + r];
     sh_row[r] = live ? fabs(tot - (double)wr[i]) : 0.0;
@@ -1917,7 +1994,7 @@ hipError_t launch_update_mat(const Launch& a, int blocks, hipStream_t st, hipEve
 }
 hipError_t launch_check64(const Launch& a, const GuardArgs& g, int blocks, hipStream_t st) {
   if (blocks <= 0) return hipSuccess;
-  if (a.rows != 32 && a.rows != 64) return hipErrorInvalidValue;   // rows per item
+  if (a.rows != 32 && a.rows != 64 && a.rows != 128) return hipErrorInvalidValue;
   const dim3 grid(blocks), block(kGuardThreads);
   if (g.d <= 4) hipLaunchKernelGGL(k_check64<4>, grid, block, 0, st, a, g);
   else if (g.d <= 8) hipLaunchKernelGGL(k_check64<8>, grid, block, 0, st, a, g);
