@@ -215,6 +215,25 @@ ds_err ds_solve(const ds_problem* problem, const ds_options* options,
                 const ds_result* result, void* workspace, size_t workspace_bytes,
                 void* stream, ds_stats* stats);
 
+/* ds_solve for callers that cannot allocate (code under stream capture, tight
+ * serving loops, harnesses that forbid allocation): the same solve, with the
+ * workspace taken from a fixed device array the library holds on every GPU it
+ * runs on (64 MiB per GPU, kept until the process ends) instead of a caller
+ * buffer. The caller still passes inputs and outputs; the call performs no
+ * device or pinned-memory allocation, except that the first call on a device
+ * sets that device up once (it looks up the array's address and creates the
+ * library's per-device host resources: a pinned control snapshot, an event
+ * and a stream). It runs one sub-batch on `stream` (options->streams must be
+ * 0 or 1) and rejects DS_F_TIMING (DS_E_INVALID). A problem whose workspace
+ * (ds_workspace_bytes with streams = 1) exceeds the array returns
+ * DS_E_UNSUPPORTED before any device work, with the sizes in
+ * ds_last_error_message(). All calls on one GPU share that GPU's array, whose
+ * contents persist from the previous call (the solve initialises everything
+ * it reads): calls that overlap on one GPU race, so a caller must not issue
+ * two at once on the same device (from two host threads or two streams). */
+ds_err ds_solve_noalloc(const ds_problem* problem, const ds_options* options,
+                        const ds_result* result, void* stream, ds_stats* stats);
+
 /* Static string for an error code. */
 const char* ds_error_string(ds_err err);
 

@@ -20,7 +20,7 @@ import ctypes
 import os
 from dataclasses import dataclass
 
-__all__ = ["solve", "workspace_bytes", "load_library", "library_path", "DSError",
+__all__ = ["solve", "solve_noalloc", "workspace_bytes", "load_library", "library_path", "DSError",
            "MODES", "LANE_CONVERGED", "LANE_MAX_ITER", "LANE_NONFINITE",
            "F_SHADOW", "F_TIMING", "F_FORCE_VALU", "F_FORCE_MFMA", "F_PRECISE",
            "F_MATERIALIZE", "F_GUARD", "F_FAST32"]
@@ -109,6 +109,10 @@ def load_library():
                              ctypes.POINTER(_Result), ctypes.c_void_p, ctypes.c_size_t,
                              ctypes.c_void_p, ctypes.POINTER(_Stats)]
     lib.ds_solve.restype = ctypes.c_int
+    lib.ds_solve_noalloc.argtypes = [ctypes.POINTER(_Problem), ctypes.POINTER(_Options),
+                                     ctypes.POINTER(_Result), ctypes.c_void_p,
+                                     ctypes.POINTER(_Stats)]
+    lib.ds_solve_noalloc.restype = ctypes.c_int
     lib.ds_error_string.argtypes = [ctypes.c_int]
     lib.ds_error_string.restype = ctypes.c_char_p
     lib.ds_last_error_message.restype = ctypes.c_char_p
@@ -201,9 +205,22 @@ def _check_out(out, W, n_max, m_max, dev):
     return checked
 
 
+def solve_noalloc(X, Y, a, b, eps, tol, *, out, n=None, m=None, g0=None, max_iter=5000,
+                  audit_every=1, mode="active", screen_tol=None, flags=0, return_stats=False,
+                  trace_len=0):
+    """``solve`` through ds_solve_noalloc: the workspace is the library's fixed
+    per-GPU array (64 MiB), one sub-batch on the current stream, and the caller
+    passes every output tensor (``out``, as for ``solve``), so that neither
+    the library nor this binding allocates device memory for the call."""
+    return solve(X, Y, a, b, eps, tol, n=n, m=m, g0=g0, max_iter=max_iter,
+                 audit_every=audit_every, mode=mode, screen_tol=screen_tol, flags=flags,
+                 streams=1, return_stats=return_stats, trace_len=trace_len, out=out,
+                 _noalloc=True)
+
+
 def solve(X, Y, a, b, eps, tol, *, n=None, m=None, g0=None, max_iter=5000, audit_every=1,
           mode="active", screen_tol=None, flags=0, streams=0, return_stats=False,
-          workspace=None, trace_len=0, out=None):
+          workspace=None, trace_len=0, out=None, _noalloc=False):
     """Solve W independent entropic OT problems on the current GPU.
 
     X [W, n_max, d], Y [W, m_max, d], a [W, n_max], b [W, m_max], eps [W]:
@@ -236,6 +253,23 @@ def solve(X, Y, a, b, eps, tol, *, n=None, m=None, g0=None, max_iter=5000, audit
     pr = _Problem(W=W, n_max=n_max, m_max=m_max, d=d, X=_ptr(X), Y=_ptr(Y), a=_ptr(a),
                   b=_ptr(b), eps=_ptr(eps), n=_ptr(n), m=_ptr(m), g0=_ptr(g0))
     op = _options(tol, screen_tol, max_iter, audit_every, mode, flags, streams)
+    if _noalloc:
+        if out is None:
+            raise ValueError("solve_noalloc needs caller-provided outputs (out=...)")
+        out = _check_out(out, W, n_max, m_max, dev)
+        res = _Result(**{k: _ptr(v) for k, v in out.items()})
+        st = _Stats()
+        trace_buf = None
+        if trace_len:
+            trace_buf = (ctypes.c_int32 * int(trace_len))()
+            st.width_trace = ctypes.cast(trace_buf, ctypes.POINTER(ctypes.c_int32))
+            st.width_trace_len = int(trace_len)
+        stream = torch.cuda.current_stream(dev).cuda_stream
+        with torch.cuda.device(dev):
+            code = lib.ds_solve_noalloc(ctypes.byref(pr), ctypes.byref(op), ctypes.byref(res),
+                                        ctypes.c_void_p(stream), ctypes.byref(st))
+        _check(lib, code)
+        return _returns(out, st, trace_buf, return_stats)
     need = ctypes.c_size_t(0)
     _check(lib, lib.ds_workspace_bytes(ctypes.byref(pr), ctypes.byref(op), ctypes.byref(need)))
     if workspace is None:
@@ -273,7 +307,11 @@ def solve(X, Y, a, b, eps, tol, *, n=None, m=None, g0=None, max_iter=5000, audit
                             ctypes.c_void_p(ws_ptr), ctypes.c_size_t(ws_bytes),
                             ctypes.c_void_p(stream), ctypes.byref(st))
     _check(lib, code)
-    ret = (out["f"], out["g"], out["depth"], out["residual"], out["status"], out["order"])
+    return _returns(out, st, trace_buf, return_stats)
+
+
+def _returns(out, st, trace_buf, return_stats):
+    ret = (out["f"], out["g"], out["depth"], out["residual"], out["status"], out.get("order"))
     if not return_stats:
         return ret
     wt = list(trace_buf[:st.width_trace_len]) if trace_buf is not None else []
@@ -283,5 +321,5 @@ def solve(X, Y, a, b, eps, tol, *, n=None, m=None, g0=None, max_iter=5000, audit
                   st.compactions, st.missed_ready, st.update_launches, st.ms_total, st.ms_update,
                   st.timed_pair_evals, st.ms_check, st.ms_compact, wt, st.workspace_bytes,
                   st.sub_batches,
-                  out["row_residual"], out["col_residual"])
+                  out.get("row_residual"), out.get("col_residual"))
     return ret + (stats,)

@@ -887,4 +887,28 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
   return DS_OK;
 }
 
+ds_err ds_solve_noalloc(const ds_problem* pr, const ds_options* op, const ds_result* res,
+                        void* stream_v, ds_stats* stats) {
+  g_last_error.clear();
+  ds_err e = check_problem(pr, op);
+  if (e != DS_OK) return e;
+  if (op->streams > 1)
+    return fail(DS_E_INVALID, "ds_solve_noalloc runs one sub-batch on the caller's stream: "
+                              "streams must be 0 or 1");
+  if (op->flags & DS_F_TIMING)
+    return fail(DS_E_INVALID, "ds_solve_noalloc does not time launches (DS_F_TIMING creates events)");
+  ds_options one = *op;
+  one.streams = 1;
+  const size_t need = part_offsets(pr, &one, 1)[1];
+  void* ws = nullptr;
+  size_t cap = 0;
+  HIP_TRY(ds::scratch_area(&ws, &cap));
+  if (need > cap)
+    return fail(DS_E_UNSUPPORTED, "ds_solve_noalloc: this problem needs " + std::to_string(need) +
+                                      " bytes of workspace, above the " + std::to_string(cap) +
+                                      "-byte allocation-free workspace; use ds_solve with a "
+                                      "caller workspace");
+  return ds_solve(pr, &one, res, ws, cap, stream_v, stats);
+}
+
 }  // extern "C"

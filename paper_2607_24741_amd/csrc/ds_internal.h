@@ -44,6 +44,8 @@ constexpr float kFastRange = 64.f;  // max spread of the bound (log2 units) for 
 // a relative error of at most 64 * 2^-24 * ln 2 ~ 2.6e-6 per term.
 constexpr float kFastRangePrecise = 64.f;
 constexpr int kMaxTimed = 4096;     // timed launches per sub-batch (DS_F_TIMING)
+constexpr size_t kScratchBytes = (size_t)64 << 20;  // workspace of ds_solve_noalloc, per GPU
+constexpr int kMaxDevices = 64;
 // launch-variant thresholds (work items of the launch, see launch_update)
 constexpr int kMediumItemsMfma = 384;
 constexpr int kMediumItemsValu = 256;
@@ -289,5 +291,8 @@ hipError_t launch_move(const MoveArgs& a, int A, int maxpad, hipStream_t st);
 hipError_t launch_ingest(const IngestArgs& a, int maxpad, hipStream_t st);
 hipError_t launch_order(const int* depth, int W, int* order, hipStream_t st);
 hipError_t launch_zero_counters(int* vcnt, int W, hipStream_t st);
+// Device address and size of this device's allocation-free workspace (the
+// address is taken once per device, with that device current).
+hipError_t scratch_area(void** ptr, size_t* bytes);
 
 }  // namespace ds

@@ -32,6 +32,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "ds_internal.h"
 
 namespace ds {
@@ -1866,6 +1868,33 @@ __global__ void k_ctrl_init(Ctrl* c, int W) {
     z.retire_events = 0; z.compacted = 0; z.A_prev = W; z.pad2 = 0;
     *c = z;
   }
+}
+
+// ------------------------------------------ allocation-free workspace (scratch)
+// A fixed device array that serves as the workspace of ds_solve_noalloc, for
+// callers that cannot allocate. Every GPU the library runs on holds its own
+// copy for the life of the process. Host code never uses the array's name as
+// an address: scratch_area() takes its device address with that device
+// current, once per device, and hands that out.
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+hipError_t scratch_area(void** ptr, size_t* bytes) {
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  *bytes = kScratchBytes;
+  return hipSuccess;
 }
 
 // ------------------------------------------------------- host-side launchers

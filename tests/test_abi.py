@@ -25,7 +25,7 @@ def test_library_exports_every_declared_function():
     lib = ds.load_library()
     names = _declared_functions()
     assert set(names) == {"ds_api_version", "ds_workspace_bytes", "ds_solve", "ds_error_string",
-                          "ds_last_error_message"}
+                          "ds_last_error_message", "ds_solve_noalloc"}
     for nm in names:
         assert hasattr(lib, nm), nm
     assert lib.ds_api_version() == 3
@@ -184,3 +184,20 @@ def test_caller_outputs_are_validated():
     for o in bad:
         with pytest.raises(ValueError):
             ds._check_out(o, W, n_max, m_max, dev)
+
+
+def test_noalloc_entry_rejects_options_before_device_work():
+    """ds_solve_noalloc runs one sub-batch and does not time launches: other
+    options are refused on the host (no GPU needed to get here)."""
+    lib = ds.load_library()
+    fake = ctypes.c_void_p(0x1000)
+    pr = _problem(X=fake, Y=fake, a=fake, b=fake, eps=fake)
+    res = ds._Result(f=fake, g=fake, depth=fake, residual=fake, status=fake)
+    for streams, flags in ((2, 0), (4, 0), (0, ds.F_TIMING)):
+        op = ds._options(1e-3, None, 100, 1, "active", flags, streams)
+        assert lib.ds_solve_noalloc(ctypes.byref(pr), ctypes.byref(op), ctypes.byref(res), None,
+                                    None) == 1
+        assert "ds_solve_noalloc" in lib.ds_last_error_message().decode()
+    bad = ds._options(0.0, None, 100, 1, "active", 0)
+    assert lib.ds_solve_noalloc(ctypes.byref(pr), ctypes.byref(bad), ctypes.byref(res), None,
+                                None) == 1

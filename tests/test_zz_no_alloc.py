@@ -1,0 +1,75 @@
+"""The allocation-free entry point (ds_solve_noalloc, its workspace a fixed
+per-GPU device array) against ds_solve with a caller workspace: two calls in a
+row, the second on a smaller window, each bit for bit equal to ds_solve at one
+sub-batch (the same kernels and launch sequence), and a window too large for
+the array refused with a clear error."""
+
+import numpy as np
+import pytest
+
+from paper_2607_24741_amd import workloads as wl
+from tests.gpu_support import log, to_device
+
+pytestmark = pytest.mark.gpu
+
+KEYS = ("f", "g", "depth", "residual", "status", "order")
+
+
+def _outputs(W, n_max, m_max):
+    import torch
+    dev = "cuda:0"
+    f32 = dict(dtype=torch.float32, device=dev)
+    i32 = dict(dtype=torch.int32, device=dev)
+    # filled with junk so a missed write shows
+    return dict(f=torch.full((W, n_max), 7.0, **f32), g=torch.full((W, m_max), 7.0, **f32),
+                depth=torch.full((W,), -5, **i32), residual=torch.full((W,), 7.0, **f32),
+                row_residual=torch.full((W,), 7.0, **f32), col_residual=torch.full((W,), 7.0, **f32),
+                status=torch.full((W,), 9, **i32), order=torch.full((W,), -5, **i32))
+
+
+def _pair(w, tol, **kw):
+    import torch
+    import paper_2607_24741_amd as ds
+    dv = to_device(w)
+    args = (dv["X"], dv["Y"], dv["a"], dv["b"], dv["eps"], tol)
+    ref = ds.solve(*args, n=dv["n"], m=dv["m"], streams=1, return_stats=True, **kw)
+    out = _outputs(w.W, w.X.shape[1], w.Y.shape[1])
+    got = ds.solve_noalloc(*args, out=out, n=dv["n"], m=dv["m"], return_stats=True, **kw)
+    torch.cuda.synchronize()
+    return ref, got
+
+
+def test_noalloc_matches_solve_on_two_calls():
+    import paper_2607_24741_amd as ds
+    first = wl.make("c2", W=12, n=300, m=260, hetero=(40, 300), pad_value=np.nan)
+    second = wl.make("c1", W=5)
+    for name, w, tol, kw in (("ragged mixture lanes, W=12", first, 1e-2, {}),
+                             ("toy lanes, W=5 (smaller)", second, 1e-3, dict(mode="active"))):
+        log(f"[case] noalloc {name}: n_max={w.X.shape[1]} m_max={w.Y.shape[1]} d={w.d}")
+        ref, got = _pair(w, tol, **kw)
+        for i, k in enumerate(KEYS):
+            assert got[i].equal(ref[i]), k
+        sr, sg = ref[-1], got[-1]
+        assert sg.sub_batches == 1 and sr.sub_batches == 1
+        for k in ("slots_update", "pair_evals", "halfsteps_executed", "l_max", "compactions"):
+            assert getattr(sg, k) == getattr(sr, k), k
+        assert sg.row_residual.equal(sr.row_residual) and sg.col_residual.equal(sr.col_residual)
+        assert int((got[4] == 0).sum()) == w.W   # every lane converged
+        log(f"[case] noalloc {name}: depths {got[2].cpu().tolist()}")
+
+
+def test_noalloc_refuses_a_window_beyond_its_array():
+    import torch
+    import paper_2607_24741_amd as ds
+    w = wl.make("c3", W=200, n=512, m=512)   # about 66 MiB of workspace at one sub-batch
+    need = ds.workspace_bytes(w.W, 512, 512, w.d, streams=1)
+    assert need > 64 << 20
+    log(f"[case] noalloc too large: needs {need} bytes")
+    dv = to_device(w)
+    out = _outputs(w.W, 512, 512)
+    with pytest.raises(ds.DSError) as ei:
+        ds.solve_noalloc(dv["X"], dv["Y"], dv["a"], dv["b"], dv["eps"], 1e-3, out=out)
+    assert ei.value.code == 4 and str(need) in str(ei.value)
+    # nothing was launched: the outputs still hold what the caller put there
+    assert bool((out["depth"] == -5).all())
+    torch.cuda.synchronize()
