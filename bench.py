@@ -121,34 +121,54 @@ def study(args):
         return 1e3 * (time.perf_counter() - t0), r[2].cpu().numpy()
 
     W = w.W
-    widths = [k for k in (1, 2, 4, 8, 16, 32, 64, 128, 256) if k <= W]
+    widths = [k for k in (1, 2, 4, 8, 16, 32, 64, 128, 256, 512, 1024) if k <= W]
     # (a) width-cost curve: K fixed cycles (unreachable tolerance) at width A
     K = 64
     curve = []
     for A in widths:
         ms, _ = run(list(range(A)), "static", 1e-30, K)
         curve.append({"A": A, "ms_per_cycle": ms / K, "us_per_lane_cycle": 1e3 * ms / K / A})
-    # (b) width sweep: windows of W lanes, static time over active time
+        print(f"[study] {args.config} width-cost A={A}: {ms / K:.3f} ms per cycle", file=sys.stderr,
+              flush=True)
+    # (b) width sweep: windows of W lanes cut from the window (at most 8 per
+    # width, evenly spaced), static time over active time
     sweep = []
     for Wd in widths:
+        starts = list(range(0, W - Wd + 1, Wd))
+        if len(starts) > 8:
+            starts = [starts[int(q)] for q in np.linspace(0, len(starts) - 1, 8).round()]
         ratios = []
-        for s0 in range(0, W - Wd + 1, Wd):
+        for s0 in starts:
             idx = list(range(s0, s0 + Wd))
             ta, _ = run(idx, "active", args.tol, w.max_iter)
             ts, _ = run(idx, "static", args.tol, w.max_iter)
             ratios.append(ts / ta)
         r = np.array(ratios)
+        print(f"[study] {args.config} width {Wd}: static/active median {np.median(r):.3f} over "
+              f"{len(r)} windows", file=sys.stderr, flush=True)
         sweep.append({"W": Wd, "windows": len(r), "static_over_active_median": float(np.median(r)),
                       "min": float(r.min()), "max": float(r.max()), "wins": int((r > 1).sum())})
-    # (c) grouping intervention: one lane multiset in windows of G lanes
+    # eq:active-gate: the smallest width from which active execution wins --
+    # static over active above 1.02 (the spread of repeated equal-work solves
+    # at W = 1) in the median over the windows -- at every larger width measured
+    above = [q["W"] for q in sweep if q["static_over_active_median"] > 1.02]
+    gate = None
+    for q in reversed(sweep):
+        if q["static_over_active_median"] > 1.02:
+            gate = q["W"]
+        else:
+            break
+    # (c) grouping intervention: one lane multiset (the first 128 lanes at
+    # most) in windows of G lanes
     G = min(16, W)
-    _, depth = run(list(range(W)), "active", args.tol, w.max_iter)
+    Wg = min(W, 128)
+    _, depth = run(list(range(Wg)), "active", args.tol, w.max_iter)
     order = np.argsort(depth, kind="stable")
-    nwin = W // G
+    nwin = Wg // G
     groupings = {"homogeneous": [order[q * G:(q + 1) * G] for q in range(nwin)],
                  "heterogeneous": [order[q::nwin][:G] for q in range(nwin)]}
     for rs in (1, 2, 3):
-        perm = np.random.default_rng(rs).permutation(W)
+        perm = np.random.default_rng(rs).permutation(Wg)
         groupings[f"random {rs}"] = [perm[q * G:(q + 1) * G] for q in range(nwin)]
     grouping = []
     for name, wins in groupings.items():
@@ -163,13 +183,16 @@ def study(args):
             ts, _ = run([int(i) for i in idx], "static", args.tol, w.max_iter)
             ta_sum += ta
             ts_sum += ts
+        print(f"[study] {args.config} grouping {name}: static/active {ts_sum / ta_sum:.3f}",
+              file=sys.stderr, flush=True)
         grouping.append({"grouping": name, "H_D": float(np.mean(hd)), "padding": float(np.mean(pad)),
                          "active_slots": float(act / stat), "static_over_active": ts_sum / ta_sum})
     rec = {"study": "execution surface", "config": {"workload": wl.DESCRIPTIONS[args.config],
                                                     "name": args.config, "tol": args.tol,
                                                     "sub_batches": 1, "window_for_grouping": G},
            "width_cost_curve": {"fixed_cycles": K, "points": curve},
-           "width_sweep": sweep, "grouping": grouping}
+           "width_sweep": sweep, "active_wins_from_W": gate, "widths_active_wins": above,
+           "grouping_lanes": Wg, "grouping": grouping}
     print(json.dumps(rec), flush=True)
 
 

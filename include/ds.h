@@ -78,8 +78,11 @@ typedef enum {
 } ds_lane_status;
 
 enum {
-  DS_F_SHADOW = 1u,     /* also run the full check on screen-negative lanes and
-                           count already-releasable lanes the screen missed      */
+  DS_F_SHADOW = 1u,     /* shadow replay: also run the full check on screen-
+                           negative lanes and count already-releasable lanes the
+                           screen missed, and recompute the row marginal of every
+                           audited state by a dedicated pass, reporting its largest
+                           distance from the fused screen (ds_stats)            */
   DS_F_TIMING = 2u,     /* time the update launches of every 32nd cycle with HIP
                            events in their dispatches (ds_stats)                 */
   DS_F_FORCE_VALU = 4u, /* float32 state on the vector-ALU update kernels (d <= 16) */
@@ -195,6 +198,11 @@ typedef struct {
   int32_t width_trace_len;    /* capacity in; entries written out                  */
   size_t workspace_bytes;     /* bytes of workspace the call used                   */
   int32_t sub_batches;        /* concurrent sub-batches the call ran (see streams)  */
+  double screen_discrepancy;  /* DS_F_SHADOW: max over lanes and audits of
+                                 |row screen - row residual recomputed by a full
+                                 pass over (i, j) at the audited state|, over the
+                                 audits where either is at most 2 tol (where a
+                                 release can be decided)                          */
 } ds_stats;
 
 /* Version of this header the library was built from (DS_API_VERSION). */

@@ -78,7 +78,8 @@ class _Stats(ctypes.Structure):
                 ("ms_check", ctypes.c_double), ("ms_compact", ctypes.c_double),
                 ("width_trace", ctypes.POINTER(ctypes.c_int32)),
                 ("width_trace_len", ctypes.c_int32),
-                ("workspace_bytes", ctypes.c_size_t), ("sub_batches", ctypes.c_int32)]
+                ("workspace_bytes", ctypes.c_size_t), ("sub_batches", ctypes.c_int32),
+                ("screen_discrepancy", ctypes.c_double)]
 
 
 _lib = None
@@ -166,6 +167,7 @@ class Stats:
     width_trace: list
     workspace_bytes: int
     sub_batches: int
+    screen_discrepancy: float
     row_residual: object = None   # [W] tensor
     col_residual: object = None   # [W] tensor
 
@@ -320,6 +322,6 @@ def _returns(out, st, trace_buf, return_stats):
                   st.l_max, st.cycles, st.audits, st.screen_positive, st.check_failures,
                   st.compactions, st.missed_ready, st.update_launches, st.ms_total, st.ms_update,
                   st.timed_pair_evals, st.ms_check, st.ms_compact, wt, st.workspace_bytes,
-                  st.sub_batches,
+                  st.sub_batches, st.screen_discrepancy,
                   out.get("row_residual"), out.get("col_residual"))
     return ret + (stats,)

@@ -113,6 +113,7 @@ ds::Layout plan(const ds_problem* pr, const ds_options* op, void* ws) {
   L.center = c.take<float>(W * (size_t)L.d);
   L.vcnt = c.take<int>(W);
   L.nchk = c.take<int>(W);
+  L.disc = (op->flags & DS_F_SHADOW) ? c.take<float>(W) : nullptr;
   L.audit = c.take<ds::Audit>(W);
   L.off[0] = c.take<int>(W + 1);
   L.off[1] = c.take<int>(W + 1);
@@ -273,6 +274,7 @@ struct PartOut {
   std::vector<Timed> timed;
   double ms_update = 0.0, ms_compact = 0.0;
   std::vector<int32_t> nchk;
+  std::vector<float> disc;   // shadow mode: screen discrepancy per lane
   std::vector<ds::SlotInfo> lanes;
   size_t ws_bytes = 0;
 };
@@ -307,7 +309,7 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
   ia.pad[0] = L.pad[0]; ia.pad[1] = L.pad[1];
   ia.bank = L.bank[0];
   ia.center = L.center;
-  ia.vcnt = L.vcnt; ia.nchk = L.nchk; ia.rbmax = L.rbmax;
+  ia.vcnt = L.vcnt; ia.nchk = L.nchk; ia.disc = L.disc; ia.rbmax = L.rbmax;
   ia.precise = precise ? 1 : 0;
   ia.mat = mat ? 1 : 0;
   ia.ctrl = L.ctrl;
@@ -396,7 +398,7 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
     l.tol = op->tol;
     l.slot = L.bank[bank].slot; l.dec = L.bank[bank].dec;
     l.audit = L.audit; l.vcnt = L.vcnt; l.ctrl = L.ctrl;
-    l.hsnap = R->snap_dev; l.nchk = L.nchk;
+    l.hsnap = R->snap_dev; l.nchk = L.nchk; l.disc = L.disc;
     l.progress = &R->snap_dev->progress;
     l.Q = L.Q; l.q_lane = (size_t)L.pad[0] * L.pad[1]; l.q_ld = L.pad[1];
     return l;
@@ -540,6 +542,17 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
       lc.nb0 = std::max(items[0], 0);
       HIP_TRY(launch_check64(lc, ga, lc.nb0 + std::max(items[1], 0), st));
     }
+    if (audit_prev && shadow && !guard) {
+      // shadow mode: the row marginal of state k-1 recomputed by a dedicated
+      // pass, so the decision can record how far the fused screen is from it
+      Launch lr = make_launch();
+      lr.p[0] = make_pass(0, 1, pk1, pk1, pk1);
+      lr.p[0].depth = k - 1;
+      lr.p[0].verify_all = 1;
+      lr.nb0 = blocks_of(items[0]);
+      r = run(lr, pick(items[0], 0), lr.nb0, false, k, 1);
+      if (r != DS_OK) return r;
+    }
     // g-half of cycle k (+ column check and decision for state k-1)
     // (the check blocks come last: most of them exit at once, and at the front
     // they would delay the update blocks' dispatch)
@@ -621,6 +634,10 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
   }
   out.nchk.resize(W);
   HIP_TRY(hipMemcpyAsync(out.nchk.data(), L.nchk, sizeof(int32_t) * W, hipMemcpyDeviceToHost, st));
+  if (L.disc) {
+    out.disc.resize(W);
+    HIP_TRY(hipMemcpyAsync(out.disc.data(), L.disc, sizeof(float) * W, hipMemcpyDeviceToHost, st));
+  }
   HIP_TRY(hipStreamSynchronize(st));
   out.ctrl = ctrl;
   out.launched = launched;
@@ -827,6 +844,7 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
         chk += (int64_t)o.nchk[u] * nm[t];
       }
       retire_events += o.ctrl.retire_events;
+      for (float v : o.disc) S.screen_discrepancy = std::max(S.screen_discrepancy, (double)v);
       launched = std::max(launched, o.launched);
       finished_all &= o.ctrl.finished ? 1 : 0;
       S.screen_positive += o.ctrl.screen_pos;

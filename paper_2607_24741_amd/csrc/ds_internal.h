@@ -141,6 +141,7 @@ struct Layout {
   float* center;     // [W][d] (ingest only)
   int* vcnt;         // [W] column-check arrival counters
   int* nchk;         // [W] marginal evaluation passes spent on checks, per caller lane
+  float* disc;       // [W] shadow mode: max |row screen - recomputed row residual|, per caller lane
   Audit* audit;      // [W]
   int* off[2];       // work item offsets per role [W + 1]
   Ctrl* ctrl;
@@ -197,6 +198,7 @@ struct Launch {
   Ctrl* ctrl;
   HostSnap* hsnap;                // may be null
   int* nchk;                      // [W] check passes per caller lane
+  float* disc;                    // [W] shadow mode: screen discrepancy per caller lane (else null)
   const float* Q;                 // materialised cost (caller lane l at Q + l * q_lane)
   size_t q_lane;                  // floats per lane
   int q_ld;                       // row stride of Q (padded target count)
@@ -255,6 +257,7 @@ struct IngestArgs {
   float* center;
   int* vcnt;
   int* nchk;
+  float* disc;
   int rbmax;
   Ctrl* ctrl;
 };

@@ -347,6 +347,15 @@ __device__ void finish_rows_r(const Launch& L, const Pass& P, int s, const SlotI
   if (P.final_audit) {
     const LaneAgg gr = lane_aggregate(P.agg_rowchk, s, L.rbmax, row_blocks(si.n, UNIT), false);
     rrow = gr.sum;
+  } else if (L.disc) {
+    // shadow mode: the row marginal of the audited state was also recomputed
+    // by a dedicated check pass; record how far the screen is from it where a
+    // release can be decided (either value within twice the tolerance)
+    const LaneAgg gr = lane_aggregate(P.agg_rowchk, s, L.rbmax, row_blocks(si.n, UNIT), false);
+    const float dsc = fabsf(rhat - gr.sum);
+    if (lane == 0 && dsc == dsc && fminf(rhat, gr.sum) <= 2.f * L.tol)
+      // non-negative floats order as their bit patterns
+      atomicMax(reinterpret_cast<int*>(&L.disc[si.lane]), __float_as_int(dsc));
   }
   if (lane != 0) return;
   // marginal evaluations spent on this lane's check (the final audit
@@ -1745,6 +1754,7 @@ __global__ __launch_bounds__(256) void k_ingest_lanes(IngestArgs p) {
     p.bank.dec[t] = d;
     p.vcnt[t] = 0;
     p.nchk[t] = 0;
+    if (p.disc) p.disc[t] = 0.f;
   }
   // no previous half-step: the first update of each side runs unanchored
   const float4 none = make_float4(0.f, INFINITY, -INFINITY, 1.f);

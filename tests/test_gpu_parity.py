@@ -539,13 +539,27 @@ def test_padding_isolation():
     assert np.all(np.isfinite(gn["f"]))
 
 
-def test_shadow_replay_counts_no_missed_ready():
-    w = wl.make("c1")
-    log("[case] shadow replay")
-    g = run_gpu(w, 1e-3, flags=F_SHADOW)
-    assert g["stats"].missed_ready == 0
-    base = run_gpu(w, 1e-3)
-    assert np.array_equal(g["f"], base["f"]) and np.array_equal(g["depth"], base["depth"])
+@pytest.mark.parametrize("flags", [0, F_FAST32], ids=["default", "fast32"])
+@pytest.mark.parametrize("cfg", ["c1", "c2"])
+def test_shadow_replay_screen_against_full_row_check(cfg, flags):
+    """Shadow replay (Sec. 5.3): every lane is fully checked at every audit, so
+    no releasable lane may be missed by the screen, and the row marginal of
+    every audited state is recomputed by a dedicated pass over (i, j): the
+    fused screen (read off the next f-update, eq:updated-marginal) must agree
+    with it far below the 1e-6 band on the default path. The outputs equal
+    the plain run's bit for bit (the shadow work only measures)."""
+    w, tol = (wl.make("c1"), 1e-3) if cfg == "c1" else (wl.make("c2", W=6, n=200, m=176), 1e-2)
+    log(f"[case] shadow replay {cfg} flags={flags}")
+    g = run_gpu(w, tol, flags=F_SHADOW | flags)
+    st = g["stats"]
+    log(f"[case] shadow replay {cfg} flags={flags}: missed_ready {st.missed_ready}, screen "
+        f"discrepancy {st.screen_discrepancy:.3e}, depths {g['depth'].tolist()}")
+    assert st.missed_ready == 0
+    if flags == 0:
+        assert st.screen_discrepancy <= 1e-7
+    base = run_gpu(w, tol, flags=flags)
+    for k in ("f", "g", "depth", "residual", "status"):
+        assert np.array_equal(g[k], base[k]), k
 
 
 def _tiny_lanes():
