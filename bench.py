@@ -233,9 +233,16 @@ def roofline(w, args, stats, T, traffic_summary):
     ms_upd = sum(s.ms_update for s in stats)
     launches = sum(s.update_launches for s in stats)
     kept_pairs = sum(s.pair_evals for s in stats)
-    mat = args.materialize or w.d > 32
+    mfree = w.d > 32 and args.matrix_free
+    mat = args.materialize or (w.d > 32 and not mfree)
     rec = {}
-    if mat:
+    if mfree:
+        # the contraction on the matrix cores: 2 d flops per term, fp32 peak
+        per_pair, unit, peak, bound = 2.0 * w.d, "TFLOP/s", 157.3, "mfma"
+        algo = "2 d flops of the x~.y~ contraction per valid (i,j) term"
+        kname = "k_update_mfma_k (f- and g-half-steps)"
+        scale = 1e12
+    elif mat:
         per_pair, unit, peak, bound = 4.0, "GB/s", HBM_PEAK_GBS, "hbm"
         algo = "4 bytes of materialised cost per valid (i,j) term"
         kname = "k_mat_rows / k_mat_cols (f- and g-half-steps)"
@@ -260,6 +267,50 @@ def roofline(w, args, stats, T, traffic_summary):
            "device_frac_lb": per_pair * kept_pairs / T / scale / peak}
     out.update(rec)
     return out
+
+
+def algorithmic_bytes(w, last, f64, st):
+    """HBM bytes an update launch must move, on average over the step's
+    launches (float64 state only): a lane's half-step with r rows and c columns
+    reads the rows' records, lse and log masses and the columns' records and
+    potentials, and writes the rows' new lse and potentials --
+    r (8 dp + 32) + c (8 dp + 8) bytes, dp = d rounded up to even -- so a cycle
+    moves (n + m)(16 dp + 40) bytes per running lane."""
+    import numpy as np
+    if not f64:
+        return {}
+    depth = last[2].cpu().numpy().astype(np.int64)
+    dp = w.d + (w.d & 1)
+    per_cycle = (w.n.astype(np.int64) + w.m) * (16 * dp + 40)
+    launches = 2 * st.l_max
+    return {"hbm_bytes_per_launch_algorithmic": float((depth * per_cycle).sum()) / max(1, launches)}
+
+
+def h_terms(w, stats, last, T, steps):
+    """Where the step's time goes besides the kept half-steps (eq:time-accounting):
+    the verifier's (i, j) work (the column check of screen-positive lanes runs in
+    the g-half launches; the final audit's passes), the fused screen's overhead
+    (a retired lane's discarded f-half and the g-half that shared its check's
+    launch), both as shares of the arithmetic work, and the compaction launches
+    (scan + gather, timed with events) as a share of the wall time. The rest of
+    the wall time beyond the kernels -- launch gaps and host control -- is read
+    from the kernel-trace profile (summed kernel time against the solve time)."""
+    import numpy as np
+    depth = last[2].cpu().numpy().astype(np.int64)
+    status = last[4].cpu().numpy()
+    area = w.n.astype(np.int64) * w.m
+    st = stats[-1]
+    kept = st.pair_evals
+    check = st.check_pair_evals
+    retired = (status == 0) & (depth < w.max_iter)
+    extra = int(2 * area[retired].sum())     # the two extra half-steps of each retired lane
+    total = kept + check + extra
+    ms_compact = sum(s.ms_compact for s in stats) / steps
+    return {"kept_update_pairs": kept, "check_pairs": check, "screen_extra_pairs": extra,
+            "check_work_share": check / total, "screen_work_share": extra / total,
+            "extra_halfsteps": st.halfsteps_executed - 2 * st.slots_update,
+            "compaction_ms": ms_compact, "compaction_share": ms_compact / (1e3 * T / steps),
+            "compactions": st.compactions}
 
 
 def mixture_extras(args, flags):
@@ -321,6 +372,8 @@ def main():
     ap.add_argument("--force-valu", action="store_true",
                     help="float32 state on the vector-ALU kernels (DS_F_FORCE_VALU)")
     ap.add_argument("--materialize", action="store_true", help="materialised cost (DS_F_MATERIALIZE)")
+    ap.add_argument("--matrix-free", action="store_true",
+                    help="d > 32: K-looped matrix-core half-step (DS_F_MATRIX_FREE)")
     ap.add_argument("--guard", action="store_true", help="guarded release (DS_F_GUARD)")
     ap.add_argument("--no-tol-sweep", action="store_true",
                     help="skip the mixture window's modes and tolerance sweep")
@@ -344,7 +397,8 @@ def main():
     t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(dev)
     X, Y, a, b, eps, n, m = (t(w.X), t(w.Y), t(w.a), t(w.b), t(w.eps), t(w.n), t(w.m))
     base_flags = ((ds.F_FAST32 if args.fast32 else 0) | (ds.F_FORCE_VALU if args.force_valu else 0)
-                  | (ds.F_MATERIALIZE if args.materialize else 0) | (ds.F_GUARD if args.guard else 0))
+                  | (ds.F_MATERIALIZE if args.materialize else 0) | (ds.F_GUARD if args.guard else 0)
+                  | (ds.F_MATRIX_FREE if args.matrix_free else 0))
     need = ds.workspace_bytes(w.W, w.X.shape[1], w.Y.shape[1], w.d, tol=args.tol,
                               max_iter=w.max_iter, mode=args.mode, flags=base_flags,
                               streams=args.streams)
@@ -395,7 +449,9 @@ def main():
         "lanes_max_iter": int((status == 1).sum()),
         "compactions": stats[-1].compactions,
         "timed_update_launches_per_step": sum(s.update_launches for s in stats) // args.steps,
-        "roofline": roofline(w, args, stats, T, traffic_summary),
+        "roofline": dict(roofline(w, args, stats, T, traffic_summary),
+                         **algorithmic_bytes(w, last, f64, stats[-1])),
+        "h_terms": h_terms(w, stats, last, T, args.steps),
     }
     if not args.no_tol_sweep:
         rec["mixture_modes"], rec["mixture_tol_sweep"] = mixture_extras(args, base_flags)

@@ -95,7 +95,8 @@ enum {
                            outputs stay float32.                                */
   DS_F_MATERIALIZE = 32u, /* build the cost C (base-2 units, float32) once per call
                            in the workspace and stream it from HBM in every
-                           half-step; always on for d > 32 (n_max, m_max <= 8192) */
+                           half-step; the default for d > 32 when n_max, m_max
+                           <= 8192 (required here)                                */
   DS_F_GUARD = 64u,     /* guarded release (eq:release-contract in float64): a lane
                            whose float32 row screen is within the guard margin
                            (r^ <= (1 + 1/64) tau_screen, or non-finite) is verified by a
@@ -104,6 +105,11 @@ enum {
                            in float64 from the caller's coordinates); that residual
                            decides the release and is the one reported. One extra
                            launch per audit cycle; n_max, m_max <= 8192.         */
+  DS_F_MATRIX_FREE = 256u, /* d > 32: recompute the cost per tile on the matrix
+                           cores (a K-looped contraction over d) instead of
+                           materialising it; the default when a side has more
+                           than 8192 points. Float32 state. Exclusive with
+                           DS_F_MATERIALIZE.                                     */
   DS_F_FAST32 = 128u    /* float32 state on the matrix-core kernels for d <= 16:
                            about 1.5-2.5x faster, but float32 rounding of the
                            scaled coordinates and potentials (exponents of size

@@ -23,7 +23,7 @@ from dataclasses import dataclass
 __all__ = ["solve", "solve_noalloc", "workspace_bytes", "load_library", "library_path", "DSError",
            "MODES", "LANE_CONVERGED", "LANE_MAX_ITER", "LANE_NONFINITE",
            "F_SHADOW", "F_TIMING", "F_FORCE_VALU", "F_FORCE_MFMA", "F_PRECISE",
-           "F_MATERIALIZE", "F_GUARD", "F_FAST32"]
+           "F_MATERIALIZE", "F_GUARD", "F_FAST32", "F_MATRIX_FREE"]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 _LIBPATH = os.path.join(_PKG, "_lib", "libdrainsinkhorn.so")
@@ -33,6 +33,7 @@ MODES = {"active": 0, "static": 1, "logical": 2}
 LANE_CONVERGED, LANE_MAX_ITER, LANE_NONFINITE = 0, 1, 2
 F_SHADOW, F_TIMING, F_FORCE_VALU, F_FORCE_MFMA, F_PRECISE, F_MATERIALIZE, F_GUARD = 1, 2, 4, 8, 16, 32, 64
 F_FAST32 = 128   # float32 state on the matrix cores (d <= 16); default: float64 state
+F_MATRIX_FREE = 256   # d > 32: K-looped matrix-core half-step instead of the materialised cost
 
 _ERRS = {0: "DS_OK", 1: "DS_E_INVALID", 2: "DS_E_WORKSPACE", 3: "DS_E_HIP",
          4: "DS_E_UNSUPPORTED", 5: "DS_E_INTERNAL"}

@@ -48,8 +48,15 @@ size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 constexpr int kMaxParts = 4;   // concurrent sub-batches of one call
 
 bool uses_mfma(const ds_problem* pr, const ds_options* op);
+// d > 32: the materialised cost (4 bytes per term from HBM) unless a side has
+// more than 8192 points or DS_F_MATRIX_FREE asks for the K-looped matrix-core
+// half-step, which recomputes x~ . y~ per tile.
+bool uses_mfree(const ds_problem* pr, const ds_options* op) {
+  if (pr->d <= ds::kMaxDSmall || (op->flags & DS_F_MATERIALIZE)) return false;
+  return (op->flags & DS_F_MATRIX_FREE) || pr->n_max > ds::kMatMaxPts || pr->m_max > ds::kMatMaxPts;
+}
 bool uses_mat(const ds_problem* pr, const ds_options* op) {
-  return pr->d > ds::kMaxDSmall || (op->flags & DS_F_MATERIALIZE) != 0;
+  return (op->flags & DS_F_MATERIALIZE) != 0 || (pr->d > ds::kMaxDSmall && !uses_mfree(pr, op));
 }
 // The float64 state is the default wherever its kernels exist (matrix-free,
 // d <= 16): rounding the scaled coordinates or the potentials to float32
@@ -84,12 +91,14 @@ ds::Layout plan(const ds_problem* pr, const ds_options* op, void* ws) {
   L.d = pr->d;
   L.dp = pr->d + (pr->d & 1);
   L.dh = L.dp / 2;
-  L.pad[0] = (int)align_up((size_t)pr->n_max, ds::kPad);
-  L.pad[1] = (int)align_up((size_t)pr->m_max, ds::kPad);
   L.mat = uses_mat(pr, op) ? 1 : 0;
   L.rows = L.mat ? ds::kRowsValu
                  : uses_f64(pr, op) ? ds::rows_f64(pr->d)
                  : uses_mfma(pr, op) ? ds::kRowsMfma : ds::kRowsValu;
+  // every lane-side holds whole work items
+  const size_t padq = (size_t)std::max(ds::kPad, L.rows);
+  L.pad[0] = (int)align_up((size_t)pr->n_max, padq);
+  L.pad[1] = (int)align_up((size_t)pr->m_max, padq);
   L.es = uses_f64(pr, op) ? 2 : 1;
   if (L.mat) L.dp = 0;   // no point records: the cost is materialised
   L.rbmax = std::max(L.pad[0], L.pad[1]) / L.rows;
@@ -158,6 +167,10 @@ ds_err check_problem(const ds_problem* pr, const ds_options* op) {
   if (op->streams < 0 || op->streams > kMaxParts) return fail(DS_E_INVALID, "streams must be in 0..4");
   if (op->streams > 1 && op->mode != DS_MODE_ACTIVE)
     return fail(DS_E_INVALID, "sub-batches (streams > 1) need the active mode");
+  if ((op->flags & DS_F_MATRIX_FREE) && (op->flags & DS_F_MATERIALIZE))
+    return fail(DS_E_INVALID, "DS_F_MATRIX_FREE and DS_F_MATERIALIZE are exclusive");
+  if (uses_mfree(pr, op) && (op->flags & DS_F_FORCE_VALU))
+    return fail(DS_E_UNSUPPORTED, "the matrix-free large-d half-step runs on the matrix cores");
   if ((op->flags & DS_F_FORCE_VALU) && (op->flags & DS_F_FORCE_MFMA))
     return fail(DS_E_INVALID, "DS_F_FORCE_VALU and DS_F_FORCE_MFMA are exclusive");
   if ((op->flags & DS_F_FORCE_VALU) && pr->d > 16)
@@ -424,9 +437,8 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
   }
   auto pick = [&](int items, int role) -> int {
     if (mat) return VAR_MEDIUM;   // one layout: 64-row items, one block each
-    // (the float64 kernel's items are 128 rows up to d = 12: half as many items per width)
-    const int medium = use_mfma ? kMediumItemsMfma
-                       : (precise && L.rows == 128) ? kMediumItemsF64 : kMediumItemsValu;
+    // (the float64 kernel's items hold 64 to 256 rows: fewer items per width)
+    const int medium = use_mfma ? kMediumItemsMfma : kMediumItemsValu * kRowsValu / L.rows;
     if (items < medium) return VAR_NARROW;
     return (use_mfma && tpg[role] <= 2) ? VAR_MEDIUM4 : VAR_MEDIUM;
   };
@@ -441,6 +453,7 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
     hipEvent_t h0 = e0 >= 0 ? (*tm.pool)[e0] : nullptr, h1 = e1 >= 0 ? (*tm.pool)[e1] : nullptr;
     if (mat) HIP_TRY(launch_update_mat(l, blocks, st, h0, h1));
     else if (precise) HIP_TRY(launch_update_f64(l, d, variant, blocks, st, h0, h1));
+    else if (d > kMaxDSmall) HIP_TRY(launch_update_mfma_k(l, variant, blocks, st, h0, h1));
     else HIP_TRY(launch_update(l, d, use_mfma, variant, blocks, st, h0, h1));
     if (timed) {
       tm.spans[0].push_back({e0, e1});

@@ -49,7 +49,6 @@ constexpr int kMaxDevices = 64;
 // launch-variant thresholds (work items of the launch, see launch_update)
 constexpr int kMediumItemsMfma = 384;
 constexpr int kMediumItemsValu = 256;
-constexpr int kMediumItemsF64 = 128;
 
 // Per physical slot lane descriptor; moved by compaction with the rest of the
 // lane-indexed state.
@@ -151,7 +150,10 @@ struct Layout {
   size_t bytes;
 };
 
-// rows per work item of the float64-state kernel: two per lane up to d = 12
+// rows per work item of the float64-state kernel: two per lane up to d = 12,
+// then one (the rows' coordinates must fit in registers); four per lane at
+// d = 3 measured slower (2087 against 1980 ms per LiDAR-shaped solve: lower
+// occupancy, fewer work items in narrow launches)
 __host__ __device__ constexpr int rows_f64(int d) { return d <= 12 ? 128 : 64; }
 
 // work items of one lane-side: one per block of `rows` rows (all columns)
@@ -273,6 +275,9 @@ hipError_t launch_update(const Launch& a, int d, bool use_mfma, int variant, int
                          hipStream_t st, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 hipError_t launch_update_f64(const Launch& a, int d, int variant, int blocks, hipStream_t st,
                              hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
+// matrix-free matrix-core half-step for any d (K-looped contraction)
+hipError_t launch_update_mfma_k(const Launch& a, int variant, int blocks, hipStream_t st,
+                                hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 hipError_t launch_update_mat(const Launch& a, int blocks, hipStream_t st, hipEvent_t e0 = nullptr,
                              hipEvent_t e1 = nullptr);
 

@@ -726,6 +726,145 @@ void k_update_mfma(Launch L) {
                              rhat);
 }
 
+// --------------------------------------------------- matrix-free, large d
+// The same half-step as k_update_mfma for any d: the contraction x~ . y~ is
+// K-looped over the coordinates on v_mfma_f32_32x32x2_f32, both operands read
+// per tile from memory (a row item's coordinates stay in the L1/L2 caches
+// across its column tiles; a lane's columns in L2), KU coordinate pairs per
+// batch of loads; then the augmented pair (gam_j, 1) . (1, -anchor_i) and the
+// same streaming base-2 sum, fixed column groups and merge as k_update_mfma.
+// It is the path for d > 32 when the cost cannot be materialised (more than
+// 8192 points on a side) or on request (DS_F_MATRIX_FREE).
+template <int GW, bool UNI>
+__global__ __launch_bounds__(64 * (kGroups / GW), 2)
+void k_update_mfma_k(Launch L) {
+  note_progress(L);
+  constexpr int KU = 8;                       // coordinate pairs per batch of loads
+  __shared__ float2 sh_part[kGroups][2][32];
+  const int b = blockIdx.x;
+  const int pi = b >= L.nb0;
+  const Pass P = L.p[pi];
+  int s, rb0, nrows, ncols, c_fin, c_A;
+  SlotInfo si;
+  if (!place_item<1, UNI ? 1 : 0>(L, P, pass_blocks(L, pi), pi ? b - L.nb0 : b, s, rb0, nrows,
+                                  ncols, si, c_fin, c_A))
+    return;
+  const bool upd = P.kind == KIND_UPDATE;
+  float rhat = NAN;
+  if (!upd) {
+    const bool chk = check_facts(L, P, s, P.role ? ncols : nrows, rhat);
+    if (!item_live(L, P, s, si, c_fin, c_A) || !chk) return;
+  }
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int h = lane >> 5;
+  const int r = lane & 31;
+  const int DP = L.dp;
+  const int DH = DP >> 1;
+  const size_t ridx = (size_t)s * P.padr + rb0 * 32 + r;
+  const float lse_r = P.lse_in[ridx];
+  const float* rrow = P.rec_row + ridx * DP + h * DH;   // this lane's half of the row
+  const int orow = rb0 * 32 + lane;
+  const bool owner = wave == 0 && lane < 32 && orow < nrows;
+  float own_lm = 0.f, own_w = 0.f;
+  if (owner) own_lm = P.lm_row[(size_t)s * P.padr + orow];
+  bool fast = false;
+  float M = 0.f;
+  if (upd) {
+    update_facts(L, P, s, ncols, fast, M);
+    if (!item_live(L, P, s, si, c_fin, c_A)) return;
+  }
+  if (owner) own_w = P.w_row[(size_t)si.lane * P.w_ld + orow];
+  const bool live_r = rb0 * 32 + r < nrows && lse_r != INFINITY;
+  float bias = 0.f;
+  if (live_r) {
+    if (!upd) bias = -lse_r;
+    else if (fast) bias = -(lse_r + M);
+  }
+  const float baug = h ? bias : 1.f;
+
+  const int ct = (ncols + kColTile - 1) / kColTile;
+  const int tpg = (ct + kGroups - 1) / kGroups;
+  const float* ccol = P.rec_col + (size_t)s * P.padc * DP + h * DH + (size_t)r * DP;
+  const float* gcol = P.gam_col + (size_t)s * P.padc + r;
+#pragma unroll 1
+  for (int u = 0; u < GW; ++u) {
+    const int g = wave * GW + u;
+    const int t0 = min(ct, g * tpg), t1 = min(ct, g * tpg + tpg);
+    float mrun = fast ? 0.f : -INFINITY, srun = 0.f;
+#pragma unroll 1
+    for (int t = t0; t < t1; ++t) {
+      const float* c = ccol + (size_t)t * kColTile * DP;
+      f32x16 acc = f32x16{0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll 1
+      for (int k0 = 0; k0 < DH; k0 += KU) {
+        float av[KU], bw[KU];
+#pragma unroll
+        for (int q = 0; q < KU; ++q) {
+          const bool in = k0 + q < DH;
+          av[q] = in ? c[k0 + q] : 0.f;
+          bw[q] = in ? rrow[k0 + q] : 0.f;
+        }
+#pragma unroll
+        for (int q = 0; q < KU; ++q) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av[q], bw[q], acc, 0, 0, 0);
+      }
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(h ? 1.f : gcol[(size_t)t * kColTile], baug, acc, 0, 0, 0);
+      float e[16];
+      if (fast) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) e[v] = ex2(acc[v]);
+#pragma unroll
+        for (int w = 8; w > 0; w >>= 1)
+#pragma unroll
+          for (int v = 0; v < w; ++v) e[v] += e[v + w];
+        srun += e[0];
+      } else {
+        float tm = acc[0];
+#pragma unroll
+        for (int v = 1; v < 16; ++v) tm = fmaxf(tm, acc[v]);
+        const float mn = fmaxf(mrun, tm);
+        const float mref = (mn == -INFINITY) ? 0.f : mn;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) e[v] = ex2(acc[v] - mref);
+#pragma unroll
+        for (int w = 8; w > 0; w >>= 1)
+#pragma unroll
+          for (int v = 0; v < w; ++v) e[v] += e[v + w];
+        srun = srun * ex2(mrun - mref) + e[0];
+        mrun = mn;
+      }
+    }
+    sh_part[g][h][r] = make_float2(mrun, srun);
+  }
+  __syncthreads();
+  if (wave != 0) return;
+  // merge per row: half-waves, then groups, in order (as k_update_mfma)
+  float Mt = 0.f, St = 0.f;
+  if (owner && fast) {
+#pragma unroll
+    for (int g = 0; g < kGroups; ++g) St += sh_part[g][0][lane].y + sh_part[g][1][lane].y;
+  } else if (owner) {
+    float Mg[kGroups], Sg[kGroups];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int g = 0; g < kGroups; ++g) {
+      const float2 pa = sh_part[g][0][lane], pb = sh_part[g][1][lane];
+      const float mw = fmaxf(pa.x, pb.x);
+      const float mref = (mw == -INFINITY) ? 0.f : mw;
+      Sg[g] = pa.y * ex2(pa.x - mref) + pb.y * ex2(pb.x - mref);
+      Mg[g] = mw;
+      mx = fmaxf(mx, mw);
+    }
+    Mt = (mx == -INFINITY) ? 0.f : mx;
+#pragma unroll
+    for (int g = 0; g < kGroups; ++g) St += Sg[g] * ex2(Mg[g] - Mt);
+  }
+  // lane l < 32 owns row l of the item, whose input lse lane l read
+  const bool live = owner && lse_r != INFINITY;
+  finish_rows<32, 1, float>(L, P, s, si, rb0, owner, live, fast, M, lse_r, own_lm, own_w, Mt, St,
+                            rhat);
+}
+
 // --------------------------------------------------------- VALU half-step
 // Work item = 64 rows (one per lane) of one lane against all its columns, with
 // the same fixed column groups as the matrix-core kernel; each wave sweeps GW
@@ -856,10 +995,9 @@ void k_update_valu(Launch L) {
 // used while the bound's spread is at most kFastRangePrecise). The terms of one
 // 32-column tile are summed in float32 and each tile's sum is added in float64.
 //
-// A work item is 64 R rows (rows_f64(D): R = 2 up to d = 12, above which the
-// two rows' coordinates no longer fit in registers beside a column's): lane l
-// owns rows l + 64 r (r < R), so every column value read from LDS serves R
-// terms. Column data is the same for
+// A work item is 64 R rows (rows_f64(D): R = 2 up to d = 12, above which two
+// rows' coordinates no longer fit in registers beside a column's): lane l owns
+// rows l + 64 r (r < R), so every column value read from LDS serves R terms. Column data is the same for
 // every lane; each wave stages its tiles in its own LDS double buffer
 // (coalesced loads: records, then the column operand gam written into slot D
 // of each column -- the record's padding double when D is odd) and reads them
@@ -1538,8 +1676,8 @@ __global__ __launch_bounds__(kGuardThreads) void k_check64(Launch L, GuardArgs G
   __shared__ double sh_y[DR == 0 ? 1 : CH * DS];
   __shared__ double sh_pot[CH];
   __shared__ double sh_acc[kGuardThreads];
-  __shared__ double sh_row[128];
-  __shared__ int sh_bad[128];
+  __shared__ double sh_row[256];
+  __shared__ int sh_bad[256];
   const int b = blockIdx.x;
   const int pi = b >= L.nb0;
   const Pass& P = L.p[pi];
@@ -1557,7 +1695,7 @@ __global__ __launch_bounds__(kGuardThreads) void k_check64(Launch L, GuardArgs G
   }
   if (!item_live(L, P, s, si, c_fin, c_A) || !checked) return;
   const int lane_id = si.lane;
-  const int R = L.rows;                        // 32, 64 or 128 rows per item
+  const int R = L.rows;                        // 32 to 256 rows per item
   const int nph = kGuardThreads / R;           // column phases
   const int tid = threadIdx.x;
   const int r = tid % R, ph = tid / R;
@@ -1830,7 +1968,7 @@ __global__ __launch_bounds__(256) void k_ingest_points(IngestArgs p, int chunk) 
         continue;
       }
       float* rec = p.bank.rec[side] + idx * p.dp;
-      float nrm = 0.f;
+      double nrm = 0.0;
       if (live) {
         for (int k = 0; k < p.d; ++k) {
           const double v = sigma * ((double)P[((size_t)t * ld + q) * p.d + k] - (double)c[k]);
@@ -1838,7 +1976,7 @@ __global__ __launch_bounds__(256) void k_ingest_points(IngestArgs p, int chunk) 
           // de-interleaved: even components first, then odd ones
           const int pos = (k & 1) ? (p.dh + (k >> 1)) : (k >> 1);
           rec[pos] = fv;
-          nrm = fmaf(fv, fv, nrm);
+          nrm = fma((double)fv, (double)fv, nrm);   // |y~|^2 of the rounded coordinates
         }
         if (p.d & 1) rec[p.dp - 1] = 0.f;
       } else {
@@ -1855,7 +1993,7 @@ __global__ __launch_bounds__(256) void k_ingest_points(IngestArgs p, int chunk) 
           p.bank.gam[0][par][idx] = NAN;
         } else {
           // gam^y = kappa (g^0 - |y - c|^2) = kappa g^0 - |y~|^2 / 2 (cold start: g^0 = 0)
-          const float gam0 = p.g0 ? (float)(kg0 - 0.5 * (double)nrm) : -0.5f * nrm;
+          const float gam0 = (float)(kg0 - 0.5 * nrm);
           p.bank.gam[1][par][idx] = gam0;
           p.bank.lse[1][par][idx] = (float)lm - gam0;
         }
@@ -1998,6 +2136,20 @@ hipError_t launch_update(const Launch& a, int d, bool use_mfma, int variant, int
   }
 }
 
+hipError_t launch_update_mfma_k(const Launch& a, int variant, int blocks, hipStream_t st,
+                                hipEvent_t e0, hipEvent_t e1) {
+  if (blocks <= 0) return hipSuccess;
+  const bool uni = a.p[0].ipl > 0;   // both passes of a launch share the shapes
+  if (variant == VAR_NARROW) {
+    if (uni) hipExtLaunchKernelGGL((k_update_mfma_k<1, true>), dim3(blocks), dim3(512), 0, st, e0, e1, 0, a);
+    else hipExtLaunchKernelGGL((k_update_mfma_k<1, false>), dim3(blocks), dim3(512), 0, st, e0, e1, 0, a);
+  } else {
+    if (uni) hipExtLaunchKernelGGL((k_update_mfma_k<2, true>), dim3(blocks), dim3(256), 0, st, e0, e1, 0, a);
+    else hipExtLaunchKernelGGL((k_update_mfma_k<2, false>), dim3(blocks), dim3(256), 0, st, e0, e1, 0, a);
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_update_f64(const Launch& a, int d, int variant, int blocks, hipStream_t st,
                              hipEvent_t e0, hipEvent_t e1) {
   if (blocks <= 0) return hipSuccess;
@@ -2033,7 +2185,7 @@ hipError_t launch_update_mat(const Launch& a, int blocks, hipStream_t st, hipEve
 }
 hipError_t launch_check64(const Launch& a, const GuardArgs& g, int blocks, hipStream_t st) {
   if (blocks <= 0) return hipSuccess;
-  if (a.rows != 32 && a.rows != 64 && a.rows != 128) return hipErrorInvalidValue;
+  if (a.rows != 32 && a.rows != 64 && a.rows != 128 && a.rows != 256) return hipErrorInvalidValue;
   const dim3 grid(blocks), block(kGuardThreads);
   if (g.d <= 4) hipLaunchKernelGGL(k_check64<4>, grid, block, 0, st, a, g);
   else if (g.d <= 8) hipLaunchKernelGGL(k_check64<8>, grid, block, 0, st, a, g);

@@ -47,15 +47,19 @@ def _decision_exempt(dg, sg, ell, r_near, tol):
     return worst <= EXEMPT_BAND, worst
 
 
-@pytest.mark.parametrize("name", ["c2", "c4", "c5"])
-def test_full_size_window_against_stored_oracle(name):
+@pytest.mark.parametrize("name,flags", [("c2", 0), ("c4", 0), ("c5", 0), ("c4", 256)],
+                         ids=["c2", "c4", "c5", "c4-matrix-free"])
+def test_full_size_window_against_stored_oracle(name, flags):
+    """flags 256 = DS_F_MATRIX_FREE: the feature window on the K-looped
+    matrix-core half-step instead of the materialised cost."""
     path = os.path.join(GOLDEN, f"full_size_{name}.npz")
     z = np.load(path, allow_pickle=False)
     tol = float(z["tol"])
     lanes = [int(t) for t in z["lanes"]]
     w = wl.make(name)
-    log(f"[case] full size {name}: W={w.W} streams={STREAMS[name]} compared lanes {lanes}")
-    g = run_gpu(w, tol, max_iter=int(z["max_iter"]), streams=STREAMS[name])
+    log(f"[case] full size {name} flags={flags}: W={w.W} streams={STREAMS[name]} compared lanes "
+        f"{lanes}")
+    g = run_gpu(w, tol, max_iter=int(z["max_iter"]), streams=STREAMS[name], flags=flags)
     exempt, worst_pot, worst_res = [], 0.0, 0.0
     for q, t in enumerate(lanes):
         nt, mt = int(w.n[t]), int(w.m[t])

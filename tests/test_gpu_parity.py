@@ -15,6 +15,7 @@ pytestmark = pytest.mark.gpu
 
 F_SHADOW, F_FORCE_VALU, F_FORCE_MFMA, F_PRECISE, F_MATERIALIZE, F_GUARD = 1, 4, 8, 16, 32, 64
 F_FAST32 = 128
+F_MATRIX_FREE = 256
 # opt-in float32 kernels: outside the 1e-6 depth contract (see tests/gpu_support.py)
 FP32_FLAGS = F_FAST32 | F_FORCE_VALU | F_FORCE_MFMA | F_MATERIALIZE
 
@@ -105,6 +106,36 @@ def test_features_large_d_reduced_ragged():
     sizes in one window."""
     w = wl.make("c4", W=4, n=256, m=240, hetero=(90, 256), pad_value=np.nan)
     _case("c4-reduced", w, 1e-3)
+
+
+def test_matrix_free_large_d_reduced_ragged():
+    """d = 512 on the K-looped matrix-core half-step (DS_F_MATRIX_FREE: the
+    cost recomputed per tile instead of materialised): ragged NaN-padded lanes
+    against the oracle."""
+    w = wl.make("c4", W=4, n=256, m=240, hetero=(90, 256), pad_value=np.nan)
+    _case("c4-reduced-matrix-free", w, 1e-3, flags=F_MATRIX_FREE)
+
+
+def test_large_d_beyond_the_materialised_limit():
+    """At d > 32 a side with more than 8192 points cannot be materialised: the
+    default is then the matrix-free half-step (here d = 40, one lane with 9000
+    source points and one with 8300 target points)."""
+    rng = np.random.default_rng(17)
+    W, n_max, m_max, d = 2, 9000, 8300, 40
+    n = np.array([9000, 300], np.int32)
+    m = np.array([200, 8300], np.int32)
+    X = np.full((W, n_max, d), np.nan, np.float32)
+    Y = np.full((W, m_max, d), np.nan, np.float32)
+    a = np.full((W, n_max), np.nan, np.float32)
+    b = np.full((W, m_max), np.nan, np.float32)
+    for t in range(W):
+        X[t, :n[t]] = rng.standard_normal((n[t], d)) / np.sqrt(d)
+        Y[t, :m[t]] = (rng.standard_normal((m[t], d)) + 0.3) / np.sqrt(d)
+        aa = rng.gamma(1.0, size=n[t]); a[t, :n[t]] = aa / aa.sum()
+        bb = rng.gamma(1.0, size=m[t]); b[t, :m[t]] = bb / bb.sum()
+    eps = np.array([0.1, 0.15], np.float32)
+    w = wl.Workload("large-d-wide", X, Y, a, b, eps, n, m, 1e-3, 5000)
+    _case("large-d beyond 8192 points", w, 1e-3)
 
 
 @pytest.mark.parametrize("name", ["c2", "c5"])
