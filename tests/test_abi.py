@@ -88,8 +88,9 @@ def test_precise_state_default_validation_and_size():
 
 def test_materialised_cost_validation_and_size():
     """d > 32 selects the materialised cost: the workspace holds W n_pad m_pad
-    floats of cost; the float64 state and forced kernels are refused for it,
-    and so are more than 8192 points per side."""
+    floats of cost; the float64 state and forced kernels are refused for it.
+    More than 8192 points on a side (or DS_F_MATRIX_FREE) selects the
+    matrix-free large-d half-step instead."""
     op = ds._options(1e-3, None, 100, 1, "active", 0)
     code, n512 = _bytes(_problem(W=2, n_max=256, m_max=200, d=512), op)
     assert code == 0 and n512 >= 2 * 256 * 256 * 4
@@ -99,7 +100,17 @@ def test_materialised_cost_validation_and_size():
     for fl in (ds.F_PRECISE, ds.F_FAST32, ds.F_FORCE_VALU, ds.F_FORCE_MFMA):
         o = ds._options(1e-3, None, 100, 1, "active", fl)
         assert _bytes(_problem(d=64), o)[0] == 4
-    assert _bytes(_problem(n_max=9000, d=64), op)[0] == 4
+    # a side beyond 8192 points cannot be materialised: the matrix-free large-d
+    # half-step takes it (no cost matrix in the workspace); forcing the
+    # materialised cost there is refused, and the two flags are exclusive
+    code, nfree = _bytes(_problem(W=2, n_max=9000, m_max=200, d=64), op)
+    assert code == 0 and nfree < 2 * 9000 * 200 * 4
+    assert _bytes(_problem(n_max=9000, d=64), opm)[0] == 4
+    opf = ds._options(1e-3, None, 100, 1, "active", ds.F_MATRIX_FREE)
+    code, nf = _bytes(_problem(W=2, n_max=256, m_max=200, d=512), opf)
+    assert code == 0 and nf < 2 * 256 * 256 * 4
+    both = ds._options(1e-3, None, 100, 1, "active", ds.F_MATRIX_FREE | ds.F_MATERIALIZE)
+    assert _bytes(_problem(d=64), both)[0] == 1
 
 
 def test_solve_rejects_bad_arguments_before_device_work():
