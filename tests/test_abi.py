@@ -108,7 +108,8 @@ def test_materialised_cost_validation_and_size():
     assert _bytes(_problem(n_max=9000, d=64), opm)[0] == 4
     opf = ds._options(1e-3, None, 100, 1, "active", ds.F_MATRIX_FREE)
     code, nf = _bytes(_problem(W=2, n_max=256, m_max=200, d=512), opf)
-    assert code == 0 and nf < 2 * 256 * 256 * 4
+    # point records (2 banks x 2 sides x W x 256 padded points x 512 floats), no cost
+    assert code == 0 and nf >= 2 * 2 * 2 * 256 * 512 * 4 and nf != n512
     both = ds._options(1e-3, None, 100, 1, "active", ds.F_MATRIX_FREE | ds.F_MATERIALIZE)
     assert _bytes(_problem(d=64), both)[0] == 1
 
