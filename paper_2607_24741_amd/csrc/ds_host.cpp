@@ -94,6 +94,7 @@ ds::Layout plan(const ds_problem* pr, const ds_options* op, void* ws) {
   L.mat = uses_mat(pr, op) ? 1 : 0;
   L.rows = L.mat ? ds::kRowsValu
                  : uses_f64(pr, op) ? ds::rows_f64(pr->d)
+                 : uses_mfree(pr, op) ? ds::kRowsMfmaK
                  : uses_mfma(pr, op) ? ds::kRowsMfma : ds::kRowsValu;
   // every lane-side holds whole work items
   const size_t padq = (size_t)std::max(ds::kPad, L.rows);
@@ -438,7 +439,8 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
   auto pick = [&](int items, int role) -> int {
     if (mat) return VAR_MEDIUM;   // one layout: 64-row items, one block each
     // (the float64 kernel's items hold 64 to 256 rows: fewer items per width)
-    const int medium = use_mfma ? kMediumItemsMfma : kMediumItemsValu * kRowsValu / L.rows;
+    const int medium = use_mfma ? kMediumItemsMfma * kRowsMfma / L.rows
+                                : kMediumItemsValu * kRowsValu / L.rows;
     if (items < medium) return VAR_NARROW;
     return (use_mfma && tpg[role] <= 2) ? VAR_MEDIUM4 : VAR_MEDIUM;
   };

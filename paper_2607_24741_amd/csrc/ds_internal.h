@@ -34,6 +34,7 @@ constexpr int kColTile = 32;     // columns per MFMA tile
 constexpr int kGroups = 8;       // fixed column groups of a lane (whole tiles each)
 constexpr int kRowsMfma = 32;    // rows per work item, matrix-core kernel
 constexpr int kRowsValu = 64;    // rows per work item, vector-ALU kernel
+constexpr int kRowsMfmaK = 128;  // rows per work item, matrix-free large-d kernel
 constexpr int kMaxW = 4096;
 constexpr int kMaxDSmall = 32;   // matrix-free kernels
 constexpr int kMaxDF64 = 16;     // matrix-free float64-state kernels

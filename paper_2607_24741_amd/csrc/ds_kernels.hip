@@ -729,18 +729,22 @@ void k_update_mfma(Launch L) {
 // --------------------------------------------------- matrix-free, large d
 // The same half-step as k_update_mfma for any d: the contraction x~ . y~ is
 // K-looped over the coordinates on v_mfma_f32_32x32x2_f32, both operands read
-// per tile from memory (a row item's coordinates stay in the L1/L2 caches
-// across its column tiles; a lane's columns in L2), KU coordinate pairs per
-// batch of loads; then the augmented pair (gam_j, 1) . (1, -anchor_i) and the
-// same streaming base-2 sum, fixed column groups and merge as k_update_mfma.
-// It is the path for d > 32 when the cost cannot be materialised (more than
-// 8192 points on a side) or on request (DS_F_MATRIX_FREE).
+// per tile from memory, KU coordinate pairs per batch of loads (two register
+// buffers: the next batch is in flight while the current one runs). A work
+// item is kRowsMfmaK = 128 rows (RT = 4 row tiles), so each column operand a
+// lane loads feeds four matrix-core instructions; the row operands are shared
+// by the block's waves through the caches. Then the augmented pair
+// (gam_j, 1) . (1, -anchor_i) and the same streaming base-2 sum, fixed column
+// groups and merge as k_update_mfma. It is the path for d > 32 when the cost
+// cannot be materialised (more than 8192 points on a side) or on request
+// (DS_F_MATRIX_FREE).
 template <int GW, bool UNI>
 __global__ __launch_bounds__(64 * (kGroups / GW), 2)
 void k_update_mfma_k(Launch L) {
   note_progress(L);
-  constexpr int KU = 8;                       // coordinate pairs per batch of loads
-  __shared__ float2 sh_part[kGroups][2][32];
+  constexpr int KU = 4;                       // coordinate pairs per batch of loads
+  constexpr int RT = kRowsMfmaK / 32;         // row tiles per item
+  __shared__ float2 sh_part[kGroups][2][kRowsMfmaK];
   const int b = blockIdx.x;
   const int pi = b >= L.nb0;
   const Pass P = L.p[pi];
@@ -753,7 +757,8 @@ void k_update_mfma_k(Launch L) {
   float rhat = NAN;
   if (!upd) {
     const bool chk = check_facts(L, P, s, P.role ? ncols : nrows, rhat);
-    if (!item_live(L, P, s, si, c_fin, c_A) || !chk) return;
+    if (!item_live(L, P, s, si, c_fin, c_A)) return;
+    if (!chk) return;
   }
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -761,27 +766,45 @@ void k_update_mfma_k(Launch L) {
   const int r = lane & 31;
   const int DP = L.dp;
   const int DH = DP >> 1;
-  const size_t ridx = (size_t)s * P.padr + rb0 * 32 + r;
-  const float lse_r = P.lse_in[ridx];
-  const float* rrow = P.rec_row + ridx * DP + h * DH;   // this lane's half of the row
-  const int orow = rb0 * 32 + lane;
-  const bool owner = wave == 0 && lane < 32 && orow < nrows;
-  float own_lm = 0.f, own_w = 0.f;
-  if (owner) own_lm = P.lm_row[(size_t)s * P.padr + orow];
+  const int row0 = rb0 * kRowsMfmaK;
+  float lse_t[RT];
+  const float* rrow[RT];
+#pragma unroll
+  for (int q = 0; q < RT; ++q) {
+    const size_t ridx = (size_t)s * P.padr + row0 + 32 * q + r;
+    lse_t[q] = P.lse_in[ridx];
+    rrow[q] = P.rec_row + ridx * DP + h * DH;   // this lane's half of row tile q's row r
+  }
+  // wave 0 lane l owns rows row0 + l and row0 + 64 + l
+  bool owner[2];
+  float own_lm[2] = {0.f, 0.f}, own_w[2] = {0.f, 0.f}, own_lse[2];
+#pragma unroll
+  for (int e = 0; e < 2; ++e) {
+    const int orow = row0 + 64 * e + lane;
+    owner[e] = wave == 0 && orow < nrows;
+    if (owner[e]) own_lm[e] = P.lm_row[(size_t)s * P.padr + orow];
+    own_lse[e] = P.lse_in[(size_t)s * P.padr + orow];
+  }
   bool fast = false;
   float M = 0.f;
   if (upd) {
     update_facts(L, P, s, ncols, fast, M);
     if (!item_live(L, P, s, si, c_fin, c_A)) return;
   }
-  if (owner) own_w = P.w_row[(size_t)si.lane * P.w_ld + orow];
-  const bool live_r = rb0 * 32 + r < nrows && lse_r != INFINITY;
-  float bias = 0.f;
-  if (live_r) {
-    if (!upd) bias = -lse_r;
-    else if (fast) bias = -(lse_r + M);
+#pragma unroll
+  for (int e = 0; e < 2; ++e)
+    if (owner[e]) own_w[e] = P.w_row[(size_t)si.lane * P.w_ld + row0 + 64 * e + lane];
+  float baug[RT];
+#pragma unroll
+  for (int q = 0; q < RT; ++q) {
+    const bool live_q = row0 + 32 * q + r < nrows && lse_t[q] != INFINITY;
+    float bias = 0.f;
+    if (live_q) {
+      if (!upd) bias = -lse_t[q];
+      else if (fast) bias = -(lse_t[q] + M);
+    }
+    baug[q] = h ? bias : 1.f;
   }
-  const float baug = h ? bias : 1.f;
 
   const int ct = (ncols + kColTile - 1) / kColTile;
   const int tpg = (ct + kGroups - 1) / kGroups;
@@ -791,78 +814,105 @@ void k_update_mfma_k(Launch L) {
   for (int u = 0; u < GW; ++u) {
     const int g = wave * GW + u;
     const int t0 = min(ct, g * tpg), t1 = min(ct, g * tpg + tpg);
-    float mrun = fast ? 0.f : -INFINITY, srun = 0.f;
+    float mrun[RT], srun[RT];
+#pragma unroll
+    for (int q = 0; q < RT; ++q) { mrun[q] = fast ? 0.f : -INFINITY; srun[q] = 0.f; }
 #pragma unroll 1
     for (int t = t0; t < t1; ++t) {
       const float* c = ccol + (size_t)t * kColTile * DP;
-      f32x16 acc = f32x16{0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-#pragma unroll 1
-      for (int k0 = 0; k0 < DH; k0 += KU) {
-        float av[KU], bw[KU];
+      f32x16 acc[RT];
 #pragma unroll
-        for (int q = 0; q < KU; ++q) {
-          const bool in = k0 + q < DH;
-          av[q] = in ? c[k0 + q] : 0.f;
-          bw[q] = in ? rrow[k0 + q] : 0.f;
+      for (int q = 0; q < RT; ++q)
+        acc[q] = f32x16{0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+      float av0[KU], av1[KU], bw0[RT][KU], bw1[RT][KU];
+      auto fetch = [&](int k0, float* av, float (*bw)[KU]) {
+#pragma unroll
+        for (int v = 0; v < KU; ++v) {
+          const bool in = k0 + v < DH;
+          av[v] = in ? c[k0 + v] : 0.f;
+#pragma unroll
+          for (int q = 0; q < RT; ++q) bw[q][v] = in ? rrow[q][k0 + v] : 0.f;
         }
+      };
+      auto mma = [&](const float* av, float (*bw)[KU]) {
 #pragma unroll
-        for (int q = 0; q < KU; ++q) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av[q], bw[q], acc, 0, 0, 0);
+        for (int v = 0; v < KU; ++v)
+#pragma unroll
+          for (int q = 0; q < RT; ++q)
+            acc[q] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[v], bw[q][v], acc[q], 0, 0, 0);
+      };
+      fetch(0, av0, bw0);
+#pragma unroll 1
+      for (int k0 = 0; k0 < DH; k0 += 2 * KU) {
+        if (k0 + KU < DH) fetch(k0 + KU, av1, bw1);
+        mma(av0, bw0);
+        if (k0 + 2 * KU < DH) fetch(k0 + 2 * KU, av0, bw0);
+        if (k0 + KU < DH) mma(av1, bw1);
       }
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(h ? 1.f : gcol[(size_t)t * kColTile], baug, acc, 0, 0, 0);
-      float e[16];
-      if (fast) {
+      const float ag = h ? 1.f : gcol[(size_t)t * kColTile];
 #pragma unroll
-        for (int v = 0; v < 16; ++v) e[v] = ex2(acc[v]);
+      for (int q = 0; q < RT; ++q) {
+        acc[q] = __builtin_amdgcn_mfma_f32_32x32x2f32(ag, baug[q], acc[q], 0, 0, 0);
+        float e[16];
+        if (fast) {
 #pragma unroll
-        for (int w = 8; w > 0; w >>= 1)
+          for (int v = 0; v < 16; ++v) e[v] = ex2(acc[q][v]);
 #pragma unroll
-          for (int v = 0; v < w; ++v) e[v] += e[v + w];
-        srun += e[0];
-      } else {
-        float tm = acc[0];
+          for (int w = 8; w > 0; w >>= 1)
 #pragma unroll
-        for (int v = 1; v < 16; ++v) tm = fmaxf(tm, acc[v]);
-        const float mn = fmaxf(mrun, tm);
-        const float mref = (mn == -INFINITY) ? 0.f : mn;
+            for (int v = 0; v < w; ++v) e[v] += e[v + w];
+          srun[q] += e[0];
+        } else {
+          float tm = acc[q][0];
 #pragma unroll
-        for (int v = 0; v < 16; ++v) e[v] = ex2(acc[v] - mref);
+          for (int v = 1; v < 16; ++v) tm = fmaxf(tm, acc[q][v]);
+          const float mn = fmaxf(mrun[q], tm);
+          const float mref = (mn == -INFINITY) ? 0.f : mn;
 #pragma unroll
-        for (int w = 8; w > 0; w >>= 1)
+          for (int v = 0; v < 16; ++v) e[v] = ex2(acc[q][v] - mref);
 #pragma unroll
-          for (int v = 0; v < w; ++v) e[v] += e[v + w];
-        srun = srun * ex2(mrun - mref) + e[0];
-        mrun = mn;
+          for (int w = 8; w > 0; w >>= 1)
+#pragma unroll
+            for (int v = 0; v < w; ++v) e[v] += e[v + w];
+          srun[q] = srun[q] * ex2(mrun[q] - mref) + e[0];
+          mrun[q] = mn;
+        }
       }
     }
-    sh_part[g][h][r] = make_float2(mrun, srun);
+#pragma unroll
+    for (int q = 0; q < RT; ++q) sh_part[g][h][32 * q + r] = make_float2(mrun[q], srun[q]);
   }
   __syncthreads();
   if (wave != 0) return;
   // merge per row: half-waves, then groups, in order (as k_update_mfma)
-  float Mt = 0.f, St = 0.f;
-  if (owner && fast) {
+  float Mt[2] = {0.f, 0.f}, St[2] = {0.f, 0.f};
 #pragma unroll
-    for (int g = 0; g < kGroups; ++g) St += sh_part[g][0][lane].y + sh_part[g][1][lane].y;
-  } else if (owner) {
-    float Mg[kGroups], Sg[kGroups];
-    float mx = -INFINITY;
+  for (int e = 0; e < 2; ++e) {
+    const int ri = 64 * e + lane;
+    if (!owner[e]) continue;
+    if (fast) {
 #pragma unroll
-    for (int g = 0; g < kGroups; ++g) {
-      const float2 pa = sh_part[g][0][lane], pb = sh_part[g][1][lane];
-      const float mw = fmaxf(pa.x, pb.x);
-      const float mref = (mw == -INFINITY) ? 0.f : mw;
-      Sg[g] = pa.y * ex2(pa.x - mref) + pb.y * ex2(pb.x - mref);
-      Mg[g] = mw;
-      mx = fmaxf(mx, mw);
+      for (int g = 0; g < kGroups; ++g) St[e] += sh_part[g][0][ri].y + sh_part[g][1][ri].y;
+    } else {
+      float Mg[kGroups], Sg[kGroups];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int g = 0; g < kGroups; ++g) {
+        const float2 pa = sh_part[g][0][ri], pb = sh_part[g][1][ri];
+        const float mw = fmaxf(pa.x, pb.x);
+        const float mref = (mw == -INFINITY) ? 0.f : mw;
+        Sg[g] = pa.y * ex2(pa.x - mref) + pb.y * ex2(pb.x - mref);
+        Mg[g] = mw;
+        mx = fmaxf(mx, mw);
+      }
+      Mt[e] = (mx == -INFINITY) ? 0.f : mx;
+#pragma unroll
+      for (int g = 0; g < kGroups; ++g) St[e] += Sg[g] * ex2(Mg[g] - Mt[e]);
     }
-    Mt = (mx == -INFINITY) ? 0.f : mx;
-#pragma unroll
-    for (int g = 0; g < kGroups; ++g) St += Sg[g] * ex2(Mg[g] - Mt);
   }
-  // lane l < 32 owns row l of the item, whose input lse lane l read
-  const bool live = owner && lse_r != INFINITY;
-  finish_rows<32, 1, float>(L, P, s, si, rb0, owner, live, fast, M, lse_r, own_lm, own_w, Mt, St,
-                            rhat);
+  const bool live[2] = {owner[0] && own_lse[0] != INFINITY, owner[1] && own_lse[1] != INFINITY};
+  finish_rows_r<kRowsMfmaK, 1, 2, float>(L, P, s, si, rb0, owner, live, fast, M, own_lse, own_lm,
+                                         own_w, Mt, St, rhat);
 }
 
 // --------------------------------------------------------- VALU half-step
