@@ -201,7 +201,7 @@ def cpu_baseline(w, tol):
     bounded sample of the window, each lane run for a fixed number of cycles
     with the two-sided audit after every cycle (the same work per slot as the
     solver), one process per core (at most 16). Mixed-size windows take 16
-    lanes at evenly spaced ranks of n_t m_t for 4 cycles; uniform ones their
+    lanes at evenly spaced ranks of n_t m_t for 12 cycles; uniform ones their
     first 16 lanes for 600 cycles."""
     import numpy as np
     import oracle
@@ -211,7 +211,7 @@ def cpu_baseline(w, tol):
     if len(set(area.tolist())) > 1:
         order = np.argsort(area, kind="stable")
         sel = [int(t) for t in order[np.linspace(0, w.W - 1, min(16, w.W)).round().astype(int)]]
-        cycles, what = 4, "lanes at evenly spaced ranks of n_t m_t"
+        cycles, what = 12, "lanes at evenly spaced ranks of n_t m_t"
     else:
         sel, cycles, what = list(range(min(16, w.W))), 600, "first lanes"
     t0 = time.perf_counter()

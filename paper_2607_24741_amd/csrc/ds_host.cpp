@@ -136,10 +136,11 @@ ds::Layout plan(const ds_problem* pr, const ds_options* op, void* ws) {
   return L;
 }
 
-// The matrix-core kernel is the default at every d: even at d = 2 or 3 its
-// augmented contraction (K = 2 ceil(d/2) + 2) costs fewer SIMD cycles per term
-// than the vector kernel's d fused multiply-adds plus the bias add, and it
-// was measured faster at d = 2, 3, 8 and 16.
+// Wherever the float32 state runs (DS_F_FAST32, or 16 < d <= 32), the
+// matrix-core kernel is the default: even at d = 2 or 3 its augmented
+// contraction (K = 2 ceil(d/2) + 2) costs fewer SIMD cycles per term than the
+// vector kernel's d fused multiply-adds plus the bias add, and it was measured
+// faster at d = 2, 3, 8 and 16.
 bool uses_mfma(const ds_problem* pr, const ds_options* op) {
   if (uses_f64(pr, op)) return false;
   if (op->flags & DS_F_FORCE_VALU) return false;

@@ -21,6 +21,14 @@
 // so the f-update of cycle k+1 yields the row screen of state k with no extra
 // pass over (i, j) (eq:updated-marginal makes the column marginal the current
 // one; Sec. 3.1).
+//
+// Precision. With the float64 state (the default for d <= 16) the records,
+// log masses, lse and gam are doubles and every exponent is formed in double
+// before one rounding to float32 for the exponential: the terms of the method
+// are of size C/eps (thousands in base-2 units), so rounding the scaled
+// coordinates or the potentials to float32 perturbs each exponent by
+// ~C/eps * 2^-24 and moves the residual trajectory by 1e-6..1e-5, while the
+// single rounding of an exponent of magnitude <= 64 costs ~1e-8 on it.
 #pragma once
 
 #include <stdint.h>

@@ -1,20 +1,30 @@
 // gfx950 kernels of the active-set batched Sinkhorn path (wave64, CDNA4).
 //
-//  k_update_mfma<DH, RT, GW, UNI>
+//  k_update_f64<D, GW>
 //                     one half-step of eq:sinkhorn-cycle for every (slot, row
-//                     block) work item: x~.y~ on the fp32 matrix cores
-//                     (v_mfma_f32_32x32x2_f32) with the column potential and the
-//                     row anchor folded into the contraction, streaming base-2
-//                     log-sum-exp on the vector ALU over 8 fixed column groups,
-//                     fused row screen; with a second pass in the same launch,
-//                     the column check and release decision (the default path
-//                     for every d <= 32).
-//  k_update_valu<D>   the same half-step on the vector ALU, column data
+//                     block) work item with the state in float64: every
+//                     exponent formed in float64 on the vector ALU (d fused
+//                     multiply-adds and an add) and rounded once to float32
+//                     for v_exp_f32, column data staged in LDS and broadcast,
+//                     two rows per lane up to d = 12, streaming base-2
+//                     log-sum-exp over 8 fixed column groups, fused row screen;
+//                     with a second pass in the same launch, the column check
+//                     and release decision (the default path for d <= 16).
+//  k_update_mfma<DH, RT, GW, UNI>
+//                     the same half-step with the state in float32: x~.y~ on
+//                     the fp32 matrix cores (v_mfma_f32_32x32x2_f32) with the
+//                     column potential and the row anchor folded into the
+//                     contraction (DS_F_FAST32 for d <= 16; the default for
+//                     16 < d <= 32).
+//  k_update_valu<D>   the float32 half-step on the vector ALU, column data
 //                     wave-uniform (scalar loads, SGPR operands); on request.
-//  k_update_f64<D>    the same half-step with the state in float64.
+//  k_update_mfma_k<GW, UNI>
+//                     the float32 matrix-core half-step for any d, K-looped
+//                     over the coordinates (d > 32 without a materialised cost).
 //  k_cost, k_mat_rows, k_mat_cols
 //                     the materialised cost: built once on the matrix cores,
-//                     then streamed from HBM by both half-steps (d > 32).
+//                     then streamed from HBM by both half-steps (the default
+//                     for d > 32 up to 8192 points a side).
 //  k_check64<DR>      float64 verification of the exported potentials (guarded
 //                     release).
 //  k_scan             one block: compaction map (survivor ranks, new work item
@@ -22,6 +32,7 @@
 //  k_move             retiree emission in caller lane order + survivor gather
 //                     into the other bank (physical compaction, Sec. 3.2).
 //  k_ingest_*         validation, centring/scaling, log masses, proposals.
+//  scratch            the fixed per-GPU workspace of ds_solve_noalloc.
 //
 // Determinism: every reduction runs in a fixed order (no float atomics); the
 // column groups and tile order of a lane depend only on its (n, m), so a lane's
