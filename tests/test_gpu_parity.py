@@ -23,7 +23,11 @@ FP32_FLAGS = F_FAST32 | F_FORCE_VALU | F_FORCE_MFMA | F_MATERIALIZE
 def band_for(flags, d):
     """Depth-decision band: the contract's 1e-6 on the default path, FP32_BAND
     for the opt-in float32 kernels (and for the float32 matrix-core default of
-    16 < d <= 32, where no float64-state kernel exists)."""
+    16 < d <= 32, where no float64-state kernel exists), and the guarded
+    release's residual bar for DS_F_GUARD, which decides on the rounded
+    float32 potentials it returns, not on the iterate."""
+    if flags & F_GUARD:
+        return GUARD_RES_ATOL
     if flags & FP32_FLAGS:
         return FP32_BAND
     if 16 < d <= 32 and not flags & F_PRECISE:
