@@ -453,6 +453,13 @@ def main():
                          **algorithmic_bytes(w, last, f64, stats[-1])),
         "h_terms": h_terms(w, stats, last, T, args.steps),
     }
+    if args.guard:
+        # lane-audits whose row marginal was verified in float64 (the outward
+        # bound excluded the rest), rejections, and the checks' (i, j) terms
+        rec["guard"] = {"lane_audits": int(sum(int(x) for x in last[2].cpu().numpy())),
+                        "row_verifications": stats[-1].screen_positive,
+                        "rejected": stats[-1].check_failures,
+                        "check_pair_evals": stats[-1].check_pair_evals}
     if not args.no_tol_sweep:
         rec["mixture_modes"], rec["mixture_tol_sweep"] = mixture_extras(args, base_flags)
     if not args.no_cpu_baseline:

@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define DS_API_VERSION 3
+#define DS_API_VERSION 4
 
 typedef enum {
   DS_OK = 0,
@@ -97,14 +97,20 @@ enum {
                            in the workspace and stream it from HBM in every
                            half-step; the default for d > 32 when n_max, m_max
                            <= 8192 (required here)                                */
-  DS_F_GUARD = 64u,     /* guarded release (eq:release-contract in float64): a lane
-                           whose float32 row screen is within the guard margin
-                           (r^ <= (1 + 1/64) tau_screen, or non-finite) is verified by a
-                           float64 evaluation of both marginals of exactly the
-                           float32 potentials the caller will receive (cost formed
-                           in float64 from the caller's coordinates); that residual
-                           decides the release and is the one reported. One extra
-                           launch per audit cycle; n_max, m_max <= 8192.         */
+  DS_F_GUARD = 64u,     /* guarded release (eq:release-contract in float64): the
+                           release is decided on a float64 evaluation of both
+                           marginals of exactly the float32 potentials the caller
+                           will receive (cost formed in float64 from the caller's
+                           coordinates), and that residual is the one reported.
+                           With the float64 state an outward bound on how far the
+                           rounding to float32 outputs and the screen's own
+                           arithmetic move the row residual (from the per-lane
+                           rounding sums, eps and the lane's masses) selects the
+                           lanes to verify: only those that could meet tol. With
+                           a float32 state every audited lane is verified. The
+                           column marginal is evaluated only for lanes whose row
+                           residual met tol. Two extra launches per audit cycle;
+                           n_max, m_max <= 8192.                                 */
   DS_F_MATRIX_FREE = 256u, /* d > 32: recompute the cost per tile on the matrix
                            cores (a K-looped contraction over d) instead of
                            materialising it; the default when a side has more
@@ -209,6 +215,9 @@ typedef struct {
                                  pass over (i, j) at the audited state|, over the
                                  audits where either is at most 2 tol (where a
                                  release can be decided)                          */
+  int32_t guard_missed;       /* DS_F_GUARD | DS_F_SHADOW: audits at which the
+                                 outward bound excluded a lane whose verified row
+                                 residual met tol (0 when the bound holds)         */
 } ds_stats;
 
 /* Version of this header the library was built from (DS_API_VERSION). */

@@ -27,7 +27,7 @@ __all__ = ["solve", "solve_noalloc", "workspace_bytes", "load_library", "library
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 _LIBPATH = os.path.join(_PKG, "_lib", "libdrainsinkhorn.so")
-API_VERSION = 3   # the structs below mirror include/ds.h at this version
+API_VERSION = 4   # the structs below mirror include/ds.h at this version
 
 MODES = {"active": 0, "static": 1, "logical": 2}
 LANE_CONVERGED, LANE_MAX_ITER, LANE_NONFINITE = 0, 1, 2
@@ -80,7 +80,7 @@ class _Stats(ctypes.Structure):
                 ("width_trace", ctypes.POINTER(ctypes.c_int32)),
                 ("width_trace_len", ctypes.c_int32),
                 ("workspace_bytes", ctypes.c_size_t), ("sub_batches", ctypes.c_int32),
-                ("screen_discrepancy", ctypes.c_double)]
+                ("screen_discrepancy", ctypes.c_double), ("guard_missed", ctypes.c_int32)]
 
 
 _lib = None
@@ -169,6 +169,7 @@ class Stats:
     workspace_bytes: int
     sub_batches: int
     screen_discrepancy: float
+    guard_missed: int
     row_residual: object = None   # [W] tensor
     col_residual: object = None   # [W] tensor
 
@@ -323,6 +324,6 @@ def _returns(out, st, trace_buf, return_stats):
                   st.l_max, st.cycles, st.audits, st.screen_positive, st.check_failures,
                   st.compactions, st.missed_ready, st.update_launches, st.ms_total, st.ms_update,
                   st.timed_pair_evals, st.ms_check, st.ms_compact, wt, st.workspace_bytes,
-                  st.sub_batches, st.screen_discrepancy,
+                  st.sub_batches, st.screen_discrepancy, st.guard_missed,
                   out.get("row_residual"), out.get("col_residual"))
     return ret + (stats,)

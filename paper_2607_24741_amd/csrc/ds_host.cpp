@@ -130,8 +130,11 @@ ds::Layout plan(const ds_problem* pr, const ds_options* op, void* ws) {
   L.ctrl = c.take<ds::Ctrl>(1);
   L.Q = L.mat ? c.take<float>(W * (size_t)L.pad[0] * (size_t)L.pad[1]) : nullptr;
   L.guard = (op->flags & DS_F_GUARD) ? 1 : 0;
-  for (int side = 0; side < 2; ++side)
+  for (int side = 0; side < 2; ++side) {
     L.agg64[side] = L.guard ? c.take<double2>(W * (size_t)L.rbmax) : nullptr;
+    L.gerr[side] = (L.guard && L.es == 2) ? c.take<float4>(W * (size_t)L.rbmax) : nullptr;
+  }
+  L.row64 = L.guard ? c.take<ds::RowCert>(W) : nullptr;
   L.bytes = align_up(c.off, 256);
   return L;
 }
@@ -324,7 +327,7 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
   ia.pad[0] = L.pad[0]; ia.pad[1] = L.pad[1];
   ia.bank = L.bank[0];
   ia.center = L.center;
-  ia.vcnt = L.vcnt; ia.nchk = L.nchk; ia.disc = L.disc; ia.rbmax = L.rbmax;
+  ia.vcnt = L.vcnt; ia.nchk = L.nchk; ia.disc = L.disc; ia.row64 = L.row64; ia.rbmax = L.rbmax;
   ia.precise = precise ? 1 : 0;
   ia.mat = mat ? 1 : 0;
   ia.ctrl = L.ctrl;
@@ -399,12 +402,16 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
     ga.ld_row[role] = role ? pr->m_max : pr->n_max;
     ga.ld_col[role] = role ? pr->n_max : pr->m_max;
     ga.agg64[role] = L.agg64[role];
+    ga.gerr[role] = L.gerr[role];
   }
+  ga.row64 = L.row64;
   ga.eps = pr->eps; ga.d = pr->d; ga.es = L.es;
-  // the float32 screen and the float64 residual of the returned potentials
-  // differ by the rounding of the state to float32 outputs (~1e-5 on c2-like
-  // lanes): a lane is verified once its screen is within 1/64 of the threshold
-  ga.tau_guard = (op->screen_tol > 0.f ? op->screen_tol : op->tol) * (1.f + 1.f / 64.f);
+  // with the float64 state the update kernels bound how far rounding to the
+  // float32 outputs moves the residual, and only lanes within that bound of
+  // tol are verified; a float32 state has no such bound below its own
+  // coordinate rounding (about 2^-24 C / eps per exponent), so every audited
+  // lane is verified
+  ga.bound = L.es == 2 ? 1 : 0;
   auto make_launch = [&]() {
     Launch l;
     std::memset(&l, 0, sizeof(l));
@@ -541,22 +548,28 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
     Launch lf = make_launch();
     lf.p[0] = make_pass(0, 0, pk1, pk, pk1);
     lf.p[0].depth = k - 1;
+    // guarded release: the export rounding of state k-1's f, before its check
+    if (audit_prev && guard) lf.p[0].gerr_out = L.gerr[0];
     const int vf = pick(items[0], 0);
     lf.nb0 = blocks_of(items[0]);
     ds_err r = run(lf, vf, lf.nb0, sample, k, 0);
     if (r != DS_OK) return r;
     if (audit_prev && guard) {
-      // guarded release: float64 verification of state k-1 (both marginals of
-      // the potentials the emission would write) before the g-half
+      // guarded release: float64 verification of state k-1 (the potentials the
+      // emission would write) before the g-half: the row marginal of the lanes
+      // the outward bound leaves, then the column marginal of those whose row
+      // residual met tol
       Launch lc = make_launch();
-      lc.p[0] = make_pass(0, 1, pk1, pk1, pk1);   // row marginal of state k-1
-      lc.p[1] = make_pass(1, 1, pk1, pk1, pk1);   // column marginal of state k-1
-      for (Pass& q : lc.p) {
-        q.depth = k - 1;
-        q.verify_all = shadow ? 1 : 0;
-      }
+      lc.p[0] = make_pass(0, 1, pk1, pk1, pk1);
+      lc.p[0].depth = k - 1;
+      lc.p[0].verify_all = shadow ? 1 : 0;
       lc.nb0 = std::max(items[0], 0);
-      HIP_TRY(launch_check64(lc, ga, lc.nb0 + std::max(items[1], 0), st));
+      HIP_TRY(launch_check64(lc, ga, lc.nb0, st));
+      Launch lk = make_launch();
+      lk.p[1] = make_pass(1, 1, pk1, pk1, pk1);
+      lk.p[1].depth = k - 1;
+      lk.nb0 = 0;
+      HIP_TRY(launch_check64(lk, ga, std::max(items[1], 0), st));
     }
     if (audit_prev && shadow && !guard) {
       // shadow mode: the row marginal of state k-1 recomputed by a dedicated
@@ -588,6 +601,8 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
       lg.p[0] = make_pass(1, 0, pk1, pk, pk);
       lg.nb0 = nbg;
     }
+    // guarded release: the export rounding of state k's g, for its audit
+    if (guard && k % ae == 0) lg.p[0].gerr_out = L.gerr[1];
     r = run(lg, vg, blocks, sample, k, 0);
     if (r != DS_OK) return r;
     launched = k;
@@ -606,7 +621,8 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
     HIP_TRY(launch_zero_counters(L.vcnt, W, st));
     int saveA = A;
     if (guard) {
-      // both marginals of state K in float64, every lane still running
+      // both marginals of state K in float64, every lane still running (the
+      // column launch decides)
       Launch lc = make_launch();
       lc.p[0] = make_pass(0, 1, pK, pK, pK);
       lc.p[1] = make_pass(1, 1, pK, pK, pK);
@@ -614,7 +630,9 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
         q.final_audit = 1; q.depth = K; q.verify_all = 1; q.decide = 1;
       }
       lc.nb0 = ctrl.items_f;
-      HIP_TRY(launch_check64(lc, ga, ctrl.items_f + ctrl.items_g, st));
+      HIP_TRY(launch_check64(lc, ga, ctrl.items_f, st));
+      lc.nb0 = 0;
+      HIP_TRY(launch_check64(lc, ga, ctrl.items_g, st));
     } else {
       Launch lv = make_launch();
       lv.p[0] = make_pass(0, 1, pK, pK, pK);
@@ -866,6 +884,7 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
       S.screen_positive += o.ctrl.screen_pos;
       S.check_failures += o.ctrl.check_fail;
       S.missed_ready += o.ctrl.missed_ready;
+      S.guard_missed += o.ctrl.guard_missed;
       S.compactions += o.compactions;
       S.update_launches += o.n_timed;   // timed launches
       S.workspace_bytes += o.ws_bytes;

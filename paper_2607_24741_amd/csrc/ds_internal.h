@@ -88,7 +88,8 @@ struct Ctrl {
   int retire_events; // retirements at ordinary audits (each ran one extra cycle)
   int compacted;     // retired lanes already removed by compaction
   int A_prev;        // width before the latest compaction map
-  int pad2;
+  int guard_missed;  // guarded release + shadow mode: audits whose verified row
+                     // residual met tol although the outward bound had excluded them
 };
 
 // Best-effort mirror of the control counters in pinned host memory, written
@@ -98,6 +99,14 @@ struct Ctrl {
 // the stream has completed.
 struct HostSnap {
   int n_active, n_retired, compacted, epoch, finished, items_act_f, items_act_g, progress;
+};
+
+// Guarded release: the float64 row residual of a verified state, by caller lane,
+// and the depth of that state (the column check of the same audit reads it).
+struct RowCert {
+  double r;
+  int depth;
+  int bad;       // non-finite marginal
 };
 
 // Per slot audit scratch (indexed by the slot at audit time).
@@ -155,6 +164,10 @@ struct Layout {
   Ctrl* ctrl;
   float* Q;          // materialised cost [W][pad0][pad1] by caller lane, base-2 units
   double2* agg64[2]; // guarded checks: per row block float64 partials [W][rbmax] (else null)
+  float4* gerr[2];   // guarded release, float64 state: per caller lane and row block
+                     // [W][rbmax] {sum of mass x export rounding, max export rounding,
+                     // sum of mass, 0} of each side's potentials (else null)
+  RowCert* row64;    // guarded release: [W] latest verified row residual by caller lane
   int guard;
   size_t bytes;
 };
@@ -183,6 +196,8 @@ struct Pass {
   const float* w_row;     // caller masses of the row side, [W][w_ld] by lane id
   const int* off;         // [A + 1] work item offsets (ipl == 0)
   float4* agg_out;        // [W][rbmax] this pass's row-block aggregates
+  float4* gerr_out;       // update kind, guarded release with the float64 state: the
+                          // export rounding of this side's potentials, by caller lane
   const float4* agg_bound;   // update: the column side's latest update aggregates
   const float4* agg_screen;  // column check: the f-half aggregates (row screen)
   const float4* agg_rowchk;  // final column check: the row-check aggregates
@@ -225,9 +240,12 @@ struct GuardArgs {
   const float* xy_col[2];                   // and of the column side, by lane id
   int ld_row[2], ld_col[2];                 // their point strides (n_max / m_max)
   double2* agg64[2];      // [W][rbmax] per row block {sum |marginal - mass|, non-finite}
+  const float4* gerr[2];  // export rounding per side (float64 state), see Layout::gerr
+  RowCert* row64;         // [W] row residual of the audit, read by its column check
   const float* eps;       // caller eps [W]
   int d, es;              // point dimension; state element size in floats
-  float tau_guard;        // screen threshold with the guard margin
+  int bound;              // 1: gate the row check by the outward bound (float64
+                          // state); 0: verify every audited lane
 };
 
 struct ScanArgs {          // compaction map over the slots of the current bank
@@ -269,6 +287,7 @@ struct IngestArgs {
   int* vcnt;
   int* nchk;
   float* disc;
+  RowCert* row64;        // guarded release: cleared (depth 0 matches no audit)
   int rbmax;
   Ctrl* ctrl;
 };

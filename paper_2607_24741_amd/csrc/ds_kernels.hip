@@ -260,7 +260,8 @@ __device__ __forceinline__ bool check_facts(const Launch& L, const Pass& P, int 
 // (Mt, St) of that row; R > 1 only with one aggregate per item, UNIT = 64 R).
 // Writes the new lse / gam (update kind), one aggregate per UNIT-row block
 // (NU of them), and -- for the deciding column check -- takes the lane's
-// retirement decision in the last arriving item of the lane.
+// retirement decision in the last arriving item of the lane. `gam_keep`, when
+// given, receives the new column operand of each live owned row (update kind).
 __device__ __forceinline__ float log2_t(float x) { return lg2(x); }
 __device__ __forceinline__ double log2_t(double x) { return log2(x); }
 __device__ __forceinline__ float exp2_t(float x) { return ex2(x); }
@@ -270,7 +271,8 @@ template <int UNIT, int NU, int R, typename T>
 __device__ void finish_rows_r(const Launch& L, const Pass& P, int s, const SlotInfo& si, int rb0,
                               const bool (&owner)[R], const bool (&live)[R], bool fast, float Mf,
                               const T (&lse_old)[R], const T (&lm)[R], const float (&w)[R],
-                              const T (&Mt)[R], const T (&St)[R], float rhat) {
+                              const T (&Mt)[R], const T (&St)[R], float rhat,
+                              T* gam_keep = nullptr) {
   static_assert(UNIT * NU <= 64 * R, "one wave owns the rows of an item");
   static_assert(R == 1 || (NU == 1 && UNIT == 64 * R), "several rows per lane: one aggregate");
   const int lane = threadIdx.x & 63;
@@ -290,6 +292,7 @@ __device__ void finish_rows_r(const Launch& L, const Pass& P, int s, const SlotI
         const T anchor = fast ? lse_old[r] + M : (T)0;   // the sweep's row anchor
         lse_new[r] = anchor + (Mt[r] + log2_t(St[r]));
         gam_new[r] = lm[r] - lse_new[r];
+        if (gam_keep) gam_keep[r] = gam_new[r];
         const float dl = (float)(lse_new[r] - lse_old[r]);
         if (isfinite(dl)) { dmin = fminf(dmin, dl); dmax = fmaxf(dmax, dl); } else { bad = 1.f; }
         if (P.role == 0) {
@@ -1049,6 +1052,15 @@ void k_update_valu(Launch L) {
                                    Mt, St, rhat);
 }
 
+// The potential of a float64-state point in the caller's units, before its
+// rounding to the float32 output: kappa f = gam + |x~|^2 / 2 (gam as stored,
+// nrm = |x~|^2 summed by fused multiply-adds in component order). Written with
+// an explicit fma so that every caller gets the same bits: the emission, and
+// the export-rounding sums of guarded release.
+__device__ __forceinline__ double potential_f64(double gam, double nrm, double kappa64) {
+  return fma(0.5, nrm, gam) * (1.0 / kappa64);
+}
+
 // ------------------------------------------------- float64 (precise) half-step
 // The vector-ALU half-step with the state (records, log masses, lse, gam) in
 // float64 and every exponent formed in float64 -- d fused multiply-adds and one
@@ -1263,8 +1275,34 @@ void k_update_f64(Launch L) {
   bool lo[R];
 #pragma unroll
   for (int r = 0; r < R; ++r) lo[r] = live[r] && owner[r];
+  double gkeep[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) gkeep[r] = -(double)INFINITY;
   finish_rows_r<ROWS, 1, R, double>(L, P, s, si, rb, owner, lo, fast, M, lse_old, lm, w, Mt, St,
-                                    rhat);
+                                    rhat, gkeep);
+  if (P.gerr_out == nullptr) return;
+  // Guarded release: how far rounding to the float32 outputs moves this item's
+  // potentials -- of the input state in the f-half (its column operand is
+  // lm - lse_old, bit for bit what that state's f-half stored), of the new
+  // state in the g-half. Per item {sum of mass x |rounding|, max |rounding|,
+  // sum of mass} over the points with mass; each |rounding| also covers the
+  // float64 evaluation of the potential (a few units of 2^-53 of its terms).
+  float sd = 0.f, md = 0.f, sw = 0.f;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const double gq = P.role ? gkeep[r] : lm[r] - lse_old[r];
+    if (!owner[r] || w[r] == 0.f || !(fabs(gq) < (double)INFINITY)) continue;
+    double nrm = 0.0;
+#pragma unroll
+    for (int k = 0; k < D; ++k) nrm = fma(xr[r][k], xr[r][k], nrm);
+    const double F = potential_f64(gq, nrm, si.kappa64);
+    const double dl = fabs((double)(float)F - F) + (fabs(gq) + 0.5 * nrm) * (0x1p-46 / si.kappa64);
+    sd += w[r] * (float)dl;
+    md = fmaxf(md, (float)dl);
+    sw += w[r];
+  }
+  const float4 v = make_float4(wave64(sd, OpAdd()), wave64(md, OpMax()), wave64(sw, OpAdd()), 0.f);
+  if (lane == 0) P.gerr_out[(size_t)si.lane * L.rbmax + rb] = v;
 }
 
 // ----------------------------------------------- materialised-cost half-steps
@@ -1627,7 +1665,7 @@ __device__ __forceinline__ float export_potential(const float* gam, const float*
     const double* r = reinterpret_cast<const double*>(rec) + e * dp;
     double nrm = 0.0;
     for (int k = 0; k < dp; ++k) nrm = fma(r[k], r[k], nrm);
-    return (float)((gq + 0.5 * nrm) * (1.0 / si.kappa64));
+    return (float)potential_f64(gq, nrm, si.kappa64);
   }
   const float gq = gam[e];
   if (gq == -INFINITY) return 0.f;
@@ -1708,13 +1746,20 @@ __global__ __launch_bounds__(256) void k_move(MoveArgs p) {
 
 // ------------------------------------------- float64 verification (DS_F_GUARD)
 // One marginal of the audited state in float64, for one work item (rows rows of a
-// lane against all its columns) of a lane the float32 screen calls ready within
-// the guard margin -- or of every lane at the final audit. The potentials are the
-// float32 values the emission writes for that state, the cost is formed in
-// float64 from the caller's coordinates, the exponentials are float64: the
-// residual that decides a release is that of the potentials the caller receives
-// (eq:release-contract), to float64 rounding. Pass 0: row marginal (rows = x),
-// pass 1: column marginal (rows = y).
+// lane against all its columns). The potentials are the float32 values the
+// emission writes for that state, the cost is formed in float64 from the
+// caller's coordinates, the exponentials are float64: the residual that decides
+// a release is that of the potentials the caller receives (eq:release-contract),
+// to float64 rounding.
+//
+// Two launches per audit. The row pass (pass 0, rows = x) runs for the lanes the
+// outward bound cannot exclude (guard_lower_bound) -- every lane at the final
+// audit -- and its last block records the row residual; a lane whose row
+// residual exceeds tol is rejected there. The column pass (pass 1, rows = y)
+// runs only for lanes whose row residual of the same audit met tol (every lane
+// at the final audit), and its last block takes the decision. Launched between
+// the f-half and the g-half of an audited cycle (state k-1 is read-only there)
+// and at the final audit.
 //
 // Thread (r, p) of the block owns row r of the item and column phase p (every
 // NPH-th column); it keeps the row's coordinates in registers (DR >= d of them,
@@ -1722,13 +1767,53 @@ __global__ __launch_bounds__(256) void k_move(MoveArgs p) {
 // coordinates and exported potentials are staged CH at a time in LDS, where
 // the lanes of a wave read the same column (a broadcast). A row's sum is its
 // phases' partial sums added in phase order. Each block publishes its rows' sum
-// of |marginal - mass| (row order); the last block of the lane over both
-// passes adds them in block order and takes the decision. Launched between the
-// f-half and the g-half of an audited cycle (state k-1 is read-only there) and
-// at the final audit.
+// of |marginal - mass| (row order); the last block of the lane adds them in
+// block order.
+// Outward bound of guarded release (float64 state). The verified residual is
+// that of the float32 outputs U, the screen rhat that of the state (f, g) the
+// iteration holds. Rounding moves each potential by |df_i|, |dg_j| (summed per
+// side by the update kernels as S = sum mass |d|, M = max |d|, A = sum mass), so
+// every coupling entry changes by a factor exp((df_i + dg_j) / eps), and with
+// |e^x - 1| <= |x| e^|x|:
+//   |r_row(U) - r_row| <= e^D / eps (sum_i R_i |df_i| + sum_j C_j |dg_j|),
+//   D = (M_f + M_g) / eps, sum_i R_i |df_i| <= S_f + r_row M_f,
+//   sum_j C_j |dg_j| <= (1 + eta) S_g (the g-half leaves C_j = b_j (1 +- eta)).
+// The screen itself is the row residual of (f, g) up to eta per row ratio
+// (exponents rounded once to float32 at |z| <= 64 after float64 formation:
+// 2.6e-6; v_exp_f32: 2.4e-7; float32 tile sums of at most 32 terms: 1.9e-6)
+// and a relative 4e-6 for its float32 summation over rows, so
+//   (rhat (1 - 4e-6) - eta A_f) / (1 + eta) <= r_row <= (rhat (1 + 4e-6) + eta A_f) / (1 - eta)
+// with eta = 1e-5. A lane whose lower bound on r_row(U) exceeds tol cannot be
+// released at this audit and is not verified. The float32 sums of the rounding
+// partials are inflated by 1e-5 relative.
+__device__ double guard_lower_bound(const Launch& L, const GuardArgs& G, const SlotInfo& si,
+                                    float rhat) {
+  float sf = 0.f, mf = 0.f, af = 0.f, sg = 0.f, mg = 0.f;
+  for (int side = 0; side < 2; ++side) {
+    const float4* base = G.gerr[side] + (size_t)si.lane * L.rbmax;
+    const int nrb = row_blocks(side ? si.m : si.n, L.rows);
+    float t0 = 0.f, t1 = 0.f, t2 = 0.f;
+    for (int q = (int)(threadIdx.x & 63); q < nrb; q += 64) {
+      const float4 v = base[q];
+      t0 += v.x;
+      t1 = fmaxf(t1, v.y);
+      t2 += v.z;
+    }
+    const float s0 = wave64(t0, OpAdd()), s1 = wave64(t1, OpMax()), s2 = wave64(t2, OpAdd());
+    if (side == 0) { sf = s0; mf = s1; af = s2; } else { sg = s0; mg = s1; }
+  }
+  const double eta = 1e-5, infl = 1.0 + 1e-5;
+  const double inv_eps = 1.0 / (double)G.eps[si.lane];
+  const double Sf = sf * infl, Mf = mf * infl, Af = af * infl, Sg = sg * infl, Mg = mg * infl;
+  const double r_lo = ((double)rhat * (1.0 - 4e-6) - eta * Af) / (1.0 + eta);
+  const double r_hi = ((double)rhat * (1.0 + 4e-6) + eta * Af) / (1.0 - eta);
+  const double eD = exp((Mf + Mg) * inv_eps);
+  return r_lo - eD * inv_eps * (Sf + r_hi * Mf + (1.0 + eta) * Sg) * infl;
+}
+
 constexpr int kGuardThreads = 256;
 template <int DR>
-constexpr int guard_chunk() { return DR == 0 ? 256 : (2048 / DR < 256 ? 2048 / DR : 256); }
+constexpr int guard_chunk() { return DR == 0 ? 256 : (2048 / (DR ? DR : 1) < 256 ? 2048 / (DR ? DR : 1) : 256); }
 
 template <int DR>
 __global__ __launch_bounds__(kGuardThreads) void k_check64(Launch L, GuardArgs G) {
@@ -1747,12 +1832,20 @@ __global__ __launch_bounds__(kGuardThreads) void k_check64(Launch L, GuardArgs G
   if (!place_item<1>(L, P, pass_blocks(L, pi), pi ? b - L.nb0 : b, s, rb, nrows, ncols, si, c_fin,
                      c_A))
     return;
-  // the lane's float32 row screen of the audited state (same gate for both passes)
-  const int n_x = P.role ? ncols : nrows;
-  bool checked = true;
+  // Row pass: the lane's row screen of the audited state against the outward
+  // bound (every lane without one, and every lane in shadow mode, which counts
+  // the verified rows the bound had excluded); column pass: the lanes whose
+  // row residual of this audit met tol. Every item of a lane decides alike.
+  bool checked = true, gate = true;
   if (!P.final_audit) {
-    const LaneAgg g = lane_aggregate(P.agg_screen, s, L.rbmax, row_blocks(n_x, L.rows), false);
-    checked = P.verify_all || !isfinite(g.sum) || g.sum <= G.tau_guard;
+    if (P.role == 0) {
+      const LaneAgg g = lane_aggregate(P.agg_screen, s, L.rbmax, row_blocks(nrows, L.rows), false);
+      gate = !isfinite(g.sum) || !G.bound || guard_lower_bound(L, G, si, g.sum) <= (double)L.tol;
+      checked = gate || P.verify_all;
+    } else {
+      const RowCert rc = G.row64[si.lane];
+      checked = rc.depth == P.depth && !rc.bad && rc.r <= (double)L.tol;
+    }
   }
   if (!item_live(L, P, s, si, c_fin, c_A) || !checked) return;
   const int lane_id = si.lane;
@@ -1840,30 +1933,45 @@ __global__ __launch_bounds__(kGuardThreads) void k_check64(Launch L, GuardArgs G
   __hip_atomic_store(dst + 1, (unsigned long long)__double_as_longlong(bad ? 1.0 : 0.0),
                      __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   wait_mem();
-  const int total = row_blocks(si.n, R) + row_blocks(si.m, R);   // the lane's blocks, both passes
+  const int total = row_blocks(P.role ? si.m : si.n, R);   // the lane's blocks in this pass
   const int prev = atomicAdd(&L.vcnt[lane_id], 1);
   if (prev + 1 != total) return;
   atomicExch(&L.vcnt[lane_id], 0);
-  // last block of the lane: both marginals' residuals, in block order
-  double rr[2] = {0.0, 0.0};
+  // last block of the lane: this marginal's residual, in block order
+  double rr = 0.0;
   bool fin = true;
-  for (int side = 0; side < 2; ++side) {
-    const int nrb = row_blocks(side ? si.m : si.n, R);
+  {
     unsigned long long* src =
-        reinterpret_cast<unsigned long long*>(G.agg64[side] + (size_t)s * L.rbmax);
-    for (int q = 0; q < nrb; ++q) {
-      rr[side] += __longlong_as_double((long long)__hip_atomic_load(
+        reinterpret_cast<unsigned long long*>(G.agg64[P.role] + (size_t)s * L.rbmax);
+    for (int q = 0; q < total; ++q) {
+      rr += __longlong_as_double((long long)__hip_atomic_load(
           src + 2 * q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
       if (__longlong_as_double((long long)__hip_atomic_load(
               src + 2 * q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) != 0.0)
         fin = false;
     }
   }
-  const double rrow = rr[0], rcol = rr[1];
-  fin = fin && isfinite(rrow) && isfinite(rcol);
+  fin = fin && isfinite(rr);
+  atomicAdd(&L.nchk[lane_id], 1);   // one marginal evaluated
+  if (P.role == 0) {
+    RowCert rc;
+    rc.r = rr;
+    rc.depth = P.depth;
+    rc.bad = fin ? 0 : 1;
+    G.row64[lane_id] = rc;
+    L.audit[s].rhat = (float)rr;
+    if (P.final_audit) return;   // the column pass decides
+    atomicAdd(&L.ctrl->screen_pos, 1);
+    if (!gate && fin && rr <= (double)L.tol) atomicAdd(&L.ctrl->guard_missed, 1);
+    if (!fin) retire_lane(L, P, s, si, 2, (float)rr, NAN);
+    else if (rr > (double)L.tol) atomicAdd(&L.ctrl->check_fail, 1);
+    return;
+  }
+  // column pass: the decision on both residuals of the audit
+  const RowCert rc = G.row64[lane_id];
+  const double rrow = rc.r, rcol = rr;
+  fin = fin && !rc.bad && isfinite(rrow);
   const double rmax = fmax(rrow, rcol);
-  atomicAdd(&L.nchk[lane_id], 2);   // both marginals evaluated
-  L.audit[s].rhat = (float)rrow;
   L.audit[s].rcol = (float)rcol;
   if (P.final_audit) {
     if (L.mode == MODE_STATIC && si.passed) {
@@ -1874,7 +1982,6 @@ __global__ __launch_bounds__(kGuardThreads) void k_check64(Launch L, GuardArgs G
     retire_lane(L, P, s, si, !fin ? 2 : (rmax <= (double)L.tol ? 0 : 1), (float)rrow, (float)rcol);
     return;
   }
-  atomicAdd(&L.ctrl->screen_pos, 1);
   if (!fin) retire_lane(L, P, s, si, 2, (float)rrow, (float)rcol);
   else if (rmax <= (double)L.tol) retire_lane(L, P, s, si, 0, (float)rrow, (float)rcol);
   else atomicAdd(&L.ctrl->check_fail, 1);
@@ -1954,6 +2061,13 @@ __global__ __launch_bounds__(256) void k_ingest_lanes(IngestArgs p) {
     p.vcnt[t] = 0;
     p.nchk[t] = 0;
     if (p.disc) p.disc[t] = 0.f;
+    if (p.row64) {
+      RowCert rc;
+      rc.r = 0.0;
+      rc.depth = 0;
+      rc.bad = 0;
+      p.row64[t] = rc;
+    }
   }
   // no previous half-step: the first update of each side runs unanchored
   const float4 none = make_float4(0.f, INFINITY, -INFINITY, 1.f);
@@ -2074,7 +2188,7 @@ __global__ void k_ctrl_init(Ctrl* c, int W) {
     z.err_lane = 0x7fffffff; z.err_code = 0; z.n_active = W; z.n_retired = 0; z.finished = 0;
     z.final_cycle = 0; z.A = W; z.items_f = 0; z.items_g = 0; z.items_act_f = 0;
     z.items_act_g = 0; z.screen_pos = 0; z.check_fail = 0; z.missed_ready = 0;
-    z.retire_events = 0; z.compacted = 0; z.A_prev = W; z.pad2 = 0;
+    z.retire_events = 0; z.compacted = 0; z.A_prev = W; z.guard_missed = 0;
     *c = z;
   }
 }

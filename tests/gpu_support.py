@@ -19,6 +19,12 @@ d <= 16, the materialised cost above 32). The opt-in float32 kernels
 round the scaled coordinates and potentials to float32, which moves residual
 trajectories by 1e-6..1e-5; their tests pass band=FP32_BAND and still count
 the lanes outside the 1e-6 band (report["beyond_1e6"]).
+
+Guarded release (DS_F_GUARD) reports, and decides on, the residual of the
+float32 potentials it returns rather than of the iterate. Its tests widen the
+residual bar and the depth band of each lane by export_rounding_bound(): how
+far rounding to those float32 values can move the residual, derived from the
+returned values themselves (half an ulp each), the masses and eps.
 """
 
 from __future__ import annotations
@@ -77,6 +83,28 @@ def run_oracle(w, tol, *, lanes=None, **kw):
                         lanes=lanes, processes=procs(), g0=getattr(w, "g0", None), **kw)
 
 
+def export_rounding_bound(w, g, t):
+    """Upper bound on |r(U) - r(f, g)| for lane t, U the float32 potentials the
+    GPU returned and (f, g) any state they round from: every |U_i - f_i| is at
+    most half an ulp of U_i, each coupling entry then moves by a factor
+    exp((df_i + dg_j) / eps), and with |e^x - 1| <= |x| e^|x| the row residual
+    moves by at most e^D / eps (sum_i R_i |df_i| + sum_j C_j |dg_j|),
+    D = (max |df| + max |dg|) / eps, with sum_i R_i |df_i| <= <a, |df|> + r max|df|
+    and C_j <= b_j (1 + 1e-5) (the column marginal after a g-half). The same
+    bound holds for the column residual with the roles exchanged."""
+    nt, mt = int(w.n[t]), int(w.m[t])
+    a, b = w.a[t, :nt].astype(np.float64), w.b[t, :mt].astype(np.float64)
+    fu = np.abs(g["f"][t, :nt].astype(np.float32))
+    gu = np.abs(g["g"][t, :mt].astype(np.float32))
+    hf = np.where(a != 0, np.spacing(fu).astype(np.float64) / 2, 0.0)
+    hg = np.where(b != 0, np.spacing(gu).astype(np.float64) / 2, 0.0)
+    eps = float(w.eps[t])
+    r = float(g["residual"][t]) if np.isfinite(g["residual"][t]) else 1.0
+    mx = max(hf.max(initial=0.0), hg.max(initial=0.0))
+    side = max((a * hf).sum() + (1 + 1e-5) * (b * hg).sum(), (b * hg).sum() + (1 + 1e-5) * (a * hf).sum())
+    return float(np.exp(2 * mx / eps) / eps * (side + r * mx))
+
+
 def pot_err(fg, fo, gg, go, eps):
     scale = max(np.abs(fo).max(), np.abs(go).max(), eps)
     return max(np.abs(fg - fo).max(), np.abs(gg - go).max()) / scale
@@ -115,18 +143,20 @@ def compare(w, g, o, tol, *, audit_every=1, max_iter=5000, lanes=None, check_ord
     """
     lanes = range(w.W) if lanes is None else lanes
     report = dict(max_pot_err=0.0, max_res_err=0.0, near_threshold=[], beyond_1e6=0)
+    per_lane = lambda v, t: float(v[t]) if np.ndim(v) else float(v)
     for t in lanes:
         nt, mt = int(w.n[t]), int(w.m[t])
         dg, do = int(g["depth"][t]), int(o["depth"][t])
         sg, so = int(g["status"][t]), int(o["status"][t])
         ref_f, ref_g, ref_r = o["f"][t, :nt], o["g"][t, :mt], o["residual"][t]
+        band_t = per_lane(band, t)
         if dg != do or sg != so:
-            ok, margin, fw = decision_consistent(w, t, tol, dg, sg, audit_every, band=band)
+            ok, margin, fw = decision_consistent(w, t, tol, dg, sg, audit_every, band=band_t)
             report["near_threshold"].append((t, dg, do, margin))
             if margin > EXEMPT_BAND:
                 report["beyond_1e6"] += 1
             assert ok, (f"lane {t}: gpu depth/status ({dg},{sg}) vs oracle ({do},{so}): the "
-                        f"oracle's residual is {margin:.3e} from tol, outside the {band:.0e} band")
+                        f"oracle's residual is {margin:.3e} from tol, outside the {band_t:.2e} band")
             ref_f, ref_g, ref_r = fw["f"], fw["g"], fw["residual"]
         e = pot_err(g["f"][t, :nt], ref_f, g["g"][t, :mt], ref_g, float(w.eps[t]))
         report["max_pot_err"] = max(report["max_pot_err"], e)
@@ -134,7 +164,7 @@ def compare(w, g, o, tol, *, audit_every=1, max_iter=5000, lanes=None, check_ord
         if sg != oracle.NONFINITE:
             re_ = abs(g["residual"][t] - ref_r)
             report["max_res_err"] = max(report["max_res_err"], re_)
-            assert re_ <= res_atol, (t, g["residual"][t], ref_r)
+            assert re_ <= per_lane(res_atol, t), (t, g["residual"][t], ref_r, per_lane(res_atol, t))
         # padded tails are written zero
         assert np.all(g["f"][t, nt:] == 0) and np.all(g["g"][t, mt:] == 0)
     sel = set(lanes)

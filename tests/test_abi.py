@@ -28,7 +28,7 @@ def test_library_exports_every_declared_function():
                           "ds_last_error_message", "ds_solve_noalloc"}
     for nm in names:
         assert hasattr(lib, nm), nm
-    assert lib.ds_api_version() == 3
+    assert lib.ds_api_version() == 4
     for code in range(6):
         assert lib.ds_error_string(code).decode()
 
@@ -168,13 +168,26 @@ def test_sub_batch_validation_and_size():
 
 
 def test_guarded_release_validation_and_size():
-    """DS_F_GUARD keeps two float64 partials per row block and lane, and
-    stages a lane's column potentials in LDS (at most 8192 points per side)."""
+    """DS_F_GUARD keeps two float64 partials per row block and lane and one
+    row certificate per lane; with the float64 state also the export-rounding
+    sums of both sides per row block and lane (the outward bound), which a
+    float32 state does not have. At most 8192 points per side."""
     op = ds._options(1e-3, None, 100, 1, "active", 0, 1)
     opg = ds._options(1e-3, None, 100, 1, "active", ds.F_GUARD, 1)
     code, n0 = _bytes(_problem(W=4, n_max=256, m_max=256, d=8), op)
     code2, n1 = _bytes(_problem(W=4, n_max=256, m_max=256, d=8), opg)
     assert code == 0 and code2 == 0 and n1 > n0
+    W, rb = 512, 8192 // 128          # float64 state at d = 8: 128-row blocks
+    big = _problem(W=W, n_max=8192, m_max=8192, d=8)
+    c3, g64 = _bytes(big, opg)
+    c4, p64 = _bytes(big, op)
+    assert c3 == 0 and c4 == 0
+    # agg64 (2 x 16 B) and the rounding sums (2 x 16 B) per row block, 16 B per lane
+    assert g64 - p64 == W * rb * 64 + W * 16
+    f32 = ds._options(1e-3, None, 100, 1, "active", ds.F_GUARD | ds.F_FAST32, 1)
+    f0 = ds._options(1e-3, None, 100, 1, "active", ds.F_FAST32, 1)
+    rb32 = 8192 // 32                 # float32 matrix-core kernel: 32-row blocks
+    assert _bytes(big, f32)[1] - _bytes(big, f0)[1] == W * rb32 * 32 + W * 16
     assert _bytes(_problem(W=2, n_max=9000, m_max=100, d=3), opg)[0] == 4
     assert _bytes(_problem(W=2, n_max=9000, m_max=100, d=3), op)[0] == 0
 

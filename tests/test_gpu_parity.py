@@ -9,7 +9,8 @@ import pytest
 
 import oracle
 from paper_2607_24741_amd import workloads as wl
-from tests.gpu_support import EXEMPT_BAND, FP32_BAND, compare, log, procs, run_gpu, run_oracle
+from tests.gpu_support import (EXEMPT_BAND, FP32_BAND, RES_ATOL, compare, export_rounding_bound, log,
+                               procs, run_gpu, run_oracle)
 
 pytestmark = pytest.mark.gpu
 
@@ -21,13 +22,11 @@ FP32_FLAGS = F_FAST32 | F_FORCE_VALU | F_FORCE_MFMA | F_MATERIALIZE
 
 
 def band_for(flags, d):
-    """Depth-decision band: the contract's 1e-6 on the default path, FP32_BAND
-    for the opt-in float32 kernels (and for the float32 matrix-core default of
-    16 < d <= 32, where no float64-state kernel exists), and the guarded
-    release's residual bar for DS_F_GUARD, which decides on the rounded
-    float32 potentials it returns, not on the iterate."""
-    if flags & F_GUARD:
-        return GUARD_RES_ATOL
+    """Depth-decision band of the iterate: the contract's 1e-6 on the default
+    path, FP32_BAND for the opt-in float32 kernels (and for the float32
+    matrix-core default of 16 < d <= 32, where no float64-state kernel
+    exists). Guarded release adds each lane's export_rounding_bound() (see
+    guard_bars)."""
     if flags & FP32_FLAGS:
         return FP32_BAND
     if 16 < d <= 32 and not flags & F_PRECISE:
@@ -35,13 +34,25 @@ def band_for(flags, d):
     return EXEMPT_BAND
 
 
-def _case(name, w, tol, flags=0, res_atol=None, **kw):
+def guard_bars(w, g, flags):
+    """Per-lane depth band and residual bar of a guarded run: the iterate's
+    own (band_for, RES_ATOL) plus how far rounding to the returned float32
+    potentials can move the residual the guard decides on and reports."""
+    extra = np.array([export_rounding_bound(w, g, t) for t in range(w.W)])
+    log(f"[case] guarded: export rounding bound per lane max {extra.max():.2e} "
+        f"median {np.median(extra):.2e}")
+    return band_for(flags, w.d) + extra, RES_ATOL + extra
+
+
+def _case(name, w, tol, flags=0, **kw):
     band = band_for(flags, w.d)
     log(f"[case] {name}: W={w.W} n_max={w.X.shape[1]} m_max={w.Y.shape[1]} d={w.d} tol={tol} "
         f"flags={flags} band={band:.0e} {kw}")
     g = run_gpu(w, tol, flags=flags, **kw)
     o = run_oracle(w, tol, **{k: v for k, v in kw.items() if k in ("max_iter", "audit_every")})
-    extra = {} if res_atol is None else {"res_atol": res_atol}
+    extra = {}
+    if flags & F_GUARD:
+        band, extra["res_atol"] = guard_bars(w, g, flags)
     rep = compare(w, g, o, tol, audit_every=kw.get("audit_every", 1), band=band, **extra)
     log(f"[case] {name}: depths {g['depth'].tolist()} max_pot_err={rep['max_pot_err']:.2e} "
         f"max_res_err={rep['max_res_err']:.2e} near_threshold={rep['near_threshold']} "
@@ -463,15 +474,6 @@ def test_proposal_parity(flags):
     assert np.all(o["depth"][1:] <= cold["depth"][1:])
 
 
-# The guarded release reports the residual of the float32 potentials it returns.
-# Rounding the state to those float32 outputs moves the residual by up to about
-# |f| u / eps (~1e-5 on c2-shaped lanes) from that of the state the iteration
-# holds, so the comparison with the oracle's trajectory (its residual and the
-# decision band) takes 2e-5; the exact property -- reported residual = the
-# returned potentials' own float64 residual -- is checked by recomputation.
-GUARD_RES_ATOL = 2e-5
-
-
 def _certified(w, g, tol, lanes):
     """Recompute, in float64 on the host, both marginal residuals of exactly the
     float32 potentials the GPU returned (cost from the float32 coordinates): the
@@ -503,7 +505,7 @@ def test_guarded_release_certifies_returned_potentials(flags):
     the host in float64, equals the reported one to float32 rounding and meets
     tol for every converged lane (eq:release-contract)."""
     w = wl.make("c2", W=6, n=200, m=176)
-    g, o, rep = _case("c2-reduced-guard", w, 1e-2, flags=flags | F_GUARD, res_atol=GUARD_RES_ATOL)
+    g, o, rep = _case("c2-reduced-guard", w, 1e-2, flags=flags | F_GUARD)
     worst = _certified(w, g, 1e-2, range(w.W))
     log(f"[case] c2-reduced-guard: worst relative residual difference {worst:.2e}")
     assert g["stats"].check_pair_evals > 0
@@ -518,10 +520,54 @@ def test_guarded_release_mixed_shapes_and_final_audit():
     w.a[2] /= w.a[2].sum()
     w.b[7, 3] = 0.0
     w.b[7] /= w.b[7].sum()
-    g, o, rep = _case("c5-reduced-guard", w, 1e-3, flags=F_GUARD, res_atol=GUARD_RES_ATOL,
+    g, o, rep = _case("c5-reduced-guard", w, 1e-3, flags=F_GUARD,
                       max_iter=60, streams=2)
     assert np.any(g["status"] == oracle.MAX_ITER)
     _certified(w, g, 1e-3, range(w.W))
+
+
+def _guard_windows():
+    return {
+        "stress": (lambda: _stress_lanes(), 1e-3, dict(max_iter=3000)),
+        "telemetry": (lambda: wl.make("c3", W=4, n=160, m=224), 1e-2, dict(max_iter=4000)),
+        "mixture": (lambda: wl.make("c2", W=6, n=200, m=176), 1e-2, {}),
+        "lidar-final-audit": (lambda: wl.make("c5", W=12, n=400, m=380, hetero=(30, 400)), 1e-3,
+                              dict(max_iter=60, streams=2)),
+    }
+
+
+@pytest.mark.parametrize("name", ["stress", "telemetry", "mixture", "lidar-final-audit"])
+def test_guard_outward_bound_excludes_no_ready_lane(name):
+    """Guarded release with the float64 state verifies only the lanes whose
+    row residual the outward bound cannot place above tol (Sec. 5.4, C10
+    finite-precision stress). The same solve in shadow mode verifies the row
+    marginal of every lane at every audit and counts the audits where the
+    bound had excluded a lane whose verified row residual met tol: none. The
+    gate changes no decision (bitwise equal outputs), saves verifications, and
+    the decisions agree with the oracle's up to each lane's derived band."""
+    make, tol, kw = _guard_windows()[name]
+    w = make()
+    log(f"[case] guard bound {name}: guarded, then guarded + shadow")
+    g = run_gpu(w, tol, flags=F_GUARD, **kw)
+    h = run_gpu(w, tol, flags=F_GUARD | F_SHADOW, **kw)
+    st, sh = g["stats"], h["stats"]
+    log(f"[case] guard bound {name}: verified rows {st.screen_positive} of {sh.screen_positive} "
+        f"audited, check pairs {st.check_pair_evals:.3e} vs {sh.check_pair_evals:.3e}, "
+        f"excluded-but-ready {sh.guard_missed}")
+    assert sh.guard_missed == 0
+    for k in ("f", "g", "residual"):
+        assert np.array_equal(g[k], h[k], equal_nan=True), k
+    for k in ("depth", "status", "order"):
+        assert np.array_equal(g[k], h[k]), k
+    assert st.screen_positive < sh.screen_positive
+    assert st.check_pair_evals < sh.check_pair_evals
+    o = run_oracle(w, tol, **{k: v for k, v in kw.items() if k == "max_iter"})
+    band, res_atol = guard_bars(w, g, 0)
+    rep = compare(w, g, o, tol, band=band, res_atol=res_atol)
+    differ = int((g["depth"] != o["depth"]).sum() + (g["status"] != o["status"]).sum())
+    log(f"[case] guard bound {name}: decisions differing from the oracle {differ}/{w.W}, each "
+        f"within its lane's band: {rep['near_threshold']}")
+    _certified(w, g, tol, range(w.W))
 
 
 @pytest.mark.parametrize("k", range(24))
@@ -532,8 +578,7 @@ def test_randomised_windows(k):
     materialised / guarded paths, 0-2 sub-batches) against the oracle."""
     w, opt = wl.random_window(k)
     flags, streams = opt["flags"], opt["streams"]
-    res_atol = GUARD_RES_ATOL if flags == F_GUARD else None
-    g, o, rep = _case(f"random{k}", w, opt["tol"], flags=flags, res_atol=res_atol,
+    g, o, rep = _case(f"random{k}", w, opt["tol"], flags=flags,
                       audit_every=opt["audit_every"], max_iter=w.max_iter, streams=streams)
     assert np.all(g["status"] == oracle.CONVERGED)
     if flags == F_GUARD:
