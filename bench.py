@@ -375,6 +375,8 @@ def main():
     ap.add_argument("--matrix-free", action="store_true",
                     help="d > 32: K-looped matrix-core half-step (DS_F_MATRIX_FREE)")
     ap.add_argument("--guard", action="store_true", help="guarded release (DS_F_GUARD)")
+    ap.add_argument("--points", type=int, default=None,
+                    help="override the window's points per side (n = m); the same recipe")
     ap.add_argument("--no-tol-sweep", action="store_true",
                     help="skip the mixture window's modes and tolerance sweep")
     args = ap.parse_args()
@@ -393,7 +395,8 @@ def main():
     from paper_2607_24741_amd import workloads as wl
 
     dev = torch.device("cuda:0")
-    w = wl.make(args.config)
+    w = wl.make(args.config) if args.points is None else wl.make(args.config, n=args.points,
+                                                                  m=args.points)
     t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(dev)
     X, Y, a, b, eps, n, m = (t(w.X), t(w.Y), t(w.a), t(w.b), t(w.eps), t(w.n), t(w.m))
     base_flags = ((ds.F_FAST32 if args.fast32 else 0) | (ds.F_FORCE_VALU if args.force_valu else 0)
@@ -441,7 +444,8 @@ def main():
         "config": {"workload": wl.DESCRIPTIONS[args.config], "name": args.config, "W": w.W,
                    "n": int(w.X.shape[1]), "m": int(w.Y.shape[1]), "d": w.d, "tol": args.tol,
                    "audit_every": 1, "mode": args.mode, "max_iter": w.max_iter,
-                   "sub_batches": stats[-1].sub_batches},
+                   "sub_batches": stats[-1].sub_batches,
+                   "points_override": args.points},
         "slots_per_step": slots // args.steps,
         "pair_evals_per_step": pairs // args.steps,
         "l_max": stats[-1].l_max,

@@ -96,7 +96,8 @@ enum {
   DS_F_MATERIALIZE = 32u, /* build the cost C (base-2 units, float32) once per call
                            in the workspace and stream it from HBM in every
                            half-step; the default for d > 32 when n_max, m_max
-                           <= 8192 (required here)                                */
+                           <= 16384 (required here; W n_max m_max 4 bytes of
+                           workspace)                                            */
   DS_F_GUARD = 64u,     /* guarded release (eq:release-contract in float64): the
                            release is decided on a float64 evaluation of both
                            marginals of exactly the float32 potentials the caller
@@ -110,11 +111,11 @@ enum {
                            a float32 state every audited lane is verified. The
                            column marginal is evaluated only for lanes whose row
                            residual met tol. Two extra launches per audit cycle;
-                           n_max, m_max <= 8192.                                 */
+                           n_max, m_max <= 16384.                                */
   DS_F_MATRIX_FREE = 256u, /* d > 32: recompute the cost per tile on the matrix
                            cores (a K-looped contraction over d) instead of
                            materialising it; the default when a side has more
-                           than 8192 points. Float32 state. Exclusive with
+                           than 16384 points. Float32 state. Exclusive with
                            DS_F_MATERIALIZE.                                     */
   DS_F_FAST32 = 128u    /* float32 state on the matrix-core kernels for d <= 16:
                            about 1.5-2.5x faster, but float32 rounding of the

@@ -49,7 +49,7 @@ constexpr int kMaxParts = 4;   // concurrent sub-batches of one call
 
 bool uses_mfma(const ds_problem* pr, const ds_options* op);
 // d > 32: the materialised cost (4 bytes per term from HBM) unless a side has
-// more than 8192 points or DS_F_MATRIX_FREE asks for the K-looped matrix-core
+// more than 16384 points or DS_F_MATRIX_FREE asks for the K-looped matrix-core
 // half-step, which recomputes x~ . y~ per tile.
 bool uses_mfree(const ds_problem* pr, const ds_options* op) {
   if (pr->d <= ds::kMaxDSmall || (op->flags & DS_F_MATERIALIZE)) return false;
@@ -161,10 +161,10 @@ ds_err check_problem(const ds_problem* pr, const ds_options* op) {
       return fail(DS_E_UNSUPPORTED, "the materialised cost (d > 32 or DS_F_MATERIALIZE) runs "
                                     "in float32 with its own kernels: no PRECISE / FAST32 / FORCE flags");
     if (pr->n_max > ds::kMatMaxPts || pr->m_max > ds::kMatMaxPts)
-      return fail(DS_E_UNSUPPORTED, "the materialised cost supports at most 8192 points per side");
+      return fail(DS_E_UNSUPPORTED, "the materialised cost supports at most 16384 points per side");
   }
   if ((op->flags & DS_F_GUARD) && (pr->n_max > ds::kMatMaxPts || pr->m_max > ds::kMatMaxPts))
-    return fail(DS_E_UNSUPPORTED, "guarded release (DS_F_GUARD) supports at most 8192 points per side");
+    return fail(DS_E_UNSUPPORTED, "guarded release (DS_F_GUARD) supports at most 16384 points per side");
   if (!(op->tol > 0.f) || !std::isfinite(op->tol)) return fail(DS_E_INVALID, "tol must be finite and > 0");
   if (op->max_iter < 1) return fail(DS_E_INVALID, "max_iter must be >= 1");
   if (op->audit_every < 1) return fail(DS_E_INVALID, "audit_every must be >= 1");

@@ -46,7 +46,7 @@ constexpr int kRowsMfmaK = 128;  // rows per work item, matrix-free large-d kern
 constexpr int kMaxW = 4096;
 constexpr int kMaxDSmall = 32;   // matrix-free kernels
 constexpr int kMaxDF64 = 16;     // matrix-free float64-state kernels
-constexpr int kMatMaxPts = 8192; // materialised cost: points per lane side (LDS staging)
+constexpr int kMatMaxPts = 16384; // materialised cost: points per lane side (LDS staging, 64 KB)
 constexpr float kFastRange = 64.f;  // max spread of the bound (log2 units) for anchored sums
 // The same for the float64 state: there the anchored exponent (at most this
 // far above the true row maximum) is rounded once to float32 for v_exp_f32,

@@ -1365,7 +1365,7 @@ __global__ __launch_bounds__(256) void k_cost(CostArgs c) {
 // item, its lanes striding over the columns four at a time.
 __global__ __launch_bounds__(512, 2) void k_mat_rows(Launch L) {
   note_progress(L);
-  __shared__ __align__(16) float sh_gam[kMatMaxPts];
+  extern __shared__ __align__(16) float sh_gam[];   // the lane's column operand (padc floats)
   __shared__ float2 sh_row[kRowsValu];
   const int b = blockIdx.x;
   const int pi = b >= L.nb0;
@@ -1457,7 +1457,7 @@ __global__ __launch_bounds__(512, 2) void k_mat_rows(Launch L) {
 // chunks, merged per lane in chunk order.
 __global__ __launch_bounds__(512, 2) void k_mat_cols(Launch L) {
   note_progress(L);
-  __shared__ float sh_gam[kMatMaxPts];
+  extern __shared__ __align__(16) float sh_gam[];   // the lane's column operand (padc floats)
   __shared__ float2 sh_part[8][kRowsValu];
   const int b = blockIdx.x;
   const int pi = b >= L.nb0;
@@ -2352,10 +2352,22 @@ hipError_t launch_update_f64(const Launch& a, int d, int variant, int blocks, hi
 hipError_t launch_update_mat(const Launch& a, int blocks, hipStream_t st, hipEvent_t e0,
                              hipEvent_t e1) {
   if (blocks <= 0) return hipSuccess;
+  // the column operand of a lane is staged whole in LDS: padc floats (both
+  // passes of a launch have the same role, so the same padc), sized per call
+  // so that short lanes keep more blocks per CU
+  const size_t lds = (size_t)a.p[0].padc * sizeof(float);
+  if (a.p[0].padc > kMatMaxPts) return hipErrorInvalidValue;
+  static std::once_flag once;
+  std::call_once(once, [] {
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k_mat_rows),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, kMatMaxPts * 4);
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k_mat_cols),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, kMatMaxPts * 4);
+  });
   if (a.p[0].role == 0)
-    hipExtLaunchKernelGGL(k_mat_rows, dim3(blocks), dim3(512), 0, st, e0, e1, 0, a);
+    hipExtLaunchKernelGGL(k_mat_rows, dim3(blocks), dim3(512), lds, st, e0, e1, 0, a);
   else
-    hipExtLaunchKernelGGL(k_mat_cols, dim3(blocks), dim3(512), 0, st, e0, e1, 0, a);
+    hipExtLaunchKernelGGL(k_mat_cols, dim3(blocks), dim3(512), lds, st, e0, e1, 0, a);
   return hipGetLastError();
 }
 hipError_t launch_check64(const Launch& a, const GuardArgs& g, int blocks, hipStream_t st) {

@@ -89,7 +89,7 @@ def test_precise_state_default_validation_and_size():
 def test_materialised_cost_validation_and_size():
     """d > 32 selects the materialised cost: the workspace holds W n_pad m_pad
     floats of cost; the float64 state and forced kernels are refused for it.
-    More than 8192 points on a side (or DS_F_MATRIX_FREE) selects the
+    More than 16384 points on a side (or DS_F_MATRIX_FREE) selects the
     matrix-free large-d half-step instead."""
     op = ds._options(1e-3, None, 100, 1, "active", 0)
     code, n512 = _bytes(_problem(W=2, n_max=256, m_max=200, d=512), op)
@@ -100,12 +100,15 @@ def test_materialised_cost_validation_and_size():
     for fl in (ds.F_PRECISE, ds.F_FAST32, ds.F_FORCE_VALU, ds.F_FORCE_MFMA):
         o = ds._options(1e-3, None, 100, 1, "active", fl)
         assert _bytes(_problem(d=64), o)[0] == 4
-    # a side beyond 8192 points cannot be materialised: the matrix-free large-d
+    # a side beyond 16384 points cannot be materialised: the matrix-free large-d
     # half-step takes it (no cost matrix in the workspace); forcing the
     # materialised cost there is refused, and the two flags are exclusive
-    code, nfree = _bytes(_problem(W=2, n_max=9000, m_max=200, d=64), op)
-    assert code == 0 and nfree < 2 * 9000 * 200 * 4
-    assert _bytes(_problem(n_max=9000, d=64), opm)[0] == 4
+    code, nfree = _bytes(_problem(W=2, n_max=17000, m_max=200, d=64), op)
+    assert code == 0 and nfree < 2 * 17000 * 200 * 4
+    assert _bytes(_problem(n_max=17000, d=64), opm)[0] == 4
+    # up to 16384 a side is materialised (its column operand staged in 64 KB of LDS)
+    code, n16k = _bytes(_problem(W=2, n_max=16384, m_max=200, d=64), op)
+    assert code == 0 and n16k >= 2 * 16384 * 256 * 4
     opf = ds._options(1e-3, None, 100, 1, "active", ds.F_MATRIX_FREE)
     code, nf = _bytes(_problem(W=2, n_max=256, m_max=200, d=512), opf)
     # point records (2 banks x 2 sides x W x 256 padded points x 512 floats), no cost
@@ -171,7 +174,7 @@ def test_guarded_release_validation_and_size():
     """DS_F_GUARD keeps two float64 partials per row block and lane and one
     row certificate per lane; with the float64 state also the export-rounding
     sums of both sides per row block and lane (the outward bound), which a
-    float32 state does not have. At most 8192 points per side."""
+    float32 state does not have. At most 16384 points per side."""
     op = ds._options(1e-3, None, 100, 1, "active", 0, 1)
     opg = ds._options(1e-3, None, 100, 1, "active", ds.F_GUARD, 1)
     code, n0 = _bytes(_problem(W=4, n_max=256, m_max=256, d=8), op)
@@ -188,8 +191,8 @@ def test_guarded_release_validation_and_size():
     f0 = ds._options(1e-3, None, 100, 1, "active", ds.F_FAST32, 1)
     rb32 = 8192 // 32                 # float32 matrix-core kernel: 32-row blocks
     assert _bytes(big, f32)[1] - _bytes(big, f0)[1] == W * rb32 * 32 + W * 16
-    assert _bytes(_problem(W=2, n_max=9000, m_max=100, d=3), opg)[0] == 4
-    assert _bytes(_problem(W=2, n_max=9000, m_max=100, d=3), op)[0] == 0
+    assert _bytes(_problem(W=2, n_max=17000, m_max=100, d=3), opg)[0] == 4
+    assert _bytes(_problem(W=2, n_max=17000, m_max=100, d=3), op)[0] == 0
 
 
 def test_caller_outputs_are_validated():

@@ -131,14 +131,13 @@ def test_matrix_free_large_d_reduced_ragged():
     _case("c4-reduced-matrix-free", w, 1e-3, flags=F_MATRIX_FREE)
 
 
-def test_large_d_beyond_the_materialised_limit():
-    """At d > 32 a side with more than 8192 points cannot be materialised: the
-    default is then the matrix-free half-step (here d = 40, one lane with 9000
-    source points and one with 8300 target points)."""
-    rng = np.random.default_rng(17)
-    W, n_max, m_max, d = 2, 9000, 8300, 40
-    n = np.array([9000, 300], np.int32)
-    m = np.array([200, 8300], np.int32)
+def _wide_large_d(n, m, seed):
+    """Two d = 40 lanes, one with many source points and one with many target
+    points (a long column operand for each half-step)."""
+    rng = np.random.default_rng(seed)
+    W, d = 2, 40
+    n, m = np.array(n, np.int32), np.array(m, np.int32)
+    n_max, m_max = int(n.max()), int(m.max())
     X = np.full((W, n_max, d), np.nan, np.float32)
     Y = np.full((W, m_max, d), np.nan, np.float32)
     a = np.full((W, n_max), np.nan, np.float32)
@@ -149,8 +148,23 @@ def test_large_d_beyond_the_materialised_limit():
         aa = rng.gamma(1.0, size=n[t]); a[t, :n[t]] = aa / aa.sum()
         bb = rng.gamma(1.0, size=m[t]); b[t, :m[t]] = bb / bb.sum()
     eps = np.array([0.1, 0.15], np.float32)
-    w = wl.Workload("large-d-wide", X, Y, a, b, eps, n, m, 1e-3, 5000)
-    _case("large-d beyond 8192 points", w, 1e-3)
+    return wl.Workload("large-d-wide", X, Y, a, b, eps, n, m, 1e-3, 5000)
+
+
+def test_large_d_beyond_the_materialised_limit():
+    """At d > 32 a side with more than 16384 points cannot be materialised:
+    the default is then the matrix-free half-step (d = 40, one lane with 16500
+    source points and one with 16400 target points)."""
+    w = _wide_large_d([16500, 300], [200, 16400], 17)
+    _case("large-d beyond 16384 points", w, 1e-3)
+
+
+def test_materialised_cost_long_column_operand():
+    """The materialised cost with a column operand beyond 8192 points (staged
+    whole in LDS, up to 16384): d = 40, one lane with 12000 source points and
+    one with 9000 target points."""
+    w = _wide_large_d([12000, 300], [200, 9000], 19)
+    _case("materialised, 9000-12000 points a side", w, 1e-3)
 
 
 @pytest.mark.parametrize("name", ["c2", "c5"])
