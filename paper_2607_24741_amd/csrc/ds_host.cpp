@@ -135,6 +135,10 @@ ds::Layout plan(const ds_problem* pr, const ds_options* op, void* ws) {
     L.gerr[side] = (L.guard && L.es == 2) ? c.take<float4>(W * (size_t)L.rbmax) : nullptr;
   }
   L.row64 = L.guard ? c.take<ds::RowCert>(W) : nullptr;
+  // float64 state: partials and arrival words of the split (narrow) launches
+  L.spart = L.es == 2 ? c.take<double2>((size_t)ds::kSplitSlots * ds::kGroups * (size_t)L.rows)
+                      : nullptr;
+  L.scnt = L.es == 2 ? c.take<int>(2 * (size_t)ds::kSplitSlots) : nullptr;
   L.bytes = align_up(c.off, 256);
   return L;
 }
@@ -332,6 +336,7 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
   ia.mat = mat ? 1 : 0;
   ia.ctrl = L.ctrl;
   HIP_TRY(launch_ingest(ia, maxpad, st));
+  if (L.scnt) HIP_TRY(launch_zero_counters(L.scnt, 2 * kSplitSlots, st));
   HIP_TRY(launch_offsets(L.bank[0].slot, W, L.rows, L.off[0], L.off[1], L.ctrl, st));
   Ctrl ctrl;
   HIP_TRY(hipMemcpyAsync(&ctrl, L.ctrl, sizeof(Ctrl), hipMemcpyDeviceToHost, st));
@@ -423,6 +428,7 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
     l.hsnap = R->snap_dev; l.nchk = L.nchk; l.disc = L.disc;
     l.progress = &R->snap_dev->progress;
     l.Q = L.Q; l.q_lane = (size_t)L.pad[0] * L.pad[1]; l.q_ld = L.pad[1];
+    l.spart = L.spart; l.scnt = L.scnt;
     return l;
   };
   // DS_F_TIMING: both launches of every kSampleEvery-th cycle (and the final
@@ -446,6 +452,16 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
   }
   auto pick = [&](int items, int role) -> int {
     if (mat) return VAR_MEDIUM;   // one layout: 64-row items, one block each
+    // float64 state: few items get one wave per (item, sub-group). The split
+    // shortens every sweep from tpg tiles to about tpg / 4 but adds a round
+    // trip of the group partials through memory and more blocks per item, so
+    // it pays at more items the longer the groups are (measured: up to 64
+    // items with 2 tiles per group, 128 with 4, 256 with 32)
+    if (precise) {
+      const int tg = tpg[role];
+      if ((tg >= 16 && items <= 256) || (tg >= 4 && items <= 128) || (tg >= 2 && items <= 64))
+        return VAR_SPLIT;
+    }
     // (the float64 kernel's items hold 64 to 256 rows: fewer items per width)
     const int medium = use_mfma ? kMediumItemsMfma * kRowsMfma / L.rows
                                 : kMediumItemsValu * kRowsValu / L.rows;

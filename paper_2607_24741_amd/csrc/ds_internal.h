@@ -40,6 +40,15 @@ namespace ds {
 constexpr int kPad = 128;        // point padding of every lane-indexed array
 constexpr int kColTile = 32;     // columns per MFMA tile
 constexpr int kGroups = 8;       // fixed column groups of a lane (whole tiles each)
+// Float64-state kernel: each group is cut into kSubGroups fixed sub-groups of
+// whole tiles, each summed from a fresh accumulator and folded into the group
+// in order, so that a narrow launch can give every (work item, sub-group) a
+// wave of its own (k_update_f64_split, one block per group) with the same bits.
+constexpr int kSubGroups = 4;
+// most work items of one pass of a split launch; a launch holds at most two
+// passes, and its partials (in the workspace) are sized for both
+constexpr int kSplitItems = 256;
+constexpr int kSplitSlots = 2 * kSplitItems;
 constexpr int kRowsMfma = 32;    // rows per work item, matrix-core kernel
 constexpr int kRowsValu = 64;    // rows per work item, vector-ALU kernel
 constexpr int kRowsMfmaK = 128;  // rows per work item, matrix-free large-d kernel
@@ -168,6 +177,8 @@ struct Layout {
                      // [W][rbmax] {sum of mass x export rounding, max export rounding,
                      // sum of mass, 0} of each side's potentials (else null)
   RowCert* row64;    // guarded release: [W] latest verified row residual by caller lane
+  double2* spart;    // float64 state: split-launch partials (see Launch::spart)
+  int* scnt;         // float64 state: split-launch arrival counters
   int guard;
   size_t bytes;
 };
@@ -230,6 +241,9 @@ struct Launch {
   int q_ld;                       // row stride of Q (padded target count)
   int* progress;                  // &hsnap->progress as the device addresses it (may be null)
   int seqno;                      // launch sequence number written there
+  double2* spart;                 // split float64 launch: group partials
+                                  // [kSplitSlots][kGroups][rows]
+  int* scnt;                      // and per item [arrivals, skipped] [kSplitSlots][2], zero between launches
 };
 
 // Extra arguments of the float64 verification launch (guarded release), per
@@ -296,8 +310,10 @@ struct IngestArgs {
 // over waves. All variants compute identical bits; the host picks one by width.
 enum { VAR_NARROW = 0,   // 32-row items, one group per wave (8 waves)
        VAR_MEDIUM = 1,   // 32-row items, two groups per wave (4 waves)
-       VAR_MEDIUM4 = 3 };  // 32-row items, four groups per wave (2 waves): matrix-core
-                           // kernel, lanes of at most 2 column tiles per group
+       VAR_MEDIUM4 = 3,  // 32-row items, four groups per wave (2 waves): matrix-core
+                         // kernel, lanes of at most 2 column tiles per group
+       VAR_SPLIT = 4 };  // float64 kernel: a block per (item, group), a wave per sub-group, at most
+                         // kSplitItems items per pass
 // e0 / e1 (may be null): events that record the kernel's own start and end
 hipError_t launch_update(const Launch& a, int d, bool use_mfma, int variant, int blocks,
                          hipStream_t st, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);

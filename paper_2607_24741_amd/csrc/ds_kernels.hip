@@ -1081,14 +1081,180 @@ __device__ __forceinline__ double potential_f64(double gam, double nrm, double k
 template <int D>
 constexpr int f64_waves_per_simd() { return D <= 4 ? 4 : (D <= 7 ? 3 : (D <= 12 ? 2 : 3)); }
 
+// One 32-column tile of the float64 half-step for R rows per lane (the tile in
+// LDS at `cur`, column stride DG, the column operand in slot D). Anchored sums
+// add the tile's float32 sums in float64; otherwise a streaming maximum and a
+// rescaled sum over steps of four columns.
+template <int D, int R, int DG>
+__device__ __forceinline__ void f64_tile(const double* cur, const double (&xr)[R][D],
+                                         const double (&bias)[R], bool fast, double (&mrun)[R],
+                                         double (&srun)[R]) {
+  if (fast) {
+    // CV columns per step (one at large D, where the column values of two
+    // steps would not fit in registers beside the rows')
+    constexpr int CV = D <= 8 ? 2 : 1;
+    float tacc[R][2];
+#pragma unroll
+    for (int r = 0; r < R; ++r) tacc[r][0] = tacc[r][1] = 0.f;
+    for (int c = 0; c < kColTile; c += 2) {
+#pragma unroll CV
+      for (int v = 0; v < 2; ++v) {
+        double cj[D + 1];
+#pragma unroll
+        for (int k = 0; k <= D; ++k) cj[k] = cur[(c + v) * DG + k];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          double z = cj[D] + bias[r];
+#pragma unroll
+          for (int k = 0; k < D; ++k) z = fma(xr[r][k], cj[k], z);
+          tacc[r][v] += ex2((float)z);
+        }
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) srun[r] += (double)(tacc[r][0] + tacc[r][1]);
+  } else {
+    for (int c = 0; c < kColTile; c += 4) {
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        double z[4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const double* cj = cur + (c + v) * DG;
+          double zz = cj[D] + bias[r];
+#pragma unroll
+          for (int k = 0; k < D; ++k) zz = fma(xr[r][k], cj[k], zz);
+          z[v] = zz;
+        }
+        const double tm = fmax(fmax(z[0], z[1]), fmax(z[2], z[3]));
+        const double mn = fmax(mrun[r], tm);
+        const double mref = (mn == -(double)INFINITY) ? 0.0 : mn;
+        const double ts =
+            ((double)ex2((float)(z[0] - mref)) + (double)ex2((float)(z[1] - mref))) +
+            ((double)ex2((float)(z[2] - mref)) + (double)ex2((float)(z[3] - mref)));
+        srun[r] = fma(srun[r], (double)ex2((float)(mrun[r] - mref)), ts);
+        mrun[r] = mn;
+      }
+    }
+  }
+}
+
+// Fold of a sub-group partial (m, s) into its group's (gm, gs), in sub-group
+// order: the streaming merge used across tiles. The empty partial (-inf, 0) --
+// (0, 0) with anchored sums -- leaves (gm, gs) bit for bit unchanged, and the
+// first fold from the empty state returns the partial itself.
+__device__ __forceinline__ void f64_fold(double& gm, double& gs, double m, double s, bool fast) {
+  if (fast) {
+    gs += s;
+    return;
+  }
+  const double mn = fmax(gm, m);
+  const double ref = (mn == -(double)INFINITY) ? 0.0 : mn;
+  gs = fma(gs, (double)ex2((float)(gm - ref)), s * (double)ex2((float)(m - ref)));
+  gm = mn;
+}
+
+// Merge of a row's kGroups group partials in group order: (Mt, St) with
+// St * 2^Mt the row's sum.
+__device__ __forceinline__ void f64_merge(const double (&gm)[kGroups], const double (&gs)[kGroups],
+                                          double& Mt, double& St) {
+  double mx = -(double)INFINITY;
+#pragma unroll
+  for (int g = 0; g < kGroups; ++g) mx = fmax(mx, gm[g]);
+  Mt = (mx == -(double)INFINITY) ? 0.0 : mx;
+  St = 0.0;
+#pragma unroll
+  for (int g = 0; g < kGroups; ++g) St = fma(gs[g], (double)ex2((float)(gm[g] - Mt)), St);
+}
+
+// Guarded release: how far rounding to the float32 outputs moves the potentials
+// of an item's rows -- of the input state in the f-half (its column operand is
+// lm - lse_old, bit for bit what that state's f-half stored), of the new state
+// in the g-half (gnew). Per item {sum of mass x |rounding|, max |rounding|, sum
+// of mass} over the points with mass; each |rounding| also covers the float64
+// evaluation of the potential (a few units of 2^-53 of its terms). Wave 0.
+template <int D, int R>
+__device__ __forceinline__ void f64_export_rounding(const Launch& L, const Pass& P,
+                                                    const SlotInfo& si, int rb,
+                                                    const bool (&owner)[R], const float (&w)[R],
+                                                    const double (&lm)[R],
+                                                    const double (&lse_old)[R],
+                                                    const double (&gnew)[R],
+                                                    const double (&xr)[R][D]) {
+  float sd = 0.f, md = 0.f, sw = 0.f;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const double gq = P.role ? gnew[r] : lm[r] - lse_old[r];
+    if (!owner[r] || w[r] == 0.f || !(fabs(gq) < (double)INFINITY)) continue;
+    double nrm = 0.0;
+#pragma unroll
+    for (int k = 0; k < D; ++k) nrm = fma(xr[r][k], xr[r][k], nrm);
+    const double F = potential_f64(gq, nrm, si.kappa64);
+    const double dl = fabs((double)(float)F - F) + (fabs(gq) + 0.5 * nrm) * (0x1p-46 / si.kappa64);
+    sd += w[r] * (float)dl;
+    md = fmaxf(md, (float)dl);
+    sw += w[r];
+  }
+  const float4 v = make_float4(wave64(sd, OpAdd()), wave64(md, OpMax()), wave64(sw, OpAdd()), 0.f);
+  if ((threadIdx.x & 63) == 0) P.gerr_out[(size_t)si.lane * L.rbmax + rb] = v;
+}
+
+// Column tiles of a lane: ct tiles of 32 columns, kGroups groups of tpg tiles,
+// each cut into kSubGroups sub-groups of tps tiles (trailing ones may be empty).
+struct F64Tiling {
+  int ct, tpg, tps;
+  __device__ F64Tiling(int ncols) {
+    ct = (ncols + kColTile - 1) / kColTile;
+    tpg = (ct + kGroups - 1) / kGroups;
+    tps = (tpg + kSubGroups - 1) / kSubGroups;
+  }
+};
+
+// Stage tile t of the lane's column records and operand into an LDS buffer:
+// lane l moves double2 number q * 64 + l of a tile (clamped: the last lanes
+// of a partial round repeat an in-range element, harmlessly); double2 e of
+// the HBM tile is pair e % (DP / 2) of column e / (DP / 2), which lands at
+// double2 (e / (DP / 2)) * (DG / 2) + e % (DP / 2) of the LDS tile, and the
+// operand gam of column c at c * DG + D.
+template <int D>
+struct F64Stage {
+  static constexpr int DP = D + (D & 1);
+  static constexpr int DG = (D + 2) & ~1;
+  static constexpr int TREC = kColTile * DP;   // doubles of records per tile in HBM
+  static constexpr int NV2 = TREC / 2;         // double2 per tile
+  static constexpr int PER = (NV2 + 63) / 64;  // double2 per lane
+  static_assert(PER <= 4, "a float64 tile is at most 4 double2 per lane");
+  double2 pv[4];
+  double pg;
+  __device__ __forceinline__ void fetch(const double* rec_lane, const double* gam_lane, int t,
+                                        int lane) {
+    const double2* src = reinterpret_cast<const double2*>(rec_lane + (size_t)t * TREC);
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      pv[q] = q < PER ? src[min(q * 64 + lane, NV2 - 1)] : make_double2(0.0, 0.0);
+    pg = gam_lane[t * kColTile + (lane & (kColTile - 1))];
+  }
+  __device__ __forceinline__ void stash(double* dst, int lane) const {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (q < PER) {
+        const int e = min(q * 64 + lane, NV2 - 1);
+        reinterpret_cast<double2*>(dst)[(e / (DP / 2)) * (DG / 2) + e % (DP / 2)] = pv[q];
+      }
+    }
+    if (lane < kColTile) dst[lane * DG + D] = pg;
+    __builtin_amdgcn_wave_barrier();
+  }
+};
+
 template <int D, int GW>
 __global__ __launch_bounds__(64 * (kGroups / GW), (f64_waves_per_simd<D>()))
 void k_update_f64(Launch L) {
   note_progress(L);
   constexpr int ROWS = rows_f64(D);
   constexpr int R = ROWS / 64;
-  constexpr int DP = D + (D & 1);        // record stride in HBM (doubles)
-  constexpr int DG = (D + 2) & ~1;       // column stride in LDS: coordinates, gam, (pad)
+  constexpr int DP = F64Stage<D>::DP;    // record stride in HBM (doubles)
+  constexpr int DG = F64Stage<D>::DG;    // column stride in LDS: coordinates, gam, (pad)
   __shared__ double2 sh_part[kGroups][ROWS];
   __shared__ __align__(16) double sh_tile[kGroups / GW][2][kColTile * DG];
   const int b = blockIdx.x;
@@ -1144,118 +1310,54 @@ void k_update_f64(Launch L) {
     }
   }
 
-  const int ct = (ncols + kColTile - 1) / kColTile;
-  const int tpg = (ct + kGroups - 1) / kGroups;
-  constexpr int TREC = kColTile * DP;   // doubles of records per tile in HBM
-  constexpr int NV2 = TREC / 2;         // double2 per tile
-  constexpr int PER = (NV2 + 63) / 64;  // double2 per lane
-  static_assert(PER <= 4, "a float64 tile is at most 4 double2 per lane");
+  const F64Tiling T(ncols);
   double* buf0 = sh_tile[wave][0];
   double* buf1 = sh_tile[wave][1];
   const double* rec_lane = reinterpret_cast<const double*>(P.rec_col) + (size_t)s * P.padc * DP;
   const double* gam_lane = reinterpret_cast<const double*>(P.gam_col) + (size_t)s * P.padc;
-  // lane l moves double2 number q * 64 + l of a tile (clamped: the last lanes
-  // of a partial round repeat an in-range element, harmlessly); double2 e of
-  // the HBM tile is pair e % (DP / 2) of column e / (DP / 2), which lands at
-  // double2 (e / (DP / 2)) * (DG / 2) + e % (DP / 2) of the LDS tile
-#define DS_F64_LD(q) ((q) < PER ? src_[min((q) * 64 + lane, NV2 - 1)] : make_double2(0.0, 0.0))
-#define DS_F64_FETCH(t)                                                                    \
-  do {                                                                                     \
-    const double2* src_ = reinterpret_cast<const double2*>(rec_lane + (size_t)(t) * TREC); \
-    pv0 = DS_F64_LD(0); pv1 = DS_F64_LD(1); pv2 = DS_F64_LD(2); pv3 = DS_F64_LD(3);        \
-    pg = gam_lane[(t) * kColTile + (lane & (kColTile - 1))];                               \
-  } while (0)
-#define DS_F64_ST(q, v)                                                                    \
-  if ((q) < PER) {                                                                         \
-    const int e_ = min((q) * 64 + lane, NV2 - 1);                                          \
-    reinterpret_cast<double2*>(dst_)[(e_ / (DP / 2)) * (DG / 2) + e_ % (DP / 2)] = (v);    \
-  }
-#define DS_F64_STASH(dst)                                                                  \
-  do {                                                                                     \
-    double* dst_ = (dst);                                                                  \
-    DS_F64_ST(0, pv0); DS_F64_ST(1, pv1); DS_F64_ST(2, pv2); DS_F64_ST(3, pv3);             \
-    if (lane < kColTile) dst_[lane * DG + D] = pg;                                         \
-    __builtin_amdgcn_wave_barrier();                                                       \
-  } while (0)
+  const double m0 = fast ? 0.0 : -(double)INFINITY;
 #pragma unroll
   for (int u = 0; u < GW; ++u) {
     const int g = wave * GW + u;
-    const int tA = min(ct, g * tpg), tB = min(ct, g * tpg + tpg);
+    const int tA = min(T.ct, g * T.tpg), tB = min(T.ct, g * T.tpg + T.tpg);
+    // the group's running fold lives in the wave's own sh_part slots (only
+    // this wave touches them before the block barrier), not in registers
     double mrun[R], srun[R];
 #pragma unroll
-    for (int r = 0; r < R; ++r) { mrun[r] = fast ? 0.0 : -(double)INFINITY; srun[r] = 0.0; }
-    if (tA < tB) {
-      double2 pv0, pv1, pv2, pv3;
-      double pg;
-      DS_F64_FETCH(tA);
-      DS_F64_STASH(buf0);
+    for (int r = 0; r < R; ++r) {
+      mrun[r] = m0;
+      srun[r] = 0.0;
+      sh_part[g][64 * r + lane] = make_double2(m0, 0.0);
     }
+    F64Stage<D> st;
+    if (tA < tB) {
+      st.fetch(rec_lane, gam_lane, tA, lane);
+      st.stash(buf0, lane);
+    }
+    // tiles in order, the next one prefetched across sub-group boundaries;
+    // each sub-group's sums start afresh and are folded into the group's
+    int send = min(tB, tA + T.tps);
     for (int t = tA; t < tB; ++t) {
       const double* cur = ((t - tA) & 1) ? buf1 : buf0;
       double* nxt = ((t - tA) & 1) ? buf0 : buf1;
-      double2 pv0, pv1, pv2, pv3;
-      double pg = 0.0;
       const bool more = t + 1 < tB;
-      if (more) DS_F64_FETCH(t + 1);
-      if (fast) {
-        // CV columns per step (one at large D, where the column values of
-        // two steps would not fit in registers beside the rows')
-        constexpr int CV = D <= 8 ? 2 : 1;
-        float tacc[R][2];
-#pragma unroll
-        for (int r = 0; r < R; ++r) tacc[r][0] = tacc[r][1] = 0.f;
-        for (int c = 0; c < kColTile; c += 2) {
-#pragma unroll CV
-          for (int v = 0; v < 2; ++v) {
-            double cj[D + 1];
-#pragma unroll
-            for (int k = 0; k <= D; ++k) cj[k] = cur[(c + v) * DG + k];
-#pragma unroll
-            for (int r = 0; r < R; ++r) {
-              double z = cj[D] + bias[r];
-#pragma unroll
-              for (int k = 0; k < D; ++k) z = fma(xr[r][k], cj[k], z);
-              tacc[r][v] += ex2((float)z);
-            }
-          }
-        }
-#pragma unroll
-        for (int r = 0; r < R; ++r) srun[r] += (double)(tacc[r][0] + tacc[r][1]);
-      } else {
-        for (int c = 0; c < kColTile; c += 4) {
-#pragma unroll
-          for (int r = 0; r < R; ++r) {
-            double z[4];
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-              const double* cj = cur + (c + v) * DG;
-              double zz = cj[D] + bias[r];
-#pragma unroll
-              for (int k = 0; k < D; ++k) zz = fma(xr[r][k], cj[k], zz);
-              z[v] = zz;
-            }
-            const double tm = fmax(fmax(z[0], z[1]), fmax(z[2], z[3]));
-            const double mn = fmax(mrun[r], tm);
-            const double mref = (mn == -(double)INFINITY) ? 0.0 : mn;
-            const double ts =
-                ((double)ex2((float)(z[0] - mref)) + (double)ex2((float)(z[1] - mref))) +
-                ((double)ex2((float)(z[2] - mref)) + (double)ex2((float)(z[3] - mref)));
-            srun[r] = srun[r] * (double)ex2((float)(mrun[r] - mref)) + ts;
-            mrun[r] = mn;
-          }
-        }
-      }
+      if (more) st.fetch(rec_lane, gam_lane, t + 1, lane);
+      f64_tile<D, R, DG>(cur, xr, bias, fast, mrun, srun);
       __builtin_amdgcn_wave_barrier();
-      if (more) DS_F64_STASH(nxt);
-    }
+      if (more) st.stash(nxt, lane);
+      if (t + 1 == send) {
 #pragma unroll
-    for (int r = 0; r < R; ++r)
-      sh_part[g][64 * r + lane] = make_double2(mrun[r], srun[r]);   // (-inf, 0) if empty
+        for (int r = 0; r < R; ++r) {
+          double2 G = sh_part[g][64 * r + lane];
+          f64_fold(G.x, G.y, mrun[r], srun[r], fast);
+          sh_part[g][64 * r + lane] = G;
+          mrun[r] = m0;
+          srun[r] = 0.0;
+        }
+        send = min(tB, send + T.tps);
+      }
+    }
   }
-#undef DS_F64_FETCH
-#undef DS_F64_STASH
-#undef DS_F64_LD
-#undef DS_F64_ST
   __syncthreads();
   if (wave != 0) return;
   double Mt[R], St[R];
@@ -1264,13 +1366,13 @@ void k_update_f64(Launch L) {
     Mt[r] = 0.0;
     St[r] = 0.0;
     if (!owner[r]) continue;
-    double mx = -(double)INFINITY;
+    double pm[kGroups], ps[kGroups];
 #pragma unroll
-    for (int g = 0; g < kGroups; ++g) mx = fmax(mx, sh_part[g][64 * r + lane].x);
-    Mt[r] = (mx == -(double)INFINITY) ? 0.0 : mx;
-#pragma unroll
-    for (int g = 0; g < kGroups; ++g)
-      St[r] += sh_part[g][64 * r + lane].y * (double)ex2((float)(sh_part[g][64 * r + lane].x - Mt[r]));
+    for (int g = 0; g < kGroups; ++g) {
+      pm[g] = sh_part[g][64 * r + lane].x;
+      ps[g] = sh_part[g][64 * r + lane].y;
+    }
+    f64_merge(pm, ps, Mt[r], St[r]);
   }
   bool lo[R];
 #pragma unroll
@@ -1280,29 +1382,204 @@ void k_update_f64(Launch L) {
   for (int r = 0; r < R; ++r) gkeep[r] = -(double)INFINITY;
   finish_rows_r<ROWS, 1, R, double>(L, P, s, si, rb, owner, lo, fast, M, lse_old, lm, w, Mt, St,
                                     rhat, gkeep);
-  if (P.gerr_out == nullptr) return;
-  // Guarded release: how far rounding to the float32 outputs moves this item's
-  // potentials -- of the input state in the f-half (its column operand is
-  // lm - lse_old, bit for bit what that state's f-half stored), of the new
-  // state in the g-half. Per item {sum of mass x |rounding|, max |rounding|,
-  // sum of mass} over the points with mass; each |rounding| also covers the
-  // float64 evaluation of the potential (a few units of 2^-53 of its terms).
-  float sd = 0.f, md = 0.f, sw = 0.f;
+  if (P.gerr_out) f64_export_rounding<D, R>(L, P, si, rb, owner, w, lm, lse_old, gkeep, xr);
+}
+
+// device-scope (coherent) float64 store and load for the split launch's partials
+__device__ __forceinline__ void st_dev_d(double* p, double v) {
+  __hip_atomic_store(reinterpret_cast<unsigned long long*>(p),
+                     (unsigned long long)__double_as_longlong(v), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ double ld_dev_d(const double* p) {
+  return __longlong_as_double((long long)__hip_atomic_load(
+      reinterpret_cast<unsigned long long*>(const_cast<double*>(p)), __ATOMIC_RELAXED,
+      __HIP_MEMORY_SCOPE_AGENT));
+}
+
+// The float64 half-step for narrow launches: one block per (work item, group)
+// and in it one wave per sub-group, so a launch of few items still spreads
+// over the chip. Each wave sweeps its sub-group's tiles exactly as the wave of
+// k_update_f64 that owns the group does (same tiles, same order, same
+// accumulators); wave 0 folds the four sub-group partials in order and
+// publishes the group partial of every row of the item; the last of the
+// item's kGroups blocks to arrive merges the groups in group order and
+// finishes the item: the bits equal k_update_f64's.
+//
+// Arrival: every block of a placed item arrives exactly once, also one whose
+// waves found the item retired or the window finished (each wave reads that
+// on its own, so blocks of one item can disagree when a lane retires during
+// the launch): such a block marks the item skipped and the last arrival then
+// does not finish it. A check item whose lane the screen leaves unchecked (a
+// fact of the previous launch, the same for every block) is dropped by all of
+// its blocks before arriving. The last arrival clears both words for the next
+// launch.
+template <int D>
+__global__ __launch_bounds__(64 * kSubGroups, (f64_waves_per_simd<D>()))
+void k_update_f64_split(Launch L) {
+  note_progress(L);
+  constexpr int ROWS = rows_f64(D);
+  constexpr int R = ROWS / 64;
+  constexpr int DP = F64Stage<D>::DP;
+  constexpr int DG = F64Stage<D>::DG;
+  __shared__ __align__(16) double sh_tile[kSubGroups][2][kColTile * DG];
+  __shared__ double2 sh_sub[kSubGroups][ROWS];
+  __shared__ int sh_work[kSubGroups];
+  const int it = (int)(blockIdx.x / kGroups);   // work item of the launch (both passes)
+  const int g = (int)(blockIdx.x % kGroups);    // its group
+  const int pi = it >= L.nb0;
+  const Pass P = L.p[pi];
+  const int nitems = pi ? (int)(gridDim.x / kGroups) - L.nb0 : L.nb0;
+  int s, rb, nrows, ncols, c_fin, c_A;
+  SlotInfo si;
+  if (!place_item<1>(L, P, nitems, pi ? it - L.nb0 : it, s, rb, nrows, ncols, si, c_fin, c_A))
+    return;
+  const bool upd = P.kind == KIND_UPDATE;
+  float rhat = NAN;
+  bool work = true;
+  if (!upd) {
+    if (!check_facts(L, P, s, P.role ? ncols : nrows, rhat)) return;
+    work = item_live(L, P, s, si, c_fin, c_A);
+  }
+  const int lane = threadIdx.x & 63;
+  const int q = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // this wave's sub-group
+  double lse_old[R], xr[R][D];
+  bool in_prefix[R];
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    const double gq = P.role ? gkeep[r] : lm[r] - lse_old[r];
-    if (!owner[r] || w[r] == 0.f || !(fabs(gq) < (double)INFINITY)) continue;
-    double nrm = 0.0;
+    const int i = rb * ROWS + 64 * r + lane;
+    const size_t ridx = (size_t)s * P.padr + i;
+    lse_old[r] = reinterpret_cast<const double*>(P.lse_in)[ridx];
+    in_prefix[r] = i < nrows;
+    const double* rrow = reinterpret_cast<const double*>(P.rec_row) + ridx * DP;
 #pragma unroll
-    for (int k = 0; k < D; ++k) nrm = fma(xr[r][k], xr[r][k], nrm);
-    const double F = potential_f64(gq, nrm, si.kappa64);
-    const double dl = fabs((double)(float)F - F) + (fabs(gq) + 0.5 * nrm) * (0x1p-46 / si.kappa64);
-    sd += w[r] * (float)dl;
-    md = fmaxf(md, (float)dl);
-    sw += w[r];
+    for (int k = 0; k < D; ++k) xr[r][k] = rrow[k];
   }
-  const float4 v = make_float4(wave64(sd, OpAdd()), wave64(md, OpMax()), wave64(sw, OpAdd()), 0.f);
-  if (lane == 0) P.gerr_out[(size_t)si.lane * L.rbmax + rb] = v;
+  bool fast = false;
+  float M = 0.f;
+  if (upd) {
+    update_facts(L, P, s, ncols, fast, M, kFastRangePrecise);
+    work = item_live(L, P, s, si, c_fin, c_A);
+  }
+  bool live[R];
+  double bias[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    live[r] = in_prefix[r] && (lse_old[r] != (double)INFINITY);
+    bias[r] = 0.0;
+    if (live[r]) {
+      if (!upd) bias[r] = -lse_old[r];
+      else if (fast) bias[r] = -(lse_old[r] + (double)M);
+    }
+  }
+  const double m0 = fast ? 0.0 : -(double)INFINITY;
+  if (work) {
+    const F64Tiling T(ncols);
+    const int tA = min(T.ct, g * T.tpg), tB = min(T.ct, g * T.tpg + T.tpg);
+    const int sA = min(tB, tA + q * T.tps), sB = min(tB, sA + T.tps);
+    const double* rec_lane = reinterpret_cast<const double*>(P.rec_col) + (size_t)s * P.padc * DP;
+    const double* gam_lane = reinterpret_cast<const double*>(P.gam_col) + (size_t)s * P.padc;
+    double mrun[R], srun[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) { mrun[r] = m0; srun[r] = 0.0; }
+    F64Stage<D> st;
+    if (sA < sB) {
+      st.fetch(rec_lane, gam_lane, sA, lane);
+      st.stash(sh_tile[q][0], lane);
+    }
+    for (int t = sA; t < sB; ++t) {
+      const double* cur = sh_tile[q][(t - sA) & 1];
+      double* nxt = sh_tile[q][((t - sA) & 1) ^ 1];
+      const bool more = t + 1 < sB;
+      if (more) st.fetch(rec_lane, gam_lane, t + 1, lane);
+      f64_tile<D, R, DG>(cur, xr, bias, fast, mrun, srun);
+      __builtin_amdgcn_wave_barrier();
+      if (more) st.stash(nxt, lane);
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) sh_sub[q][64 * r + lane] = make_double2(mrun[r], srun[r]);
+  }
+  if (lane == 0) sh_work[q] = work ? 1 : 0;
+  __syncthreads();
+  if (q != 0) return;
+  bool all = true;
+#pragma unroll
+  for (int u = 0; u < kSubGroups; ++u) all = all && sh_work[u] != 0;
+  // the group partial of every row: the sub-groups folded in order
+  double2* part = L.spart + (size_t)it * kGroups * ROWS;
+  if (all) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      double gm = m0, gs = 0.0;
+#pragma unroll
+      for (int u = 0; u < kSubGroups; ++u) {
+        const double2 p = sh_sub[u][64 * r + lane];
+        f64_fold(gm, gs, p.x, p.y, fast);
+      }
+      double* dst = reinterpret_cast<double*>(part + (size_t)g * ROWS + 64 * r + lane);
+      st_dev_d(dst, gm);
+      st_dev_d(dst + 1, gs);
+    }
+  }
+  // arrival (the partials, or the skip mark, complete before it)
+  int last = 0, skipped = 0;
+  if (lane == 0) {
+    if (!all) atomicOr(&L.scnt[2 * it + 1], 1);
+    wait_mem();
+    const int prev = atomicAdd(&L.scnt[2 * it], 1);
+    last = prev + 1 == kGroups;
+    if (last) {
+      skipped = atomicExch(&L.scnt[2 * it + 1], 0);
+      atomicExch(&L.scnt[2 * it], 0);
+    }
+  } else {
+    wait_mem();
+  }
+  last = __builtin_amdgcn_readfirstlane(last);
+  skipped = __builtin_amdgcn_readfirstlane(skipped);
+  if (!last || skipped || !all) return;
+  // the item's finish, as wave 0 of k_update_f64 does it; every partial is
+  // loaded before the first is used
+  bool owner[R];
+  double lm[R];
+  float w[R];
+  double pm[R][kGroups], ps[R][kGroups];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+#pragma unroll
+    for (int u = 0; u < kGroups; ++u) {
+      const double* src = reinterpret_cast<const double*>(part + (size_t)u * ROWS + 64 * r + lane);
+      pm[r][u] = ld_dev_d(src);
+      ps[r][u] = ld_dev_d(src + 1);
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int i = rb * ROWS + 64 * r + lane;
+    owner[r] = in_prefix[r];
+    lm[r] = 0.0;
+    w[r] = 0.f;
+    if (owner[r]) {
+      lm[r] = reinterpret_cast<const double*>(P.lm_row)[(size_t)s * P.padr + i];
+      w[r] = P.w_row[(size_t)si.lane * P.w_ld + i];
+    }
+  }
+  double Mt[R], St[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    Mt[r] = 0.0;
+    St[r] = 0.0;
+    if (owner[r]) f64_merge(pm[r], ps[r], Mt[r], St[r]);
+  }
+  bool lo[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) lo[r] = live[r] && owner[r];
+  double gkeep[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) gkeep[r] = -(double)INFINITY;
+  finish_rows_r<ROWS, 1, R, double>(L, P, s, si, rb, owner, lo, fast, M, lse_old, lm, w, Mt, St,
+                                    rhat, gkeep);
+  if (P.gerr_out) f64_export_rounding<D, R>(L, P, si, rb, owner, w, lm, lse_old, gkeep, xr);
 }
 
 // ----------------------------------------------- materialised-cost half-steps
@@ -2254,10 +2531,18 @@ static hipError_t launch_valu_d(const Launch& a, int variant, int blocks, hipStr
 template <int D>
 static hipError_t launch_f64_d(const Launch& a, int variant, int blocks, hipStream_t st,
                                hipEvent_t e0, hipEvent_t e1) {
-  if (variant == VAR_NARROW)
+  if (variant == VAR_SPLIT) {
+    // `blocks` work items over both passes, one block per (item, group) and a
+    // wave per sub-group; the partials and arrival words of the workspace
+    // hold kSplitSlots items
+    if (blocks > kSplitSlots || a.spart == nullptr || a.scnt == nullptr) return hipErrorInvalidValue;
+    hipExtLaunchKernelGGL((k_update_f64_split<D>), dim3(blocks * kGroups), dim3(64 * kSubGroups), 0,
+                          st, e0, e1, 0, a);
+  } else if (variant == VAR_NARROW) {
     hipExtLaunchKernelGGL((k_update_f64<D, 1>), dim3(blocks), dim3(512), 0, st, e0, e1, 0, a);
-  else
+  } else {
     hipExtLaunchKernelGGL((k_update_f64<D, 2>), dim3(blocks), dim3(256), 0, st, e0, e1, 0, a);
+  }
   return hipGetLastError();
 }
 
