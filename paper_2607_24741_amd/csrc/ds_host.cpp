@@ -464,7 +464,8 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
     }
     // (the float64 kernel's items hold 64 to 256 rows: fewer items per width)
     const int medium = use_mfma ? kMediumItemsMfma * kRowsMfma / L.rows
-                                : kMediumItemsValu * kRowsValu / L.rows;
+                       : (precise && !uniform) ? kMediumItemsF64Mixed
+                                               : kMediumItemsValu * kRowsValu / L.rows;
     if (items < medium) return VAR_NARROW;
     return (use_mfma && tpg[role] <= 2) ? VAR_MEDIUM4 : VAR_MEDIUM;
   };

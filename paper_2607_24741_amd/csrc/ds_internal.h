@@ -67,6 +67,10 @@ constexpr int kMaxDevices = 64;
 // launch-variant thresholds (work items of the launch, see launch_update)
 constexpr int kMediumItemsMfma = 384;
 constexpr int kMediumItemsValu = 256;
+// float64 kernel, mixed lane shapes: eight short-sweep waves per block keep the
+// heterogeneous items balanced up to this many items (measured on LiDAR-shaped
+// lanes: 8-wave blocks faster up to 8.7k items, 4-wave blocks from 12.6k)
+constexpr int kMediumItemsF64Mixed = 10000;
 
 // Per physical slot lane descriptor; moved by compaction with the rest of the
 // lane-indexed state.
