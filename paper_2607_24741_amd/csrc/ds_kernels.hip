@@ -1076,8 +1076,10 @@ __device__ __forceinline__ double potential_f64(double gam, double nrm, double k
 // of each column -- the record's padding double when D is odd) and reads them
 // back as broadcasts. Only the wave itself touches its buffer, so no block
 // barrier is needed (a wave's LDS operations complete in order).
-// The second launch bound (minimum waves per SIMD) lets the allocator keep the
-// two rows' coordinates and the prefetched tile in registers without spilling.
+// The second launch bound (minimum waves per SIMD) sets the register budget.
+// Chosen per d by measurement: at d = 16 the wide variant spills a few
+// registers to scratch at three waves per SIMD and still runs faster than at
+// two without spills.
 template <int D>
 constexpr int f64_waves_per_simd() { return D <= 4 ? 4 : (D <= 7 ? 3 : (D <= 12 ? 2 : 3)); }
 
@@ -1089,15 +1091,14 @@ template <int D, int R, int DG>
 __device__ __forceinline__ void f64_tile(const double* cur, const double (&xr)[R][D],
                                          const double (&bias)[R], bool fast, double (&mrun)[R],
                                          double (&srun)[R]) {
-  if (fast) {
-    // CV columns per step (one at large D, where the column values of two
-    // steps would not fit in registers beside the rows')
-    constexpr int CV = D <= 8 ? 2 : 1;
+  // Anchored sums: even and odd columns of the tile in two float32 sums per
+  // row, added in float64 at the tile's end (the same order on both paths).
+  if (fast && D <= 4) {
     float tacc[R][2];
 #pragma unroll
     for (int r = 0; r < R; ++r) tacc[r][0] = tacc[r][1] = 0.f;
     for (int c = 0; c < kColTile; c += 2) {
-#pragma unroll CV
+#pragma unroll
       for (int v = 0; v < 2; ++v) {
         double cj[D + 1];
 #pragma unroll
@@ -1109,6 +1110,35 @@ __device__ __forceinline__ void f64_tile(const double* cur, const double (&xr)[R
           for (int k = 0; k < D; ++k) z = fma(xr[r][k], cj[k], z);
           tacc[r][v] += ex2((float)z);
         }
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) srun[r] += (double)(tacc[r][0] + tacc[r][1]);
+  } else if (fast) {
+    // d >= 5: the next column's values are read from LDS while the current
+    // column computes (software pipelining; the compiler alone waited on
+    // nearly every read at the occupancy these register counts allow)
+    float tacc[R][2];
+#pragma unroll
+    for (int r = 0; r < R; ++r) tacc[r][0] = tacc[r][1] = 0.f;
+    double cn[D + 1];
+#pragma unroll
+    for (int k = 0; k <= D; ++k) cn[k] = cur[k];
+#pragma unroll
+    for (int c = 0; c < kColTile; ++c) {
+      double cj[D + 1];
+#pragma unroll
+      for (int k = 0; k <= D; ++k) cj[k] = cn[k];
+      if (c + 1 < kColTile) {
+#pragma unroll
+        for (int k = 0; k <= D; ++k) cn[k] = cur[(c + 1) * DG + k];
+      }
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        double z = cj[D] + bias[r];
+#pragma unroll
+        for (int k = 0; k < D; ++k) z = fma(xr[r][k], cj[k], z);
+        tacc[r][c & 1] += ex2((float)z);
       }
     }
 #pragma unroll
