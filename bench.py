@@ -61,6 +61,7 @@ VALU_PEAK_TFLOPS = 78.6
 # issue (the published quarter rate, 9.8e12/s, is below what gfx950 was
 # measured to sustain, 1.83e13/s, so it would inflate the fraction).
 VECTOR_LANE_OPS_PEAK = VALU_PEAK_TFLOPS * 1e12 / 2.0
+MAT_MAX_POINTS = 16384   # points per side the materialised-cost kernels stage
 EXP_PEAK = 256 * 4 * 8 * 2.4e9
 
 
@@ -233,7 +234,10 @@ def roofline(w, args, stats, T, traffic_summary):
     ms_upd = sum(s.ms_update for s in stats)
     launches = sum(s.update_launches for s in stats)
     kept_pairs = sum(s.pair_evals for s in stats)
-    mfree = w.d > 32 and args.matrix_free
+    # d > 32: the library materialises the cost unless asked not to or a side
+    # has more points than its materialised kernels stage (16384)
+    mfree = w.d > 32 and not args.materialize and (
+        args.matrix_free or max(int(w.X.shape[1]), int(w.Y.shape[1])) > MAT_MAX_POINTS)
     mat = args.materialize or (w.d > 32 and not mfree)
     rec = {}
     if mfree:
