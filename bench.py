@@ -72,24 +72,39 @@ def _cores():
         return os.cpu_count() or 1
 
 
+LIBRARY_SOURCES = ("ds_kernels.hip", "ds_host.cpp", "ds_internal.h")
+
+
+def source_code_hash(texts):
+    """sha256 of the library's code with comments and blank lines taken out
+    (each line cut at `//`, stripped, empty lines dropped; the sources hold no
+    `//` inside string literals), so that a comment edit keeps a profile valid
+    and any code edit does not."""
+    import hashlib
+    h = hashlib.sha256()
+    for text in texts:
+        for line in text.splitlines():
+            code = line.split("//", 1)[0].strip()
+            if code:
+                h.update(code.encode() + b"\n")
+        h.update(b"\0")
+    return h.hexdigest()
+
+
 def measured_traffic(name):
     """HBM bytes per update launch from the committed FETCH_SIZE / WRITE_SIZE
-    summary `profiles/<name>`, or None once the library source (kernels and the
+    summary `profiles/<name>`, or None once the library's code (kernels and the
     host runtime that picks their layouts and sub-batches) has changed since it
     was taken."""
-    import hashlib
     path = os.path.join(ROOT, "profiles", name)
     csrc = os.path.join(ROOT, "paper_2607_24741_amd", "csrc")
     try:
         fields = dict(line.split(": ", 1) for line in open(path).read().splitlines()
-                      if line.startswith(("kernel_source_sha256: ", "traffic_bytes_per_launch: ")))
-        h = hashlib.sha256()
-        for name in ("ds_kernels.hip", "ds_host.cpp", "ds_internal.h"):
-            h.update(open(os.path.join(csrc, name), "rb").read())
-        cur = h.hexdigest()
+                      if line.startswith(("kernel_code_sha256: ", "traffic_bytes_per_launch: ")))
+        cur = source_code_hash(open(os.path.join(csrc, n)).read() for n in LIBRARY_SOURCES)
     except OSError:
         return None
-    if fields.get("kernel_source_sha256") != cur:
+    if fields.get("kernel_code_sha256") != cur:
         return None
     return float(fields["traffic_bytes_per_launch"])
 

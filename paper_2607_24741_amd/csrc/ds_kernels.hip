@@ -7,9 +7,15 @@
 //                     multiply-adds and an add) and rounded once to float32
 //                     for v_exp_f32, column data staged in LDS and broadcast,
 //                     two rows per lane up to d = 12, streaming base-2
-//                     log-sum-exp over 8 fixed column groups, fused row screen;
-//                     with a second pass in the same launch, the column check
-//                     and release decision (the default path for d <= 16).
+//                     log-sum-exp over 8 fixed column groups of 4 fixed
+//                     sub-groups each, fused row screen; with a second pass in
+//                     the same launch, the column check and release decision
+//                     (the default path for d <= 16).
+//  k_update_f64_split<D>
+//                     the same half-step for narrow launches: one block per
+//                     (work item, column group), one wave per sub-group, the
+//                     group partials merged by the item's last block (the
+//                     same bits).
 //  k_update_mfma<DH, RT, GW, UNI>
 //                     the same half-step with the state in float32: x~.y~ on
 //                     the fp32 matrix cores (v_mfma_f32_32x32x2_f32) with the
@@ -24,7 +30,7 @@
 //  k_cost, k_mat_rows, k_mat_cols
 //                     the materialised cost: built once on the matrix cores,
 //                     then streamed from HBM by both half-steps (the default
-//                     for d > 32 up to 8192 points a side).
+//                     for d > 32 up to 16384 points a side).
 //  k_check64<DR>      float64 verification of the exported potentials (guarded
 //                     release).
 //  k_scan             one block: compaction map (survivor ranks, new work item
@@ -1066,12 +1072,15 @@ __device__ __forceinline__ double potential_f64(double gam, double nrm, double k
 // float64 and every exponent formed in float64 -- d fused multiply-adds and one
 // add -- before it is rounded once to float32 for v_exp_f32 (anchored sums are
 // used while the bound's spread is at most kFastRangePrecise). The terms of one
-// 32-column tile are summed in float32 and each tile's sum is added in float64.
+// 32-column tile are summed in float32 and each tile's sum is added in float64;
+// a sub-group's tiles accumulate from zero and the sub-groups are folded into
+// their group in order.
 //
 // A work item is 64 R rows (rows_f64(D): R = 2 up to d = 12, above which two
 // rows' coordinates no longer fit in registers beside a column's): lane l owns
-// rows l + 64 r (r < R), so every column value read from LDS serves R terms. Column data is the same for
-// every lane; each wave stages its tiles in its own LDS double buffer
+// rows l + 64 r (r < R), so every column value read from LDS serves R terms.
+// Column data is the same for every lane; each wave stages its tiles in its own
+// LDS double buffer
 // (coalesced loads: records, then the column operand gam written into slot D
 // of each column -- the record's padding double when D is odd) and reads them
 // back as broadcasts. Only the wave itself touches its buffer, so no block

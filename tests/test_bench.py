@@ -73,22 +73,36 @@ def test_large_d_roofline_follows_the_kernel_the_library_picks():
     assert forced["bound"] == "hbm"
 
 
-def test_traffic_is_reported_only_for_the_profiled_source(tmp_path, monkeypatch):
+def test_traffic_is_reported_only_for_the_profiled_code(tmp_path, monkeypatch):
     csrc = tmp_path / "paper_2607_24741_amd" / "csrc"
     csrc.mkdir(parents=True)
     (tmp_path / "profiles").mkdir()
-    for name in ("ds_kernels.hip", "ds_host.cpp", "ds_internal.h"):
-        (csrc / name).write_text(f"// {name}\n")
+    code = {n: f"// {n}\nint f_{i}() {{ return {i}; }}  // trailing\n\n"
+            for i, n in enumerate(bench.LIBRARY_SOURCES)}
+    for name, text in code.items():
+        (csrc / name).write_text(text)
+    # the hash covers the code lines only: comments and blank lines are out
     h = hashlib.sha256()
-    for name in ("ds_kernels.hip", "ds_host.cpp", "ds_internal.h"):
-        h.update((csrc / name).read_bytes())
+    for i, n in enumerate(bench.LIBRARY_SOURCES):
+        h.update(f"int f_{i}() {{ return {i}; }}".encode() + b"\n")
+        h.update(b"\0")
+    assert bench.source_code_hash(code[n] for n in bench.LIBRARY_SOURCES) == h.hexdigest()
     (tmp_path / "profiles" / "t.md").write_text(
-        f"# summary\n\nkernel_source_sha256: {h.hexdigest()}\ntraffic_bytes_per_launch: 12345\n")
+        f"# summary\n\nkernel_code_sha256: {h.hexdigest()}\ntraffic_bytes_per_launch: 12345\n")
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
     assert bench.measured_traffic("t.md") == 12345.0
     assert bench.measured_traffic("missing.md") is None
-    (csrc / "ds_host.cpp").write_text("// changed\n")
+    # a comment edit keeps the profile valid, a code edit does not
+    (csrc / "ds_host.cpp").write_text("// another comment\n" + code["ds_host.cpp"])
+    assert bench.measured_traffic("t.md") == 12345.0
+    (csrc / "ds_host.cpp").write_text("int f_1() { return 7; }\n")
     assert bench.measured_traffic("t.md") is None
+
+
+def test_committed_traffic_profile_matches_the_library_code():
+    # the committed summary of the headline kernel's HBM traffic belongs to
+    # the code in the tree (a code change needs the counters taken again)
+    assert bench.measured_traffic("k_update_f64_c5_traffic.md") is not None
 
 
 def test_algorithmic_bytes_of_the_float64_update():
