@@ -90,6 +90,8 @@ ds::Layout plan(const ds_problem* pr, const ds_options* op, void* ws) {
   L.m_max = pr->m_max;
   L.d = pr->d;
   L.dp = pr->d + (pr->d & 1);
+  // the matrix-free large-d kernel stages whole kMfreeK-coordinate slices
+  if (uses_mfree(pr, op)) L.dp = (int)align_up((size_t)pr->d, ds::kMfreeK);
   L.dh = L.dp / 2;
   L.mat = uses_mat(pr, op) ? 1 : 0;
   L.rows = L.mat ? ds::kRowsValu
@@ -135,10 +137,16 @@ ds::Layout plan(const ds_problem* pr, const ds_options* op, void* ws) {
     L.gerr[side] = (L.guard && L.es == 2) ? c.take<float4>(W * (size_t)L.rbmax) : nullptr;
   }
   L.row64 = L.guard ? c.take<ds::RowCert>(W) : nullptr;
-  // float64 state: partials and arrival words of the split (narrow) launches
-  L.spart = L.es == 2 ? c.take<double2>((size_t)ds::kSplitSlots * ds::kGroups * (size_t)L.rows)
+  // partials and arrival words of the launches that split a work item over
+  // blocks: the float64 state's narrow launches (at most kSplitSlots items),
+  // and every launch of the matrix-free large-d kernel (both passes: at most
+  // two items per row block of every lane)
+  const bool mfree = uses_mfree(pr, op);
+  L.nslots = L.es == 2 ? ds::kSplitSlots : mfree ? (int)(2 * W * (size_t)L.rbmax) : 0;
+  L.spart = L.es == 2 ? c.take<double2>((size_t)L.nslots * ds::kGroups * (size_t)L.rows)
                       : nullptr;
-  L.scnt = L.es == 2 ? c.take<int>(2 * (size_t)ds::kSplitSlots) : nullptr;
+  L.kpart = mfree ? c.take<float2>((size_t)L.nslots * ds::kGroups * (size_t)L.rows) : nullptr;
+  L.scnt = L.nslots ? c.take<int>(2 * (size_t)L.nslots) : nullptr;
   L.bytes = align_up(c.off, 256);
   return L;
 }
@@ -336,7 +344,7 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
   ia.mat = mat ? 1 : 0;
   ia.ctrl = L.ctrl;
   HIP_TRY(launch_ingest(ia, maxpad, st));
-  if (L.scnt) HIP_TRY(launch_zero_counters(L.scnt, 2 * kSplitSlots, st));
+  if (L.scnt) HIP_TRY(launch_zero_counters(L.scnt, 2 * L.nslots, st));
   HIP_TRY(launch_offsets(L.bank[0].slot, W, L.rows, L.off[0], L.off[1], L.ctrl, st));
   Ctrl ctrl;
   HIP_TRY(hipMemcpyAsync(&ctrl, L.ctrl, sizeof(Ctrl), hipMemcpyDeviceToHost, st));
@@ -428,7 +436,7 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
     l.hsnap = R->snap_dev; l.nchk = L.nchk; l.disc = L.disc;
     l.progress = &R->snap_dev->progress;
     l.Q = L.Q; l.q_lane = (size_t)L.pad[0] * L.pad[1]; l.q_ld = L.pad[1];
-    l.spart = L.spart; l.scnt = L.scnt;
+    l.spart = L.spart; l.kpart = L.kpart; l.scnt = L.scnt; l.nslots = L.nslots;
     return l;
   };
   // DS_F_TIMING: both launches of every kSampleEvery-th cycle (and the final
@@ -480,7 +488,7 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
     hipEvent_t h0 = e0 >= 0 ? (*tm.pool)[e0] : nullptr, h1 = e1 >= 0 ? (*tm.pool)[e1] : nullptr;
     if (mat) HIP_TRY(launch_update_mat(l, blocks, st, h0, h1));
     else if (precise) HIP_TRY(launch_update_f64(l, d, variant, blocks, st, h0, h1));
-    else if (d > kMaxDSmall) HIP_TRY(launch_update_mfma_k(l, variant, blocks, st, h0, h1));
+    else if (d > kMaxDSmall) HIP_TRY(launch_update_mfma_k(l, blocks, st, h0, h1));
     else HIP_TRY(launch_update(l, d, use_mfma, variant, blocks, st, h0, h1));
     if (timed) {
       tm.spans[0].push_back({e0, e1});

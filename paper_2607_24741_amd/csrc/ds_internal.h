@@ -52,6 +52,10 @@ constexpr int kSplitSlots = 2 * kSplitItems;
 constexpr int kRowsMfma = 32;    // rows per work item, matrix-core kernel
 constexpr int kRowsValu = 64;    // rows per work item, vector-ALU kernel
 constexpr int kRowsMfmaK = 128;  // rows per work item, matrix-free large-d kernel
+constexpr int kMfreeCols = 128;  // columns per step of the matrix-free large-d kernel
+// coordinates per LDS stage of the matrix-free large-d kernel; its point
+// records are padded to a multiple of this with zeros
+constexpr int kMfreeK = 32;
 constexpr int kMaxW = 4096;
 constexpr int kMaxDSmall = 32;   // matrix-free kernels
 constexpr int kMaxDF64 = 16;     // matrix-free float64-state kernels
@@ -182,7 +186,9 @@ struct Layout {
                      // sum of mass, 0} of each side's potentials (else null)
   RowCert* row64;    // guarded release: [W] latest verified row residual by caller lane
   double2* spart;    // float64 state: split-launch partials (see Launch::spart)
-  int* scnt;         // float64 state: split-launch arrival counters
+  float2* kpart;     // matrix-free large d: group partials (see Launch::kpart)
+  int* scnt;         // split launches: arrival counters [nslots][2]
+  int nslots;        // work items the partials and counters hold
   int guard;
   size_t bytes;
 };
@@ -246,8 +252,10 @@ struct Launch {
   int* progress;                  // &hsnap->progress as the device addresses it (may be null)
   int seqno;                      // launch sequence number written there
   double2* spart;                 // split float64 launch: group partials
-                                  // [kSplitSlots][kGroups][rows]
-  int* scnt;                      // and per item [arrivals, skipped] [kSplitSlots][2], zero between launches
+                                  // [nslots][kGroups][rows]
+  float2* kpart;                  // matrix-free large d: group partials [nslots][kGroups][rows]
+  int* scnt;                      // and per item [arrivals, skipped] [nslots][2], zero between launches
+  int nslots;                     // items a launch of either kind may hold (both passes)
 };
 
 // Extra arguments of the float64 verification launch (guarded release), per
@@ -323,8 +331,9 @@ hipError_t launch_update(const Launch& a, int d, bool use_mfma, int variant, int
                          hipStream_t st, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 hipError_t launch_update_f64(const Launch& a, int d, int variant, int blocks, hipStream_t st,
                              hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
-// matrix-free matrix-core half-step for any d (K-looped contraction)
-hipError_t launch_update_mfma_k(const Launch& a, int variant, int blocks, hipStream_t st,
+// matrix-free matrix-core half-step for any d (tiled contraction), `blocks`
+// work items over both passes
+hipError_t launch_update_mfma_k(const Launch& a, int blocks, hipStream_t st,
                                 hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 hipError_t launch_update_mat(const Launch& a, int blocks, hipStream_t st, hipEvent_t e0 = nullptr,
                              hipEvent_t e1 = nullptr);

@@ -24,9 +24,12 @@
 //                     16 < d <= 32).
 //  k_update_valu<D>   the float32 half-step on the vector ALU, column data
 //                     wave-uniform (scalar loads, SGPR operands); on request.
-//  k_update_mfma_k<GW, UNI>
-//                     the float32 matrix-core half-step for any d, K-looped
-//                     over the coordinates (d > 32 without a materialised cost).
+//  k_update_mfma_k<UNI>
+//                     the float32 matrix-core half-step for any d: a tiled
+//                     contraction (128 x 128 block tiles, operands staged in
+//                     LDS) with the streaming sum as its epilogue, one block
+//                     per (work item, column group) (d > 32 without a
+//                     materialised cost).
 //  k_cost, k_mat_rows, k_mat_cols
 //                     the materialised cost: built once on the matrix cores,
 //                     then streamed from HBM by both half-steps (the default
@@ -56,6 +59,7 @@
 namespace ds {
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
 
@@ -527,6 +531,31 @@ __device__ __forceinline__ bool place_item(const Launch& L, const Pass& P, int n
   return true;
 }
 
+// Placement for kernels whose every placed block must arrive at its item's
+// counter (one block per (item, column group)): false only for blocks beyond
+// the launch's items, a fact fixed for the whole launch. Whether the item
+// still has work can change while the launch runs (a check pass of the same
+// launch may retire the lane or finish the window), so it is left to
+// item_live() on c_fin, c_A and si, and a block without work arrives marked
+// skipped.
+template <int UNI = -1>
+__device__ __forceinline__ bool place_item_all(const Launch& L, const Pass& P, int nb, int b,
+                                               int& s, int& rb0, int& nrows, int& ncols,
+                                               SlotInfo& si, int& c_fin, int& c_A) {
+  if (UNI == 1 || (UNI < 0 && P.ipl > 0))
+    return place_item<1, 1>(L, P, nb, b, s, rb0, nrows, ncols, si, c_fin, c_A);
+  const Ctrl* c = L.ctrl;
+  c_fin = c->finished;
+  c_A = min(P.A, c->A);
+  if (b >= P.off[c_A]) return false;
+  s = find_slot(P.off, c_A, b);
+  rb0 = b - P.off[s];
+  si = L.slot[s];
+  nrows = P.role ? si.m : si.n;
+  ncols = P.role ? si.n : si.m;
+  return true;
+}
+
 // --------------------------------------------------------- MFMA half-step
 // The columns of a lane are cut into kGroups fixed groups of whole 32-column
 // tiles (tpg = ceil(tiles / kGroups) tiles each). Every group is swept in tile
@@ -747,192 +776,317 @@ void k_update_mfma(Launch L) {
 }
 
 // --------------------------------------------------- matrix-free, large d
-// The same half-step as k_update_mfma for any d: the contraction x~ . y~ is
-// K-looped over the coordinates on v_mfma_f32_32x32x2_f32, both operands read
-// per tile from memory, KU coordinate pairs per batch of loads (two register
-// buffers: the next batch is in flight while the current one runs). A work
-// item is kRowsMfmaK = 128 rows (RT = 4 row tiles), so each column operand a
-// lane loads feeds four matrix-core instructions; the row operands are shared
-// by the block's waves through the caches. Then the augmented pair
-// (gam_j, 1) . (1, -anchor_i) and the same streaming base-2 sum, fixed column
-// groups and merge as k_update_mfma. It is the path for d > 32 when the cost
-// cannot be materialised (more than 8192 points on a side) or on request
-// (DS_F_MATRIX_FREE).
-template <int GW, bool UNI>
-__global__ __launch_bounds__(64 * (kGroups / GW), 2)
+// The float32 half-step for any d as a tiled contraction on the matrix cores
+// with the streaming base-2 sum as its epilogue. A block owns one work item of
+// 128 rows and one of the lane's kGroups column groups (groups of whole
+// 128-column steps), so even a launch of few items spreads over the chip. Per
+// step the block forms the 128 x 128 tile of x~ . y~: four waves of 64 x 64
+// (2 x 2 v_mfma_f32_32x32x2_f32 tiles each), K-looped over the coordinates in
+// stages of kMfreeK, every stage of both operands staged once in LDS by the
+// whole block (coalesced 16-byte loads, double-buffered: the next stage loads
+// while the current one runs). Inside a stage the matrix instruction p takes
+// coordinate 16 h + p from lane half h, so a lane reads its 16 coordinates of
+// a row as four 16-byte LDS reads (rows padded to 36 floats: no bank
+// conflicts). The column potential and the row anchor enter as one augmented
+// matrix instruction per tile, (gam_j, 1) . (1, -anchor_i), then each lane
+// reduces its 16 terms of a row per 32-column tile, tile 0 then tile 1 of its
+// half of the step, steps in order.
+//
+// A row's group partial is the fold, in the order (wave column 0, lane half 0),
+// (0, 1), (1, 0), (1, 1), of four running partials; it goes to memory with
+// device-scope stores, and the item's last block to arrive merges the groups in
+// order and finishes the item. Every order depends on the lane's (n, m, d)
+// only, so the bits do not depend on the launch.
+// One LDS stage of the matrix-free kernel: kMfreeK coordinates of the item's
+// kRowsMfmaK rows, then of the step's kMfreeCols columns, each row at a stride
+// of kMfreeK + 4 floats. Thread t moves float4 number t % 8 of rows t / 8 + 32 j
+// (j < 4) of both operands: eight threads read one row's 128 contiguous bytes.
+struct MfreeStage {
+  static constexpr int LD = kMfreeK + 4;
+  static constexpr int STAGE = (kRowsMfmaK + kMfreeCols) * LD;
+  static_assert(kRowsMfmaK == 128 && kMfreeCols == 128 && kMfreeK == 32, "256 threads, 4 rows each");
+  const float* xs;   // this thread's first float of the item's rows
+  const float* ys;   // and of the lane's columns
+  float* ss;         // its first LDS float of a stage
+  int dp;
+  // native vectors in named registers: HIP's float4 (or an array) here ended up
+  // in memory, and its stores then waited for the loads mid-stage
+  f32x4 x0, x1, x2, x3, y0, y1, y2, y3;
+  __device__ __forceinline__ MfreeStage(const float* xrec, const float* yrec, int dp_, float* sh)
+      : dp(dp_) {
+    const int row = threadIdx.x >> 3, q = (threadIdx.x & 7) * 4;
+    xs = xrec + (size_t)row * dp + q;
+    ys = yrec + (size_t)row * dp + q;
+    ss = sh + row * LD + q;
+  }
+  // coordinates k0 .. k0 + kMfreeK of step t
+  __device__ __forceinline__ void fetch(int t, int k0) {
+    const float* xq = xs + k0;
+    const float* yq = ys + (size_t)t * kMfreeCols * dp + k0;
+    const size_t r32 = (size_t)32 * dp;
+    x0 = *reinterpret_cast<const f32x4*>(xq);
+    y0 = *reinterpret_cast<const f32x4*>(yq);
+    x1 = *reinterpret_cast<const f32x4*>(xq + r32);
+    y1 = *reinterpret_cast<const f32x4*>(yq + r32);
+    x2 = *reinterpret_cast<const f32x4*>(xq + 2 * r32);
+    y2 = *reinterpret_cast<const f32x4*>(yq + 2 * r32);
+    x3 = *reinterpret_cast<const f32x4*>(xq + 3 * r32);
+    y3 = *reinterpret_cast<const f32x4*>(yq + 3 * r32);
+  }
+  __device__ __forceinline__ void stash(int buf) const {
+    float* st = ss + buf * STAGE;
+    *reinterpret_cast<f32x4*>(st) = x0;
+    *reinterpret_cast<f32x4*>(st + kRowsMfmaK * LD) = y0;
+    *reinterpret_cast<f32x4*>(st + 32 * LD) = x1;
+    *reinterpret_cast<f32x4*>(st + (kRowsMfmaK + 32) * LD) = y1;
+    *reinterpret_cast<f32x4*>(st + 64 * LD) = x2;
+    *reinterpret_cast<f32x4*>(st + (kRowsMfmaK + 64) * LD) = y2;
+    *reinterpret_cast<f32x4*>(st + 96 * LD) = x3;
+    *reinterpret_cast<f32x4*>(st + (kRowsMfmaK + 96) * LD) = y3;
+  }
+};
+
+template <bool UNI>
+__global__ __launch_bounds__(256, 2)
 void k_update_mfma_k(Launch L) {
   note_progress(L);
-  constexpr int KU = 4;                       // coordinate pairs per batch of loads
-  constexpr int RT = kRowsMfmaK / 32;         // row tiles per item
-  __shared__ float2 sh_part[kGroups][2][kRowsMfmaK];
-  const int b = blockIdx.x;
-  const int pi = b >= L.nb0;
+  constexpr int BM = kRowsMfmaK;   // rows of an item
+  constexpr int BN = kMfreeCols;   // columns of a step
+  constexpr int KC = kMfreeK;      // coordinates per stage
+  constexpr int LD = MfreeStage::LD;        // LDS row stride (floats)
+  constexpr int STAGE = MfreeStage::STAGE;
+  __shared__ __align__(16) float sh_buf[2 * STAGE];
+  __shared__ int sh_work[4];
+  const int it = (int)(blockIdx.x / kGroups);   // work item of the launch (both passes)
+  const int g = (int)(blockIdx.x % kGroups);    // its column group
+  const int pi = it >= L.nb0;
   const Pass P = L.p[pi];
+  const int nitems = pi ? (int)(gridDim.x / kGroups) - L.nb0 : L.nb0;
   int s, rb0, nrows, ncols, c_fin, c_A;
   SlotInfo si;
-  if (!place_item<1, UNI ? 1 : 0>(L, P, pass_blocks(L, pi), pi ? b - L.nb0 : b, s, rb0, nrows,
-                                  ncols, si, c_fin, c_A))
+  if (!place_item_all<UNI ? 1 : 0>(L, P, nitems, pi ? it - L.nb0 : it, s, rb0, nrows, ncols, si,
+                                   c_fin, c_A))
     return;
   const bool upd = P.kind == KIND_UPDATE;
   float rhat = NAN;
-  if (!upd) {
-    const bool chk = check_facts(L, P, s, P.role ? ncols : nrows, rhat);
-    if (!item_live(L, P, s, si, c_fin, c_A)) return;
-    if (!chk) return;
-  }
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int h = lane >> 5;
-  const int r = lane & 31;
-  const int DP = L.dp;
-  const int DH = DP >> 1;
-  const int row0 = rb0 * kRowsMfmaK;
-  float lse_t[RT];
-  const float* rrow[RT];
-#pragma unroll
-  for (int q = 0; q < RT; ++q) {
-    const size_t ridx = (size_t)s * P.padr + row0 + 32 * q + r;
-    lse_t[q] = P.lse_in[ridx];
-    rrow[q] = P.rec_row + ridx * DP + h * DH;   // this lane's half of row tile q's row r
-  }
-  // wave 0 lane l owns rows row0 + l and row0 + 64 + l
-  bool owner[2];
-  float own_lm[2] = {0.f, 0.f}, own_w[2] = {0.f, 0.f}, own_lse[2];
-#pragma unroll
-  for (int e = 0; e < 2; ++e) {
-    const int orow = row0 + 64 * e + lane;
-    owner[e] = wave == 0 && orow < nrows;
-    if (owner[e]) own_lm[e] = P.lm_row[(size_t)s * P.padr + orow];
-    own_lse[e] = P.lse_in[(size_t)s * P.padr + orow];
-  }
+  // (a fact of the previous launch: the same for every block of the item)
+  if (!upd && !check_facts(L, P, s, P.role ? ncols : nrows, rhat)) return;
   bool fast = false;
   float M = 0.f;
-  if (upd) {
-    update_facts(L, P, s, ncols, fast, M);
-    if (!item_live(L, P, s, si, c_fin, c_A)) return;
-  }
+  if (upd) update_facts(L, P, s, ncols, fast, M);
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  // the sweep has block barriers: one liveness verdict for the whole block
+  if (lane == 0) sh_work[wave] = item_live(L, P, s, si, c_fin, c_A) ? 1 : 0;
+  __syncthreads();
+  const bool work = sh_work[0] && sh_work[1] && sh_work[2] && sh_work[3];
+  const int h = lane >> 5, r = lane & 31;
+  const int wr = wave >> 1, wc = wave & 1;   // the wave's 64 rows and 64 columns of a step
+  const int DP = L.dp;
+  const int row0 = rb0 * BM;
+  float baug[2];
 #pragma unroll
-  for (int e = 0; e < 2; ++e)
-    if (owner[e]) own_w[e] = P.w_row[(size_t)si.lane * P.w_ld + row0 + 64 * e + lane];
-  float baug[RT];
-#pragma unroll
-  for (int q = 0; q < RT; ++q) {
-    const bool live_q = row0 + 32 * q + r < nrows && lse_t[q] != INFINITY;
+  for (int a = 0; a < 2; ++a) {
+    const int i = row0 + wr * 64 + a * 32 + r;
+    const float lse = P.lse_in[(size_t)s * P.padr + i];
+    const bool lv = i < nrows && lse != INFINITY;
     float bias = 0.f;
-    if (live_q) {
-      if (!upd) bias = -lse_t[q];
-      else if (fast) bias = -(lse_t[q] + M);
+    if (lv) {
+      if (!upd) bias = -lse;
+      else if (fast) bias = -(lse + M);
     }
-    baug[q] = h ? bias : 1.f;
+    baug[a] = h ? bias : 1.f;
   }
-
-  const int ct = (ncols + kColTile - 1) / kColTile;
-  const int tpg = (ct + kGroups - 1) / kGroups;
-  const float* ccol = P.rec_col + (size_t)s * P.padc * DP + h * DH + (size_t)r * DP;
-  const float* gcol = P.gam_col + (size_t)s * P.padc + r;
+  const int S = (ncols + BN - 1) / BN;
+  const int spg = (S + kGroups - 1) / kGroups;
+  const int tA = min(S, g * spg), tB = min(S, g * spg + spg);
+  const int nch = DP / KC;
+  const float m0 = fast ? 0.f : -INFINITY;
+  float mrun[2] = {m0, m0}, srun[2] = {0.f, 0.f};
+  if (work && tA < tB) {
+    const float* xrec = P.rec_row + ((size_t)s * P.padr + row0) * DP;
+    const float* yrec = P.rec_col + (size_t)s * P.padc * DP;
+    const float* gcol = P.gam_col + (size_t)s * P.padc;
+    MfreeStage stg(xrec, yrec, DP, sh_buf);
+    stg.fetch(tA, 0);
+    stg.stash(0);
+    __syncthreads();
+    int t = tA, kc = 0, buf = 0;
+    f32x16 acc[2][2];
+    float ag[2];
 #pragma unroll 1
-  for (int u = 0; u < GW; ++u) {
-    const int g = wave * GW + u;
-    const int t0 = min(ct, g * tpg), t1 = min(ct, g * tpg + tpg);
-    float mrun[RT], srun[RT];
+    while (t < tB) {
+      if (kc == 0) {
 #pragma unroll
-    for (int q = 0; q < RT; ++q) { mrun[q] = fast ? 0.f : -INFINITY; srun[q] = 0.f; }
-#pragma unroll 1
-    for (int t = t0; t < t1; ++t) {
-      const float* c = ccol + (size_t)t * kColTile * DP;
-      f32x16 acc[RT];
+        for (int a = 0; a < 2; ++a)
 #pragma unroll
-      for (int q = 0; q < RT; ++q)
-        acc[q] = f32x16{0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-      float av0[KU], av1[KU], bw0[RT][KU], bw1[RT][KU];
-      auto fetch = [&](int k0, float* av, float (*bw)[KU]) {
+          for (int b = 0; b < 2; ++b)
 #pragma unroll
-        for (int v = 0; v < KU; ++v) {
-          const bool in = k0 + v < DH;
-          av[v] = in ? c[k0 + v] : 0.f;
+            for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.f;
 #pragma unroll
-          for (int q = 0; q < RT; ++q) bw[q][v] = in ? rrow[q][k0 + v] : 0.f;
-        }
-      };
-      auto mma = [&](const float* av, float (*bw)[KU]) {
-#pragma unroll
-        for (int v = 0; v < KU; ++v)
-#pragma unroll
-          for (int q = 0; q < RT; ++q)
-            acc[q] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[v], bw[q][v], acc[q], 0, 0, 0);
-      };
-      fetch(0, av0, bw0);
-#pragma unroll 1
-      for (int k0 = 0; k0 < DH; k0 += 2 * KU) {
-        if (k0 + KU < DH) fetch(k0 + KU, av1, bw1);
-        mma(av0, bw0);
-        if (k0 + 2 * KU < DH) fetch(k0 + 2 * KU, av0, bw0);
-        if (k0 + KU < DH) mma(av1, bw1);
+        for (int b = 0; b < 2; ++b) ag[b] = h ? 1.f : gcol[(size_t)t * BN + wc * 64 + b * 32 + r];
       }
-      const float ag = h ? 1.f : gcol[(size_t)t * kColTile];
+      // the next stage (of this step, or the first of the next one) loads now;
+      // after the last one the current stage is loaded again, unused, so that
+      // the loop has no branch around its loads and stores
+      int tn = t, kn = kc + 1;
+      if (kn == nch) { kn = 0; ++tn; }
+      stg.fetch(tn < tB ? tn : t, tn < tB ? kn * KC : kc * KC);
+      __builtin_amdgcn_sched_barrier(0);   // the loads go out before the stage's matrix work
+      const float* sx = sh_buf + buf * STAGE;
+      const float* sy = sx + BM * LD;
 #pragma unroll
-      for (int q = 0; q < RT; ++q) {
-        acc[q] = __builtin_amdgcn_mfma_f32_32x32x2f32(ag, baug[q], acc[q], 0, 0, 0);
-        float e[16];
-        if (fast) {
+      for (int half = 0; half < 2; ++half) {
+        float4 xv[2][2], yv[2][2];
 #pragma unroll
-          for (int v = 0; v < 16; ++v) e[v] = ex2(acc[q][v]);
+        for (int a = 0; a < 2; ++a)
 #pragma unroll
-          for (int w = 8; w > 0; w >>= 1)
+          for (int q = 0; q < 2; ++q)
+            xv[a][q] = *reinterpret_cast<const float4*>(sx + (wr * 64 + a * 32 + r) * LD + h * 16 +
+                                                        half * 8 + q * 4);
 #pragma unroll
-            for (int v = 0; v < w; ++v) e[v] += e[v + w];
-          srun[q] += e[0];
-        } else {
-          float tm = acc[q][0];
+        for (int b = 0; b < 2; ++b)
 #pragma unroll
-          for (int v = 1; v < 16; ++v) tm = fmaxf(tm, acc[q][v]);
-          const float mn = fmaxf(mrun[q], tm);
-          const float mref = (mn == -INFINITY) ? 0.f : mn;
+          for (int q = 0; q < 2; ++q)
+            yv[b][q] = *reinterpret_cast<const float4*>(sy + (wc * 64 + b * 32 + r) * LD + h * 16 +
+                                                        half * 8 + q * 4);
 #pragma unroll
-          for (int v = 0; v < 16; ++v) e[v] = ex2(acc[q][v] - mref);
+        for (int q = 0; q < 2; ++q)
 #pragma unroll
-          for (int w = 8; w > 0; w >>= 1)
+          for (int e = 0; e < 4; ++e)
 #pragma unroll
-            for (int v = 0; v < w; ++v) e[v] += e[v + w];
-          srun[q] = srun[q] * ex2(mrun[q] - mref) + e[0];
-          mrun[q] = mn;
+            for (int a = 0; a < 2; ++a)
+#pragma unroll
+              for (int b = 0; b < 2; ++b)
+                acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(yv[b][q][e], xv[a][q][e],
+                                                                 acc[a][b], 0, 0, 0);
+      }
+      if (kc == nch - 1) {
+        // the step's epilogue: column potential and row anchor, then the
+        // streaming sum of each row (tile 0, then tile 1)
+#pragma unroll
+        for (int a = 0; a < 2; ++a) {
+#pragma unroll
+          for (int b = 0; b < 2; ++b) {
+            const f32x16 z = __builtin_amdgcn_mfma_f32_32x32x2f32(ag[b], baug[a], acc[a][b], 0, 0, 0);
+            float e[16];
+            if (fast) {
+#pragma unroll
+              for (int v = 0; v < 16; ++v) e[v] = ex2(z[v]);
+#pragma unroll
+              for (int w = 8; w > 0; w >>= 1)
+#pragma unroll
+                for (int v = 0; v < w; ++v) e[v] += e[v + w];
+              srun[a] += e[0];
+            } else {
+              float tm = z[0];
+#pragma unroll
+              for (int v = 1; v < 16; ++v) tm = fmaxf(tm, z[v]);
+              const float mn = fmaxf(mrun[a], tm);
+              const float mref = (mn == -INFINITY) ? 0.f : mn;
+#pragma unroll
+              for (int v = 0; v < 16; ++v) e[v] = ex2(z[v] - mref);
+#pragma unroll
+              for (int w = 8; w > 0; w >>= 1)
+#pragma unroll
+                for (int v = 0; v < w; ++v) e[v] += e[v + w];
+              srun[a] = srun[a] * ex2(mrun[a] - mref) + e[0];
+              mrun[a] = mn;
+            }
+          }
         }
       }
+      // (the stage's stores stay behind the matrix work: hoisted above it they
+      // would wait for the global loads before the stage runs)
+      __builtin_amdgcn_sched_barrier(0);
+      stg.stash(buf ^ 1);
+      __syncthreads();
+      buf ^= 1;
+      t = tn;
+      kc = kn;
     }
-#pragma unroll
-    for (int q = 0; q < RT; ++q) sh_part[g][h][32 * q + r] = make_float2(mrun[q], srun[q]);
   }
+  // the four running partials of every row, through LDS (the stages are done)
+  __syncthreads();
+  float2* sp = reinterpret_cast<float2*>(sh_buf);   // [wave column][lane half][row]
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+    sp[(2 * wc + h) * BM + wr * 64 + a * 32 + r] = make_float2(mrun[a], srun[a]);
   __syncthreads();
   if (wave != 0) return;
-  // merge per row: half-waves, then groups, in order (as k_update_mfma)
-  float Mt[2] = {0.f, 0.f}, St[2] = {0.f, 0.f};
+  float2* part = L.kpart + (size_t)it * kGroups * BM;
+  if (work) {
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int i = 64 * e + lane;
+      float gm = m0, gs = 0.f;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float2 pu = sp[u * BM + i];
+        if (fast) {
+          gs += pu.y;
+        } else {
+          const float mn = fmaxf(gm, pu.x);
+          const float mref = (mn == -INFINITY) ? 0.f : mn;
+          gs = gs * ex2(gm - mref) + pu.y * ex2(pu.x - mref);
+          gm = mn;
+        }
+      }
+      st_dev2(part + (size_t)g * BM + i, make_float2(gm, gs));
+    }
+  }
+  // arrival (the partials, or the skip mark, complete before it)
+  int last = 0, skipped = 0;
+  if (lane == 0) {
+    if (!work) atomicOr(&L.scnt[2 * it + 1], 1);
+    wait_mem();
+    const int prev = atomicAdd(&L.scnt[2 * it], 1);
+    last = prev + 1 == kGroups;
+    if (last) {
+      skipped = atomicExch(&L.scnt[2 * it + 1], 0);
+      atomicExch(&L.scnt[2 * it], 0);
+    }
+  } else {
+    wait_mem();
+  }
+  last = __builtin_amdgcn_readfirstlane(last);
+  skipped = __builtin_amdgcn_readfirstlane(skipped);
+  if (!last || skipped || !work) return;
+  // the item's finish: lane l owns rows row0 + l and row0 + 64 + l; every
+  // group partial is loaded before the first is used
+  float2 pg[2][kGroups];
+#pragma unroll
+  for (int e = 0; e < 2; ++e)
+#pragma unroll
+    for (int u = 0; u < kGroups; ++u) pg[e][u] = ld_dev2(part + (size_t)u * BM + 64 * e + lane);
+  bool owner[2], live[2];
+  float own_lm[2] = {0.f, 0.f}, own_w[2] = {0.f, 0.f}, own_lse[2], Mt[2] = {0.f, 0.f},
+        St[2] = {0.f, 0.f};
 #pragma unroll
   for (int e = 0; e < 2; ++e) {
-    const int ri = 64 * e + lane;
+    const int i = row0 + 64 * e + lane;
+    owner[e] = i < nrows;
+    own_lse[e] = P.lse_in[(size_t)s * P.padr + i];
+    if (owner[e]) {
+      own_lm[e] = P.lm_row[(size_t)s * P.padr + i];
+      own_w[e] = P.w_row[(size_t)si.lane * P.w_ld + i];
+    }
+    live[e] = owner[e] && own_lse[e] != INFINITY;
     if (!owner[e]) continue;
     if (fast) {
 #pragma unroll
-      for (int g = 0; g < kGroups; ++g) St[e] += sh_part[g][0][ri].y + sh_part[g][1][ri].y;
+      for (int u = 0; u < kGroups; ++u) St[e] += pg[e][u].y;
     } else {
-      float Mg[kGroups], Sg[kGroups];
       float mx = -INFINITY;
 #pragma unroll
-      for (int g = 0; g < kGroups; ++g) {
-        const float2 pa = sh_part[g][0][ri], pb = sh_part[g][1][ri];
-        const float mw = fmaxf(pa.x, pb.x);
-        const float mref = (mw == -INFINITY) ? 0.f : mw;
-        Sg[g] = pa.y * ex2(pa.x - mref) + pb.y * ex2(pb.x - mref);
-        Mg[g] = mw;
-        mx = fmaxf(mx, mw);
-      }
+      for (int u = 0; u < kGroups; ++u) mx = fmaxf(mx, pg[e][u].x);
       Mt[e] = (mx == -INFINITY) ? 0.f : mx;
 #pragma unroll
-      for (int g = 0; g < kGroups; ++g) St[e] += Sg[g] * ex2(Mg[g] - Mt[e]);
+      for (int u = 0; u < kGroups; ++u) St[e] += pg[e][u].y * ex2(pg[e][u].x - Mt[e]);
     }
   }
-  const bool live[2] = {owner[0] && own_lse[0] != INFINITY, owner[1] && own_lse[1] != INFINITY};
-  finish_rows_r<kRowsMfmaK, 1, 2, float>(L, P, s, si, rb0, owner, live, fast, M, own_lse, own_lm,
-                                         own_w, Mt, St, rhat);
+  finish_rows_r<BM, 1, 2, float>(L, P, s, si, rb0, owner, live, fast, M, own_lse, own_lm, own_w, Mt,
+                                 St, rhat);
 }
 
 // --------------------------------------------------------- VALU half-step
@@ -1475,7 +1629,7 @@ void k_update_f64_split(Launch L) {
   const int nitems = pi ? (int)(gridDim.x / kGroups) - L.nb0 : L.nb0;
   int s, rb, nrows, ncols, c_fin, c_A;
   SlotInfo si;
-  if (!place_item<1>(L, P, nitems, pi ? it - L.nb0 : it, s, rb, nrows, ncols, si, c_fin, c_A))
+  if (!place_item_all(L, P, nitems, pi ? it - L.nb0 : it, s, rb, nrows, ncols, si, c_fin, c_A))
     return;
   const bool upd = P.kind == KIND_UPDATE;
   float rhat = NAN;
@@ -2465,6 +2619,10 @@ __global__ __launch_bounds__(256) void k_ingest_points(IngestArgs p, int chunk) 
       float* rec = p.bank.rec[side] + idx * p.dp;
       double nrm = 0.0;
       if (live) {
+        // records padded beyond the next even count (matrix-free large d):
+        // zeros between and after the two halves
+        if (p.dp > p.d + (p.d & 1))
+          for (int k = 0; k < p.dp; ++k) rec[k] = 0.f;
         for (int k = 0; k < p.d; ++k) {
           const double v = sigma * ((double)P[((size_t)t * ld + q) * p.d + k] - (double)c[k]);
           const float fv = (float)v;
@@ -2577,8 +2735,8 @@ static hipError_t launch_f64_d(const Launch& a, int variant, int blocks, hipStre
   if (variant == VAR_SPLIT) {
     // `blocks` work items over both passes, one block per (item, group) and a
     // wave per sub-group; the partials and arrival words of the workspace
-    // hold kSplitSlots items
-    if (blocks > kSplitSlots || a.spart == nullptr || a.scnt == nullptr) return hipErrorInvalidValue;
+    // hold a.nslots items
+    if (blocks > a.nslots || a.spart == nullptr || a.scnt == nullptr) return hipErrorInvalidValue;
     hipExtLaunchKernelGGL((k_update_f64_split<D>), dim3(blocks * kGroups), dim3(64 * kSubGroups), 0,
                           st, e0, e1, 0, a);
   } else if (variant == VAR_NARROW) {
@@ -2639,17 +2797,18 @@ hipError_t launch_update(const Launch& a, int d, bool use_mfma, int variant, int
   }
 }
 
-hipError_t launch_update_mfma_k(const Launch& a, int variant, int blocks, hipStream_t st,
-                                hipEvent_t e0, hipEvent_t e1) {
+hipError_t launch_update_mfma_k(const Launch& a, int blocks, hipStream_t st, hipEvent_t e0,
+                                hipEvent_t e1) {
   if (blocks <= 0) return hipSuccess;
+  // `blocks` work items over both passes, one block per (item, group); the
+  // partials and arrival words of the workspace hold a.nslots items
+  if (blocks > a.nslots || a.kpart == nullptr || a.scnt == nullptr) return hipErrorInvalidValue;
+  if (a.dp % kMfreeK != 0) return hipErrorInvalidValue;   // whole stages of coordinates
   const bool uni = a.p[0].ipl > 0;   // both passes of a launch share the shapes
-  if (variant == VAR_NARROW) {
-    if (uni) hipExtLaunchKernelGGL((k_update_mfma_k<1, true>), dim3(blocks), dim3(512), 0, st, e0, e1, 0, a);
-    else hipExtLaunchKernelGGL((k_update_mfma_k<1, false>), dim3(blocks), dim3(512), 0, st, e0, e1, 0, a);
-  } else {
-    if (uni) hipExtLaunchKernelGGL((k_update_mfma_k<2, true>), dim3(blocks), dim3(256), 0, st, e0, e1, 0, a);
-    else hipExtLaunchKernelGGL((k_update_mfma_k<2, false>), dim3(blocks), dim3(256), 0, st, e0, e1, 0, a);
-  }
+  if (uni)
+    hipExtLaunchKernelGGL((k_update_mfma_k<true>), dim3(blocks * kGroups), dim3(256), 0, st, e0, e1, 0, a);
+  else
+    hipExtLaunchKernelGGL((k_update_mfma_k<false>), dim3(blocks * kGroups), dim3(256), 0, st, e0, e1, 0, a);
   return hipGetLastError();
 }
 
