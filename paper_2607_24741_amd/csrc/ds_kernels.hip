@@ -1788,50 +1788,157 @@ void k_update_f64_split(Launch L) {
 // Q is indexed by caller lane and never moved by compaction. Both kernels use
 // 64-row work items, eight waves, and the column operand staged in LDS.
 
-// Build: one 32x32 tile per wave, x~.y~ on the matrix cores over the centred
-// coordinates, then kappa (|x|^2 + |y|^2 - 2 x.y) clamped at 0. The padded
-// region is written too (zero coordinates), so every entry a half-step can
-// touch is finite.
-__global__ __launch_bounds__(256) void k_cost(CostArgs c) {
-  const int t = blockIdx.y;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int h = lane >> 5, r = lane & 31;
-  const int tiles_j = c.pad1 / 32;
-  const int tile = blockIdx.x * 4 + wave;
-  if (tile >= (c.pad0 / 32) * tiles_j) return;
-  const int ti = tile / tiles_j, tj = tile - ti * tiles_j;
-  const SlotInfo si = c.slot[t];
-  const int i = ti * 32 + r, j = tj * 32 + r;
-  const bool vi = i < si.n, vj = j < si.m;
-  const float* xr = c.X + ((size_t)t * c.n_max + (vi ? i : 0)) * c.d;
-  const float* yr = c.Y + ((size_t)t * c.m_max + (vj ? j : 0)) * c.d;
-  const float* cc = c.center + (size_t)t * c.d;
-  f32x16 acc = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  float nx = 0.f, ny = 0.f;
-  // matrix core s of a K step of 8 pairs component k0+s (lanes 0-31) with
-  // k0+4+s (lanes 32-63) of the same row and column
-  for (int k0 = 0; k0 < c.d; k0 += 8) {
+// Build: one 128 x 128 tile of a lane's cost per block. The centred
+// coordinates of the tile's rows and columns are staged in LDS kMfreeK at a
+// time (double-buffered, as in the matrix-free half-step), x~ . y~ runs on the
+// matrix cores (four waves of 64 x 64), and every thread also sums the squares
+// of one row's (tid < 128) or one column's staged coordinates in order; then
+// Q = kappa (|x|^2 + |y|^2 - 2 x.y) clamped at 0. The padded region is written
+// too (zero coordinates), so every entry a half-step can touch is finite.
+//
+// Staging: thread t moves coordinate t % 32 of the stage for rows t / 32 + 8 u
+// (u < 16) of both operands -- 32 threads read one row's 128 contiguous bytes
+// of the caller's array (any d, no alignment beyond 4 bytes).
+struct CostStage {
+  static constexpr int T = 128;
+  static constexpr int LD = kMfreeK + 4;
+  static constexpr int STAGE = 2 * T * LD;
+  static_assert(kMfreeK == 32, "a warp-wide row of 32 coordinates per stage");
+  const float* X;    // the lane's points
+  const float* Y;
+  const float* cc;   // its centre
+  int d, n, m;       // coordinates, valid points (n, m >= 1: validated before)
+  int i0, j0;        // the tile's first row and column
+  int sk, sr;
+  int k;             // the coordinate this thread loaded last
+  float ck;          // and the centre's value of it
+  f32x16 vx, vy;     // raw loaded values: centring and padding wait for stash()
+  // every load is in bounds (row, column and coordinate clamped to the valid
+  // ones), with no arithmetic on the loaded values: nothing waits for them
+  // before the stage's matrix work
+  __device__ __forceinline__ void fetch(int k0) {
+    k = k0 + sk;
+    const int kc = min(k, d - 1);
+    ck = cc[kc];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int k = k0 + 4 * h + q;
-      const float a = (vi && k < c.d) ? xr[k] - cc[k] : 0.f;
-      const float b = (vj && k < c.d) ? yr[k] - cc[k] : 0.f;
-      nx = fmaf(a, a, nx);
-      ny = fmaf(b, b, ny);
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, acc, 0, 0, 0);
+    for (int u = 0; u < 16; ++u) {
+      vx[u] = X[(size_t)min(i0 + sr + 8 * u, n - 1) * d + kc];
+      vy[u] = Y[(size_t)min(j0 + sr + 8 * u, m - 1) * d + kc];
     }
   }
-  nx += __shfl_xor(nx, 32, 64);
-  ny += __shfl_xor(ny, 32, 64);
-  const float kap = si.kappa;
-  float* Qt = c.Q + (size_t)t * c.pad0 * c.pad1;
-  // lane l holds D[m][l % 32] for m = 8 (v / 4) + 4 (l / 32) + v % 4
+  // centred values into LDS, zero for padding rows and coordinates
+  __device__ __forceinline__ void stash(float* st) const {
+    const bool kin = k < d;
 #pragma unroll
-  for (int v = 0; v < 16; ++v) {
-    const int m = 8 * (v >> 2) + 4 * h + (v & 3);
-    const float nxm = __shfl(nx, m, 64);
-    const float q = kap * fmaxf(nxm + ny - 2.f * acc[v], 0.f);
-    Qt[(size_t)(ti * 32 + m) * c.pad1 + j] = q;
+    for (int u = 0; u < 16; ++u) {
+      st[(sr + 8 * u) * LD + sk] = (kin && i0 + sr + 8 * u < n) ? vx[u] - ck : 0.f;
+      st[(T + sr + 8 * u) * LD + sk] = (kin && j0 + sr + 8 * u < m) ? vy[u] - ck : 0.f;
+    }
+  }
+};
+
+__global__ __launch_bounds__(256, 2) void k_cost(CostArgs c) {
+  constexpr int T = CostStage::T, KC = kMfreeK, LD = CostStage::LD, STAGE = CostStage::STAGE;
+  __shared__ __align__(16) float sh[2 * STAGE];
+  __shared__ float sh_nrm[2 * T];   // |x~_i|^2 of the tile's rows, then |y~_j|^2 of its columns
+  const int t = blockIdx.y;
+  const int tiles_j = c.pad1 / T;
+  const int ti = (int)blockIdx.x / tiles_j, tj = (int)blockIdx.x - ti * tiles_j;
+  const SlotInfo si = c.slot[t];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int h = lane >> 5, r = lane & 31, wr = wave >> 1, wc = wave & 1;
+  CostStage stg;
+  stg.X = c.X + (size_t)t * c.n_max * c.d;
+  stg.Y = c.Y + (size_t)t * c.m_max * c.d;
+  stg.cc = c.center + (size_t)t * c.d;
+  stg.d = c.d;
+  stg.n = si.n;
+  stg.m = si.m;
+  stg.i0 = ti * T;
+  stg.j0 = tj * T;
+  stg.sk = tid & 31;
+  stg.sr = tid >> 5;
+  const int nst = (c.d + KC - 1) / KC;
+  stg.fetch(0);
+  stg.stash(sh);
+  __syncthreads();
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.f;
+  float nrm = 0.f;
+#pragma unroll 1
+  for (int st = 0; st < nst; ++st) {
+    const int buf = st & 1;
+    // the next stage loads now (after the last, the current one again, unused)
+    stg.fetch((st + 1 < nst ? st + 1 : st) * KC);
+    __builtin_amdgcn_sched_barrier(0);
+    const float* sx = sh + buf * STAGE;
+    const float* sy = sx + T * LD;
+    {
+      // row tid of the stage (x rows, then y rows): its squares in order
+      const float* rw = sx + tid * LD;
+#pragma unroll
+      for (int q = 0; q < KC / 4; ++q) {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(rw + 4 * q);
+        nrm = fmaf(v.x, v.x, nrm);
+        nrm = fmaf(v.y, v.y, nrm);
+        nrm = fmaf(v.z, v.z, nrm);
+        nrm = fmaf(v.w, v.w, nrm);
+      }
+    }
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      float4 xv[2][2], yv[2][2];
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+          xv[a][q] = *reinterpret_cast<const float4*>(sx + (wr * 64 + a * 32 + r) * LD + h * 16 +
+                                                      half * 8 + q * 4);
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+          yv[b][q] = *reinterpret_cast<const float4*>(sy + (wc * 64 + b * 32 + r) * LD + h * 16 +
+                                                      half * 8 + q * 4);
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+          for (int a = 0; a < 2; ++a)
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+              acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(xv[a][q][e], yv[b][q][e], acc[a][b],
+                                                               0, 0, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    stg.stash(sh + (buf ^ 1) * STAGE);
+    __syncthreads();
+  }
+  sh_nrm[tid] = nrm;
+  __syncthreads();
+  const float kap = si.kappa;
+  float* Qt = c.Q + (size_t)t * c.pad0 * c.pad1 + (size_t)ti * T * c.pad1 + (size_t)tj * T;
+  // lane l holds D[i][j] of column j = l % 32 of its tile and rows
+  // i = 8 (v / 4) + 4 (l / 32) + v % 4
+#pragma unroll
+  for (int a = 0; a < 2; ++a) {
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int j = wc * 64 + b * 32 + r;
+      const float ny = sh_nrm[T + j];
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int i = wr * 64 + a * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
+        Qt[(size_t)i * c.pad1 + j] = kap * fmaxf(sh_nrm[i] + ny - 2.f * acc[a][b][v], 0.f);
+      }
+    }
   }
 }
 
@@ -1890,9 +1997,7 @@ __global__ __launch_bounds__(512, 2) void k_mat_rows(Launch L) {
       }
       const float* q = Qt + (size_t)i * L.q_ld;
       float mrun = fast ? 0.f : -INFINITY, srun = 0.f;
-      for (int j = 4 * lane; j < nc4; j += 256) {
-        const float4 qv = *reinterpret_cast<const float4*>(q + j);
-        const float4 gv = *reinterpret_cast<const float4*>(sh_gam + j);
+      auto step = [&](const float4 qv, const float4 gv) {
         const float z0 = (gv.x + bias) - qv.x, z1 = (gv.y + bias) - qv.y;
         const float z2 = (gv.z + bias) - qv.z, z3 = (gv.w + bias) - qv.w;
         if (fast) {
@@ -1904,7 +2009,22 @@ __global__ __launch_bounds__(512, 2) void k_mat_rows(Launch L) {
                  ((ex2(z0 - mref) + ex2(z1 - mref)) + (ex2(z2 - mref) + ex2(z3 - mref)));
           mrun = mn;
         }
+      };
+      // kRowBatch loads of the row in flight before the first is used (one
+      // at a time left each wave waiting for memory on every step); the sum
+      // takes the steps in column order
+      constexpr int kRowBatch = 4;
+      int j = 4 * lane;
+      for (; j + 256 * (kRowBatch - 1) < nc4; j += 256 * kRowBatch) {
+        float4 qv[kRowBatch];
+#pragma unroll
+        for (int u = 0; u < kRowBatch; ++u) qv[u] = *reinterpret_cast<const float4*>(q + j + 256 * u);
+#pragma unroll
+        for (int u = 0; u < kRowBatch; ++u)
+          step(qv[u], *reinterpret_cast<const float4*>(sh_gam + j + 256 * u));
       }
+      for (; j < nc4; j += 256)
+        step(*reinterpret_cast<const float4*>(q + j), *reinterpret_cast<const float4*>(sh_gam + j));
       // fixed-tree merge of the 64 lanes
       if (fast) {
         Mr = 0.f;
@@ -1976,9 +2096,24 @@ __global__ __launch_bounds__(512, 2) void k_mat_cols(Launch L) {
   const int i0 = min(ncols, wave * ch), i1 = min(ncols, i0 + ch);
   const float* q = L.Q + (size_t)si.lane * L.q_lane + j;
   float mrun = fast ? 0.f : -INFINITY, srun = 0.f;
+  // the column is read kColBatch rows at a time, every load of a batch issued
+  // before the first is used (one dependent load per row left each wave
+  // waiting for memory on every term); the sums take the terms in row order
+  constexpr int kColBatch = 16;
   if (fast) {
+    // even rows of the chunk into sa, odd ones into sb
     float sa = 0.f, sb = 0.f;
     int i = i0;
+    for (; i + kColBatch <= i1; i += kColBatch) {
+      float qv[kColBatch];
+#pragma unroll
+      for (int u = 0; u < kColBatch; ++u) qv[u] = q[(size_t)(i + u) * L.q_ld];
+#pragma unroll
+      for (int u = 0; u < kColBatch; u += 2) {
+        sa += ex2((sh_gam[i + u] + bias) - qv[u]);
+        sb += ex2((sh_gam[i + u + 1] + bias) - qv[u + 1]);
+      }
+    }
     for (; i + 1 < i1; i += 2) {
       const float q0 = q[(size_t)i * L.q_ld], q1 = q[(size_t)(i + 1) * L.q_ld];
       sa += ex2((sh_gam[i] + bias) - q0);
@@ -1987,13 +2122,22 @@ __global__ __launch_bounds__(512, 2) void k_mat_cols(Launch L) {
     if (i < i1) sa += ex2((sh_gam[i] + bias) - q[(size_t)i * L.q_ld]);
     srun = sa + sb;
   } else {
-    for (int i = i0; i < i1; ++i) {
-      const float z = (sh_gam[i] + bias) - q[(size_t)i * L.q_ld];
+    auto term = [&](int i, float qi) {
+      const float z = (sh_gam[i] + bias) - qi;
       const float mn = fmaxf(mrun, z);
       const float mref = (mn == -INFINITY) ? 0.f : mn;
       srun = srun * ex2(mrun - mref) + ex2(z - mref);
       mrun = mn;
+    };
+    int i = i0;
+    for (; i + kColBatch <= i1; i += kColBatch) {
+      float qv[kColBatch];
+#pragma unroll
+      for (int u = 0; u < kColBatch; ++u) qv[u] = q[(size_t)(i + u) * L.q_ld];
+#pragma unroll
+      for (int u = 0; u < kColBatch; ++u) term(i + u, qv[u]);
     }
+    for (; i < i1; ++i) term(i, q[(size_t)i * L.q_ld]);
   }
   sh_part[wave][lane] = make_float2(mrun, srun);   // (-inf, 0) for an empty chunk
   __syncthreads();
@@ -2869,8 +3013,10 @@ hipError_t launch_check64(const Launch& a, const GuardArgs& g, int blocks, hipSt
   return hipGetLastError();
 }
 hipError_t launch_cost(const CostArgs& a, hipStream_t st) {
-  const int tiles = (a.pad0 / 32) * (a.pad1 / 32);
-  hipLaunchKernelGGL(k_cost, dim3((tiles + 3) / 4, a.W), dim3(256), 0, st, a);
+  // whole 128 x 128 tiles of every lane's padded cost
+  if (a.pad0 % CostStage::T != 0 || a.pad1 % CostStage::T != 0) return hipErrorInvalidValue;
+  const int tiles = (a.pad0 / CostStage::T) * (a.pad1 / CostStage::T);
+  hipLaunchKernelGGL(k_cost, dim3(tiles, a.W), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
