@@ -119,6 +119,7 @@ ds::Layout plan(const ds_problem* pr, const ds_options* op, void* ws) {
       }
     }
     B.slot = c.take<ds::SlotInfo>(W);
+    for (int role = 0; role < 2; ++role) B.ord[role] = c.take<int>(W);
     B.dec = c.take<ds::Decision>(W);
     for (int k = 0; k < 4; ++k) B.agg[k] = c.take<float4>(W * (size_t)L.rbmax);
   }
@@ -345,7 +346,8 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
   ia.ctrl = L.ctrl;
   HIP_TRY(launch_ingest(ia, maxpad, st));
   if (L.scnt) HIP_TRY(launch_zero_counters(L.scnt, 2 * L.nslots, st));
-  HIP_TRY(launch_offsets(L.bank[0].slot, W, L.rows, L.off[0], L.off[1], L.ctrl, st));
+  HIP_TRY(launch_offsets(L.bank[0].slot, W, L.rows, L.off[0], L.off[1], L.bank[0].ord[0],
+                         L.bank[0].ord[1], L.ctrl, st));
   Ctrl ctrl;
   HIP_TRY(hipMemcpyAsync(&ctrl, L.ctrl, sizeof(Ctrl), hipMemcpyDeviceToHost, st));
   std::vector<SlotInfo> lanes(W);
@@ -388,6 +390,7 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
     u.w_row = role ? pr->b : pr->a;
     u.w_ld = role ? pr->m_max : pr->n_max;
     u.off = L.off[role];
+    u.ord = B.ord[role];
     if (kind == 0) {
       u.agg_out = B.agg[role == 0 ? AGG_F : AGG_G];
       u.agg_bound = B.agg[role == 0 ? AGG_G : AGG_F];
@@ -545,6 +548,10 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
       std::memset(&sa, 0, sizeof(sa));
       sa.slot = L.bank[bank].slot; sa.dec = L.bank[bank].dec;
       sa.off_f = L.off[0]; sa.off_g = L.off[1]; sa.ctrl = L.ctrl; sa.hsnap = R->snap_dev;
+      for (int role = 0; role < 2; ++role) {
+        sa.ord_src[role] = L.bank[bank].ord[role];
+        sa.ord_dst[role] = L.bank[bank ^ 1].ord[role];
+      }
       sa.A = A; sa.W = W; sa.compact = 1; sa.rows = L.rows; sa.epoch = epoch;
       const int e0 = tm.on ? tm.rec() : -1;
       HIP_TRY(launch_scan(sa, st));

@@ -162,6 +162,12 @@ struct Bank {
   SlotInfo* slot;    // [W]
   Decision* dec;     // [W]
   float4* agg[4];    // [W][rbmax] row-block aggregates by slot
+  // Work item order of the mixed-shape launches, per role (0: f-half and row
+  // check, 1: g-half and column check): the slots by decreasing column count
+  // (the length of each of the lane's sweeps), then by slot. Launches place
+  // the longest sweeps first, so that the short ones fill the end of the
+  // launch. Written at ingest, carried through compaction (a stable filter).
+  int* ord[2];       // [W]
 };
 
 struct Layout {
@@ -215,7 +221,8 @@ struct Pass {
   float* gam_out;         // [W][padr] (update kind)
   const float* gam_col;   // [W][padc] column operand
   const float* w_row;     // caller masses of the row side, [W][w_ld] by lane id
-  const int* off;         // [A + 1] work item offsets (ipl == 0)
+  const int* off;         // [A + 1] first work item of each position of `ord` (ipl == 0)
+  const int* ord;         // [A] slots in item order (see Bank::ord)
   float4* agg_out;        // [W][rbmax] this pass's row-block aggregates
   float4* gerr_out;       // update kind, guarded release with the float64 state: the
                           // export rounding of this side's potentials, by caller lane
@@ -279,6 +286,8 @@ struct ScanArgs {          // compaction map over the slots of the current bank
   Decision* dec;
   int* off_f;             // [W + 1] rewritten for the new layout
   int* off_g;
+  const int* ord_src[2];  // item order of the current bank, per role
+  int* ord_dst[2];        // and of the other bank (the survivors, order kept)
   Ctrl* ctrl;
   HostSnap* hsnap;
   int A, W, compact, rows, epoch;
@@ -350,8 +359,8 @@ hipError_t launch_cost(const CostArgs& a, hipStream_t st);
 // float64 two-sided check of the audited state (both marginals, two passes)
 hipError_t launch_check64(const Launch& a, const GuardArgs& g, int blocks, hipStream_t st);
 hipError_t launch_scan(const ScanArgs& a, hipStream_t st);
-hipError_t launch_offsets(SlotInfo* slot, int A, int rows, int* off_f, int* off_g, Ctrl* ctrl,
-                          hipStream_t st);
+hipError_t launch_offsets(SlotInfo* slot, int A, int rows, int* off_f, int* off_g, int* ord_f,
+                          int* ord_g, Ctrl* ctrl, hipStream_t st);
 hipError_t launch_move(const MoveArgs& a, int A, int maxpad, hipStream_t st);
 hipError_t launch_ingest(const IngestArgs& a, int maxpad, hipStream_t st);
 hipError_t launch_order(const int* depth, int W, int* order, hipStream_t st);

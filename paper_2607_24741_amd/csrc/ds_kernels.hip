@@ -36,8 +36,10 @@
 //                     for d > 32 up to 16384 points a side).
 //  k_check64<DR>      float64 verification of the exported potentials (guarded
 //                     release).
-//  k_scan             one block: compaction map (survivor ranks, new work item
-//                     offsets) from the device-side decisions (Sec. 3.2).
+//  k_offsets, k_scan  one block: the work item order and offsets of the
+//                     initial layout (longest sweeps first); the compaction
+//                     map (survivor ranks, the orders filtered, new offsets)
+//                     from the device-side decisions (Sec. 3.2).
 //  k_move             retiree emission in caller lane order + survivor gather
 //                     into the other bank (physical compaction, Sec. 3.2).
 //  k_ingest_*         validation, centring/scaling, log masses, proposals.
@@ -113,6 +115,8 @@ enum { KIND_UPDATE = 0, KIND_VERIFY = 1 };
 enum { MODE_ACTIVE = 0, MODE_STATIC = 1, MODE_LOGICAL = 2 };
 
 // --------------------------------------------------------- work item lookup
+// The position q < A in a role's item order whose work items hold item b
+// (off[q] <= b < off[q + 1]; every lane has at least one item).
 __device__ __forceinline__ int find_slot(const int* off, int A, int b) {
   int lo = 0, hi = A;
   while (hi - lo > 1) {
@@ -493,8 +497,9 @@ __device__ __forceinline__ bool locate_item(const Launch& L, const Pass& P, int 
   const int N = P.off[A];
   if (b >= N) return false;
   const int item = b;
-  s = find_slot(P.off, A, item);
-  rb0 = item - P.off[s];
+  const int q = find_slot(P.off, A, item);   // position in the role's item order
+  rb0 = item - P.off[q];
+  s = P.ord[q];
   si = L.slot[s];
   return item_live(L, P, s, si, fin, A);
 }
@@ -548,8 +553,9 @@ __device__ __forceinline__ bool place_item_all(const Launch& L, const Pass& P, i
   c_fin = c->finished;
   c_A = min(P.A, c->A);
   if (b >= P.off[c_A]) return false;
-  s = find_slot(P.off, c_A, b);
-  rb0 = b - P.off[s];
+  const int q = find_slot(P.off, c_A, b);
+  rb0 = b - P.off[q];
+  s = P.ord[q];
   si = L.slot[s];
   nrows = P.role ? si.m : si.n;
   ncols = P.role ? si.n : si.m;
@@ -2202,27 +2208,50 @@ __global__ __launch_bounds__(1024) void k_scan(ScanArgs p) {
   }
   int tot_surv, tot_f, tot_g;
   int surv_off = block_exclusive_scan(nsurv, sh, tot_surv);
-  int f_off = block_exclusive_scan(items_f, sh, tot_f);
-  int g_off = block_exclusive_scan(items_g, sh, tot_g);
+  block_exclusive_scan(items_f, sh, tot_f);   // (the totals only)
+  block_exclusive_scan(items_g, sh, tot_g);
   for (int c = 0; c < C; ++c) {
     const int s = base + c;
     if (s >= A) break;
     const SlotInfo si = p.slot[s];
-    if (!si.done) {
-      const int ns = surv_off++;
-      p.dec[s].new_slot = ns;
-      p.off_f[ns] = f_off;
-      p.off_g[ns] = g_off;
-      f_off += row_blocks(si.n, p.rows);
-      g_off += row_blocks(si.m, p.rows);
-    } else {
-      p.dec[s].new_slot = -1;
-    }
+    p.dec[s].new_slot = si.done ? -1 : surv_off++;
   }
-  __syncthreads();
-  for (int s = tot_surv + (int)threadIdx.x; s <= p.W; s += blockDim.x) {
-    p.off_f[s] = tot_f;
-    p.off_g[s] = tot_g;
+  __syncthreads();   // the map is complete (block-visible global writes)
+  // each role's item order keeps the survivors in order (a stable filter of a
+  // sorted list stays sorted), renamed to their new slots, with the offsets
+  // of their work items
+  for (int role = 0; role < 2; ++role) {
+    const int* src = p.ord_src[role];
+    int* dst = p.ord_dst[role];
+    int* off = role ? p.off_g : p.off_f;
+    int np = 0, ni = 0;
+    for (int c = 0; c < C; ++c) {
+      const int q = base + c;
+      if (q >= A) break;
+      const SlotInfo si = p.slot[src[q]];
+      if (!si.done) {
+        np++;
+        ni += row_blocks(role ? si.m : si.n, p.rows);
+      }
+    }
+    int tp, ti;
+    int pos = block_exclusive_scan(np, sh, tp);
+    int it = block_exclusive_scan(ni, sh, ti);
+    for (int c = 0; c < C; ++c) {
+      const int q = base + c;
+      if (q >= A) break;
+      const int s = src[q];
+      const SlotInfo si = p.slot[s];
+      if (!si.done) {
+        dst[pos] = p.dec[s].new_slot;
+        off[pos] = it;
+        pos++;
+        it += row_blocks(role ? si.m : si.n, p.rows);
+      }
+    }
+    __syncthreads();
+    for (int q = tp + (int)threadIdx.x; q <= p.W; q += blockDim.x) off[q] = ti;
+    __syncthreads();
   }
   if (threadIdx.x == 0) {
     Ctrl* c = p.ctrl;
@@ -2239,27 +2268,49 @@ __global__ __launch_bounds__(1024) void k_scan(ScanArgs p) {
 }
 
 // Offsets over all slots of the current bank (ingest). One block.
+// Item order and work item offsets of the initial layout (slot = caller lane):
+// per role the slots by decreasing column count, then by slot (the rank of
+// every slot counted against all the others), and the first work item of each
+// position of that order.
 __global__ __launch_bounds__(1024) void k_offsets(SlotInfo* slot, int A, int rows, int* off_f,
-                                                  int* off_g, Ctrl* ctrl) {
+                                                  int* off_g, int* ord_f, int* ord_g, Ctrl* ctrl) {
   __shared__ int sh[32];
+  __shared__ int key[2][kMaxW];   // column count of every slot per role: m (f-half), n (g-half)
+  for (int s = threadIdx.x; s < A; s += blockDim.x) {
+    key[0][s] = slot[s].m;
+    key[1][s] = slot[s].n;
+  }
+  __syncthreads();
+  for (int s = threadIdx.x; s < A; s += blockDim.x) {
+    const int k0 = key[0][s], k1 = key[1][s];
+    int r0 = 0, r1 = 0;
+    for (int u = 0; u < A; ++u) {
+      const int v0 = key[0][u], v1 = key[1][u];
+      r0 += (v0 > k0) || (v0 == k0 && u < s);
+      r1 += (v1 > k1) || (v1 == k1 && u < s);
+    }
+    ord_f[r0] = s;
+    ord_g[r1] = s;
+  }
+  __syncthreads();   // the orders are complete (block-visible global writes)
   const int C = (A + 1023) / 1024;
   const int base = threadIdx.x * C;
   int nf = 0, ng = 0;
   for (int c = 0; c < C; ++c) {
-    const int s = base + c;
-    if (s >= A) break;
-    nf += row_blocks(slot[s].n, rows);
-    ng += row_blocks(slot[s].m, rows);
+    const int q = base + c;
+    if (q >= A) break;
+    nf += row_blocks(slot[ord_f[q]].n, rows);
+    ng += row_blocks(slot[ord_g[q]].m, rows);
   }
   int tf, tg;
   int of = block_exclusive_scan(nf, sh, tf);
   int og = block_exclusive_scan(ng, sh, tg);
   for (int c = 0; c < C; ++c) {
-    const int s = base + c;
-    if (s >= A) break;
-    off_f[s] = of; off_g[s] = og;
-    of += row_blocks(slot[s].n, rows);
-    og += row_blocks(slot[s].m, rows);
+    const int q = base + c;
+    if (q >= A) break;
+    off_f[q] = of; off_g[q] = og;
+    of += row_blocks(slot[ord_f[q]].n, rows);
+    og += row_blocks(slot[ord_g[q]].m, rows);
   }
   if (threadIdx.x == 0) {
     off_f[A] = tf; off_g[A] = tg;
@@ -2621,6 +2672,59 @@ __global__ __launch_bounds__(1024) void k_order(const int* depth, int W, int* or
 }
 
 // ----------------------------------------------------------------- ingest
+// Centre of each lane: the mean of its live source points and the mean of its
+// live target points, averaged, per coordinate. Block (c, t) takes kw
+// consecutive coordinates of lane t (kw a power of two, at most 64, so a wave
+// reads 4 kw contiguous bytes of a point); thread (g, k) sums coordinate k over
+// points g, g + 256 / kw, ... in order (float64), and the partials of the g are
+// then added in order: a fixed order, independent of the launch.
+__global__ __launch_bounds__(256) void k_centre(IngestArgs p, int kw) {
+  const int t = blockIdx.y;
+  const int nt = p.n ? p.n[t] : p.n_max;
+  const int mt = p.m ? p.m[t] : p.m_max;
+  if (nt < 1 || nt > p.n_max || mt < 1 || mt > p.m_max) return;   // reported by k_ingest_lanes
+  const int pg = 256 / kw;
+  const int g = threadIdx.x / kw;
+  const int k = blockIdx.x * kw + (threadIdx.x % kw);
+  const int kc = min(k, p.d - 1);
+  const float* a = p.a + (size_t)t * p.n_max;
+  const float* b = p.b + (size_t)t * p.m_max;
+  const float* X = p.X + (size_t)t * p.n_max * p.d + kc;
+  const float* Y = p.Y + (size_t)t * p.m_max * p.d + kc;
+  double sx = 0.0, sy = 0.0, cx = 0.0, cy = 0.0;
+#pragma unroll 4
+  for (int i = g; i < nt; i += pg) {
+    const bool live = a[i] != 0.f;
+    const float v = X[(size_t)i * p.d];
+    sx += live ? (double)v : 0.0;
+    cx += live ? 1.0 : 0.0;
+  }
+#pragma unroll 4
+  for (int j = g; j < mt; j += pg) {
+    const bool live = b[j] != 0.f;
+    const float v = Y[(size_t)j * p.d];
+    sy += live ? (double)v : 0.0;
+    cy += live ? 1.0 : 0.0;
+  }
+  __shared__ double sh[4][256];
+  sh[0][threadIdx.x] = sx;
+  sh[1][threadIdx.x] = sy;
+  sh[2][threadIdx.x] = cx;
+  sh[3][threadIdx.x] = cy;
+  __syncthreads();
+  if ((int)threadIdx.x >= kw || k >= p.d) return;
+  double rx = 0.0, ry = 0.0, nx = 0.0, ny = 0.0;
+  for (int q = 0; q < pg; ++q) {
+    const int u = q * kw + (int)threadIdx.x;
+    rx += sh[0][u];
+    ry += sh[1][u];
+    nx += sh[2][u];
+    ny += sh[3][u];
+  }
+  const double mx = nx > 0 ? rx / nx : 0.0, my = ny > 0 ? ry / ny : 0.0;
+  p.center[(size_t)t * p.d + k] = (float)(0.5 * (mx + my));
+}
+
 __global__ __launch_bounds__(256) void k_ingest_lanes(IngestArgs p) {
   const int t = blockIdx.x;
   const int nt = p.n ? p.n[t] : p.n_max;
@@ -2636,34 +2740,6 @@ __global__ __launch_bounds__(256) void k_ingest_lanes(IngestArgs p) {
       if (t < old) atomicExch(&p.ctrl->err_code, code);
     }
     return;
-  }
-  // centre: mean of live source points and mean of live target points,
-  // averaged; fixed-order double reduction
-  __shared__ double sh[256];
-  auto reduce = [&](double v) -> double {
-    sh[threadIdx.x] = v;
-    __syncthreads();
-    for (int w = 128; w > 0; w >>= 1) {
-      if ((int)threadIdx.x < w) sh[threadIdx.x] += sh[threadIdx.x + w];
-      __syncthreads();
-    }
-    double r = sh[0];
-    __syncthreads();
-    return r;
-  };
-  double cntx = 0.0, cnty = 0.0;
-  for (int i = threadIdx.x; i < nt; i += blockDim.x) cntx += (p.a[(size_t)t * p.n_max + i] != 0.f);
-  for (int j = threadIdx.x; j < mt; j += blockDim.x) cnty += (p.b[(size_t)t * p.m_max + j] != 0.f);
-  const double nx = reduce(cntx), ny = reduce(cnty);
-  for (int k = 0; k < p.d; ++k) {
-    double sx = 0.0, sy = 0.0;
-    for (int i = threadIdx.x; i < nt; i += blockDim.x)
-      if (p.a[(size_t)t * p.n_max + i] != 0.f) sx += p.X[((size_t)t * p.n_max + i) * p.d + k];
-    for (int j = threadIdx.x; j < mt; j += blockDim.x)
-      if (p.b[(size_t)t * p.m_max + j] != 0.f) sy += p.Y[((size_t)t * p.m_max + j) * p.d + k];
-    const double rx = reduce(sx), ry = reduce(sy);
-    const double mx = nx > 0 ? rx / nx : 0.0, my = ny > 0 ? ry / ny : 0.0;
-    if (threadIdx.x == 0) p.center[(size_t)t * p.d + k] = (float)(0.5 * (mx + my));
   }
   if (threadIdx.x == 0) {
     SlotInfo si;
@@ -3024,9 +3100,12 @@ hipError_t launch_scan(const ScanArgs& a, hipStream_t st) {
   hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, st, a);
   return hipGetLastError();
 }
-hipError_t launch_offsets(SlotInfo* slot, int A, int rows, int* off_f, int* off_g, Ctrl* ctrl,
+hipError_t launch_offsets(SlotInfo* slot, int A, int rows, int* off_f, int* off_g, int* ord_f,
+                          int* ord_g, Ctrl* ctrl,
                           hipStream_t st) {
-  hipLaunchKernelGGL(k_offsets, dim3(1), dim3(1024), 0, st, slot, A, rows, off_f, off_g, ctrl);
+  if (A > kMaxW) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_offsets, dim3(1), dim3(1024), 0, st, slot, A, rows, off_f, off_g, ord_f,
+                     ord_g, ctrl);
   return hipGetLastError();
 }
 hipError_t launch_move(const MoveArgs& a, int A, int maxpad, hipStream_t st) {
@@ -3038,6 +3117,10 @@ hipError_t launch_move(const MoveArgs& a, int A, int maxpad, hipStream_t st) {
 hipError_t launch_ingest(const IngestArgs& a, int maxpad, hipStream_t st) {
   hipLaunchKernelGGL(k_ctrl_init, dim3(1), dim3(64), 0, st, a.ctrl, a.W);
   hipLaunchKernelGGL(k_ingest_lanes, dim3(a.W), dim3(256), 0, st, a);
+  // the centre: up to 64 coordinates per block (a power of two)
+  int kw = 1;
+  while (kw < a.d && kw < 64) kw *= 2;
+  hipLaunchKernelGGL(k_centre, dim3((a.d + kw - 1) / kw, a.W), dim3(256), 0, st, a, kw);
   const int chunk = 1024;
   const int chunks = (maxpad + chunk - 1) / chunk;
   hipLaunchKernelGGL(k_ingest_points, dim3(chunks, a.W), dim3(256), 0, st, a, chunk);
