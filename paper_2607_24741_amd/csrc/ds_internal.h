@@ -199,11 +199,13 @@ struct Layout {
   size_t bytes;
 };
 
-// rows per work item of the float64-state kernel: two per lane up to d = 12,
-// then one (the rows' coordinates must fit in registers); four per lane at
-// d = 3 measured slower (2087 against 1980 ms per LiDAR-shaped solve: lower
+// rows per work item of the float64-state kernel: two per lane, so that each
+// column value read from LDS serves two terms. At d = 16 one row per lane left
+// the sweep bound by those reads (605 against 535 ms per telemetry solve, at
+// two waves per SIMD with a few spilled registers); four per lane at d = 3
+// measured slower (2087 against 1980 ms per LiDAR-shaped solve: lower
 // occupancy, fewer work items in narrow launches)
-__host__ __device__ constexpr int rows_f64(int d) { return d <= 12 ? 128 : 64; }
+__host__ __device__ constexpr int rows_f64(int) { return 128; }
 
 // work items of one lane-side: one per block of `rows` rows (all columns)
 __host__ __device__ inline int row_blocks(int nrows, int rows) { return (nrows + rows - 1) / rows; }

@@ -1236,9 +1236,8 @@ __device__ __forceinline__ double potential_f64(double gam, double nrm, double k
 // a sub-group's tiles accumulate from zero and the sub-groups are folded into
 // their group in order.
 //
-// A work item is 64 R rows (rows_f64(D): R = 2 up to d = 12, above which two
-// rows' coordinates no longer fit in registers beside a column's): lane l owns
-// rows l + 64 r (r < R), so every column value read from LDS serves R terms.
+// A work item is 64 R rows (rows_f64(D): R = 2): lane l owns rows l + 64 r
+// (r < R), so every column value read from LDS serves R terms.
 // Column data is the same for every lane; each wave stages its tiles in its own
 // LDS double buffer
 // (coalesced loads: records, then the column operand gam written into slot D
@@ -1246,11 +1245,11 @@ __device__ __forceinline__ double potential_f64(double gam, double nrm, double k
 // back as broadcasts. Only the wave itself touches its buffer, so no block
 // barrier is needed (a wave's LDS operations complete in order).
 // The second launch bound (minimum waves per SIMD) sets the register budget.
-// Chosen per d by measurement: at d = 16 the wide variant spills a few
-// registers to scratch at three waves per SIMD and still runs faster than at
-// two without spills.
+// Chosen per d by measurement: at d = 16 two rows per lane spill a few
+// registers to scratch even at two waves per SIMD (in the per-tile
+// bookkeeping, not the column loop) and still run faster than one row.
 template <int D>
-constexpr int f64_waves_per_simd() { return D <= 4 ? 4 : (D <= 7 ? 3 : (D <= 12 ? 2 : 3)); }
+constexpr int f64_waves_per_simd() { return D <= 4 ? 4 : (D <= 7 ? 3 : 2); }
 
 // One 32-column tile of the float64 half-step for R rows per lane (the tile in
 // LDS at `cur`, column stride DG, the column operand in slot D). Anchored sums
