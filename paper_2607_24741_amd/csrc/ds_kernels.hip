@@ -1492,6 +1492,17 @@ void k_update_f64(Launch L) {
 #pragma unroll
     for (int k = 0; k < D; ++k) xr[r][k] = rrow[k];
   }
+  // the wave's first tile loads with the rows, before the lane facts and the
+  // liveness verdict are known (in bounds either way; unused if no work)
+  const F64Tiling T(ncols);
+  const double* rec_lane = reinterpret_cast<const double*>(P.rec_col) + (size_t)s * P.padc * DP;
+  const double* gam_lane = reinterpret_cast<const double*>(P.gam_col) + (size_t)s * P.padc;
+  F64Stage<D> st;
+  {
+    const int g0 = wave * GW;
+    const int tA0 = min(T.ct, g0 * T.tpg), tB0 = min(T.ct, g0 * T.tpg + T.tpg);
+    if (tA0 < tB0) st.fetch(rec_lane, gam_lane, tA0, lane);
+  }
   bool fast = false;
   float M = 0.f;
   if (upd) {
@@ -1512,11 +1523,8 @@ void k_update_f64(Launch L) {
     }
   }
 
-  const F64Tiling T(ncols);
   double* buf0 = sh_tile[wave][0];
   double* buf1 = sh_tile[wave][1];
-  const double* rec_lane = reinterpret_cast<const double*>(P.rec_col) + (size_t)s * P.padc * DP;
-  const double* gam_lane = reinterpret_cast<const double*>(P.gam_col) + (size_t)s * P.padc;
   const double m0 = fast ? 0.0 : -(double)INFINITY;
 #pragma unroll
   for (int u = 0; u < GW; ++u) {
@@ -1531,9 +1539,8 @@ void k_update_f64(Launch L) {
       srun[r] = 0.0;
       sh_part[g][64 * r + lane] = make_double2(m0, 0.0);
     }
-    F64Stage<D> st;
     if (tA < tB) {
-      st.fetch(rec_lane, gam_lane, tA, lane);
+      if (u > 0) st.fetch(rec_lane, gam_lane, tA, lane);
       st.stash(buf0, lane);
     }
     // tiles in order, the next one prefetched across sub-group boundaries;
@@ -1657,6 +1664,15 @@ void k_update_f64_split(Launch L) {
 #pragma unroll
     for (int k = 0; k < D; ++k) xr[r][k] = rrow[k];
   }
+  // the sub-group's first tile loads with the rows, before the lane facts and
+  // the liveness verdict are known (in bounds either way; unused if no work)
+  const F64Tiling T(ncols);
+  const int tA = min(T.ct, g * T.tpg), tB = min(T.ct, g * T.tpg + T.tpg);
+  const int sA = min(tB, tA + q * T.tps), sB = min(tB, sA + T.tps);
+  const double* rec_lane = reinterpret_cast<const double*>(P.rec_col) + (size_t)s * P.padc * DP;
+  const double* gam_lane = reinterpret_cast<const double*>(P.gam_col) + (size_t)s * P.padc;
+  F64Stage<D> st;
+  if (sA < sB) st.fetch(rec_lane, gam_lane, sA, lane);
   bool fast = false;
   float M = 0.f;
   if (upd) {
@@ -1676,19 +1692,10 @@ void k_update_f64_split(Launch L) {
   }
   const double m0 = fast ? 0.0 : -(double)INFINITY;
   if (work) {
-    const F64Tiling T(ncols);
-    const int tA = min(T.ct, g * T.tpg), tB = min(T.ct, g * T.tpg + T.tpg);
-    const int sA = min(tB, tA + q * T.tps), sB = min(tB, sA + T.tps);
-    const double* rec_lane = reinterpret_cast<const double*>(P.rec_col) + (size_t)s * P.padc * DP;
-    const double* gam_lane = reinterpret_cast<const double*>(P.gam_col) + (size_t)s * P.padc;
     double mrun[R], srun[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) { mrun[r] = m0; srun[r] = 0.0; }
-    F64Stage<D> st;
-    if (sA < sB) {
-      st.fetch(rec_lane, gam_lane, sA, lane);
-      st.stash(sh_tile[q][0], lane);
-    }
+    if (sA < sB) st.stash(sh_tile[q][0], lane);
     for (int t = sA; t < sB; ++t) {
       const double* cur = sh_tile[q][(t - sA) & 1];
       double* nxt = sh_tile[q][((t - sA) & 1) ^ 1];
