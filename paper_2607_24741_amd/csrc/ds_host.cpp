@@ -147,7 +147,7 @@ ds::Layout plan(const ds_problem* pr, const ds_options* op, void* ws) {
   L.spart = L.es == 2 ? c.take<double2>((size_t)L.nslots * ds::kGroups * (size_t)L.rows)
                       : nullptr;
   L.kpart = mfree ? c.take<float2>((size_t)L.nslots * ds::kGroups * (size_t)L.rows) : nullptr;
-  L.scnt = L.nslots ? c.take<int>(2 * (size_t)L.nslots) : nullptr;
+  L.scnt = L.nslots ? c.take<int>((size_t)L.nslots) : nullptr;
   L.bytes = align_up(c.off, 256);
   return L;
 }
@@ -345,7 +345,7 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
   ia.mat = mat ? 1 : 0;
   ia.ctrl = L.ctrl;
   HIP_TRY(launch_ingest(ia, maxpad, st));
-  if (L.scnt) HIP_TRY(launch_zero_counters(L.scnt, 2 * L.nslots, st));
+  if (L.scnt) HIP_TRY(launch_zero_counters(L.scnt, L.nslots, st));
   HIP_TRY(launch_offsets(L.bank[0].slot, W, L.rows, L.off[0], L.off[1], L.bank[0].ord[0],
                          L.bank[0].ord[1], L.ctrl, st));
   Ctrl ctrl;

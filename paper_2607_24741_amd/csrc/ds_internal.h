@@ -193,7 +193,7 @@ struct Layout {
   RowCert* row64;    // guarded release: [W] latest verified row residual by caller lane
   double2* spart;    // float64 state: split-launch partials (see Launch::spart)
   float2* kpart;     // matrix-free large d: group partials (see Launch::kpart)
-  int* scnt;         // split launches: arrival counters [nslots][2]
+  int* scnt;         // split launches: arrival words [nslots]
   int nslots;        // work items the partials and counters hold
   int guard;
   size_t bytes;
@@ -263,7 +263,7 @@ struct Launch {
   double2* spart;                 // split float64 launch: group partials
                                   // [nslots][kGroups][rows]
   float2* kpart;                  // matrix-free large d: group partials [nslots][kGroups][rows]
-  int* scnt;                      // and per item [arrivals, skipped] [nslots][2], zero between launches
+  int* scnt;                      // and per item its arrival word [nslots], zero between launches
   int nslots;                     // items a launch of either kind may hold (both passes)
 };
 

@@ -95,6 +95,24 @@ __device__ __forceinline__ float2 ld_dev2(const float2* p) {
       __HIP_MEMORY_SCOPE_AGENT);
   return make_float2(__uint_as_float((unsigned)bits), __uint_as_float((unsigned)(bits >> 32)));
 }
+// Arrival of one block of a work item split over kGroups blocks, by one wave,
+// after its partials (or nothing, without work) were stored: one atomic on the
+// item's word, arrivals in its low 16 bits and blocks without work counted
+// above them. True for the last block to arrive, which clears the word for the
+// next launch (a plain device-scope store: nothing reads it again before this
+// launch ends); `skipped` says whether any block of the item had no work.
+__device__ __forceinline__ bool arrive_last(int* word, bool work, bool& skipped) {
+  __builtin_amdgcn_s_waitcnt(0);   // the partial stores are complete before the arrival counts
+  int prev = 0;
+  if ((threadIdx.x & 63) == 0) prev = atomicAdd(word, work ? 1 : 1 + (1 << 16));
+  prev = __builtin_amdgcn_readfirstlane(prev);
+  const bool last = (prev & 0xFFFF) + 1 == kGroups;
+  skipped = (prev >> 16) != 0 || !work;
+  if (last && (threadIdx.x & 63) == 0)
+    __hip_atomic_store(word, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return last;
+}
+
 // best-effort publication to pinned host memory (system scope, write-through)
 __device__ __forceinline__ void st_sys(int* p, int v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
@@ -1041,30 +1059,7 @@ void k_update_mfma_k(Launch L) {
       st_dev2(part + (size_t)g * BM + i, make_float2(gm, gs));
     }
   }
-  // arrival (the partials, or the skip mark, complete before it)
-  int last = 0, skipped = 0;
-  if (lane == 0) {
-    if (!work) atomicOr(&L.scnt[2 * it + 1], 1);
-    wait_mem();
-    const int prev = atomicAdd(&L.scnt[2 * it], 1);
-    last = prev + 1 == kGroups;
-    if (last) {
-      skipped = atomicExch(&L.scnt[2 * it + 1], 0);
-      atomicExch(&L.scnt[2 * it], 0);
-    }
-  } else {
-    wait_mem();
-  }
-  last = __builtin_amdgcn_readfirstlane(last);
-  skipped = __builtin_amdgcn_readfirstlane(skipped);
-  if (!last || skipped || !work) return;
-  // the item's finish: lane l owns rows row0 + l and row0 + 64 + l; every
-  // group partial is loaded before the first is used
-  float2 pg[2][kGroups];
-#pragma unroll
-  for (int e = 0; e < 2; ++e)
-#pragma unroll
-    for (int u = 0; u < kGroups; ++u) pg[e][u] = ld_dev2(part + (size_t)u * BM + 64 * e + lane);
+  // the finish's own row data loads with the arrival (its latency overlaps it)
   bool owner[2], live[2];
   float own_lm[2] = {0.f, 0.f}, own_w[2] = {0.f, 0.f}, own_lse[2], Mt[2] = {0.f, 0.f},
         St[2] = {0.f, 0.f};
@@ -1073,10 +1068,22 @@ void k_update_mfma_k(Launch L) {
     const int i = row0 + 64 * e + lane;
     owner[e] = i < nrows;
     own_lse[e] = P.lse_in[(size_t)s * P.padr + i];
-    if (owner[e]) {
+    if (owner[e] && work) {
       own_lm[e] = P.lm_row[(size_t)s * P.padr + i];
       own_w[e] = P.w_row[(size_t)si.lane * P.w_ld + i];
     }
+  }
+  bool skipped;
+  if (!arrive_last(&L.scnt[it], work, skipped) || skipped) return;
+  // the item's finish: lane l owns rows row0 + l and row0 + 64 + l; every
+  // group partial is loaded before the first is used
+  float2 pg[2][kGroups];
+#pragma unroll
+  for (int e = 0; e < 2; ++e)
+#pragma unroll
+    for (int u = 0; u < kGroups; ++u) pg[e][u] = ld_dev2(part + (size_t)u * BM + 64 * e + lane);
+#pragma unroll
+  for (int e = 0; e < 2; ++e) {
     live[e] = owner[e] && own_lse[e] != INFINITY;
     if (!owner[e]) continue;
     if (fast) {
@@ -1618,11 +1625,10 @@ __device__ __forceinline__ double ld_dev_d(const double* p) {
 // Arrival: every block of a placed item arrives exactly once, also one whose
 // waves found the item retired or the window finished (each wave reads that
 // on its own, so blocks of one item can disagree when a lane retires during
-// the launch): such a block marks the item skipped and the last arrival then
-// does not finish it. A check item whose lane the screen leaves unchecked (a
-// fact of the previous launch, the same for every block) is dropped by all of
-// its blocks before arriving. The last arrival clears both words for the next
-// launch.
+// the launch): such a block arrives marked skipped and the last arrival then
+// does not finish the item (arrive_last). A check item whose lane the screen
+// leaves unchecked (a fact of the previous launch, the same for every block)
+// is dropped by all of its blocks before arriving.
 template <int D>
 __global__ __launch_bounds__(64 * kSubGroups, (f64_waves_per_simd<D>()))
 void k_update_f64_split(Launch L) {
@@ -1730,28 +1736,25 @@ void k_update_f64_split(Launch L) {
       st_dev_d(dst + 1, gs);
     }
   }
-  // arrival (the partials, or the skip mark, complete before it)
-  int last = 0, skipped = 0;
-  if (lane == 0) {
-    if (!all) atomicOr(&L.scnt[2 * it + 1], 1);
-    wait_mem();
-    const int prev = atomicAdd(&L.scnt[2 * it], 1);
-    last = prev + 1 == kGroups;
-    if (last) {
-      skipped = atomicExch(&L.scnt[2 * it + 1], 0);
-      atomicExch(&L.scnt[2 * it], 0);
-    }
-  } else {
-    wait_mem();
-  }
-  last = __builtin_amdgcn_readfirstlane(last);
-  skipped = __builtin_amdgcn_readfirstlane(skipped);
-  if (!last || skipped || !all) return;
-  // the item's finish, as wave 0 of k_update_f64 does it; every partial is
-  // loaded before the first is used
+  // the finish's own row data loads with the arrival (its latency overlaps it)
   bool owner[R];
   double lm[R];
   float w[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int i = rb * ROWS + 64 * r + lane;
+    owner[r] = in_prefix[r];
+    lm[r] = 0.0;
+    w[r] = 0.f;
+    if (owner[r] && all) {
+      lm[r] = reinterpret_cast<const double*>(P.lm_row)[(size_t)s * P.padr + i];
+      w[r] = P.w_row[(size_t)si.lane * P.w_ld + i];
+    }
+  }
+  bool skipped;
+  if (!arrive_last(&L.scnt[it], all, skipped) || skipped) return;
+  // the item's finish, as wave 0 of k_update_f64 does it; every partial is
+  // loaded before the first is used
   double pm[R][kGroups], ps[R][kGroups];
 #pragma unroll
   for (int r = 0; r < R; ++r) {
@@ -1760,17 +1763,6 @@ void k_update_f64_split(Launch L) {
       const double* src = reinterpret_cast<const double*>(part + (size_t)u * ROWS + 64 * r + lane);
       pm[r][u] = ld_dev_d(src);
       ps[r][u] = ld_dev_d(src + 1);
-    }
-  }
-#pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const int i = rb * ROWS + 64 * r + lane;
-    owner[r] = in_prefix[r];
-    lm[r] = 0.0;
-    w[r] = 0.f;
-    if (owner[r]) {
-      lm[r] = reinterpret_cast<const double*>(P.lm_row)[(size_t)s * P.padr + i];
-      w[r] = P.w_row[(size_t)si.lane * P.w_ld + i];
     }
   }
   double Mt[R], St[R];
