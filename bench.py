@@ -264,7 +264,7 @@ def roofline(w, args, stats, T, traffic_summary):
     elif mat:
         per_pair, unit, peak, bound = 4.0, "GB/s", HBM_PEAK_GBS, "hbm"
         algo = "4 bytes of materialised cost per valid (i,j) term"
-        kname = "k_mat_rows / k_mat_cols (f- and g-half-steps)"
+        kname = "k_mat_rows (f-half over Q, g-half over its transpose)"
         scale = 1e9
     else:
         # FMA-equivalent flops of the vector-unit model: 2 (d + 4) per term

@@ -93,11 +93,11 @@ enum {
                            FORCE flag is given; the flag is kept so a caller can
                            require it (an error where it is unavailable). The
                            outputs stay float32.                                */
-  DS_F_MATERIALIZE = 32u, /* build the cost C (base-2 units, float32) once per call
-                           in the workspace and stream it from HBM in every
-                           half-step; the default for d > 32 when n_max, m_max
-                           <= 16384 (required here; W n_max m_max 4 bytes of
-                           workspace)                                            */
+  DS_F_MATERIALIZE = 32u, /* build the cost C (base-2 units, float32) and its
+                           transpose once per call in the workspace and stream
+                           them from HBM by rows in every half-step; the default
+                           for d > 32 when n_max, m_max <= 16384 (required here;
+                           2 W n_pad m_pad 4 bytes of workspace)                 */
   DS_F_GUARD = 64u,     /* guarded release (eq:release-contract in float64): the
                            release is decided on a float64 evaluation of both
                            marginals of exactly the float32 potentials the caller
@@ -113,7 +113,7 @@ enum {
                            residual met tol. Two extra launches per audit cycle;
                            n_max, m_max <= 16384.                                */
   DS_F_MATRIX_FREE = 256u, /* d > 32: recompute the cost per tile on the matrix
-                           cores (a K-looped contraction over d) instead of
+                           cores (an LDS-tiled contraction over d) instead of
                            materialising it; the default when a side has more
                            than 16384 points. Float32 state. Exclusive with
                            DS_F_MATERIALIZE.                                     */

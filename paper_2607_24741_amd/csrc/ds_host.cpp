@@ -132,6 +132,7 @@ ds::Layout plan(const ds_problem* pr, const ds_options* op, void* ws) {
   L.off[1] = c.take<int>(W + 1);
   L.ctrl = c.take<ds::Ctrl>(1);
   L.Q = L.mat ? c.take<float>(W * (size_t)L.pad[0] * (size_t)L.pad[1]) : nullptr;
+  L.QT = L.mat ? c.take<float>(W * (size_t)L.pad[0] * (size_t)L.pad[1]) : nullptr;
   L.guard = (op->flags & DS_F_GUARD) ? 1 : 0;
   for (int side = 0; side < 2; ++side) {
     L.agg64[side] = L.guard ? c.take<double2>(W * (size_t)L.rbmax) : nullptr;
@@ -361,7 +362,7 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
   }
   if (mat) {
     CostArgs ca;
-    ca.X = pr->X; ca.Y = pr->Y; ca.center = L.center; ca.slot = L.bank[0].slot; ca.Q = L.Q;
+    ca.X = pr->X; ca.Y = pr->Y; ca.center = L.center; ca.slot = L.bank[0].slot; ca.Q = L.Q; ca.QT = L.QT;
     ca.W = W; ca.n_max = pr->n_max; ca.m_max = pr->m_max; ca.d = d;
     ca.pad0 = L.pad[0]; ca.pad1 = L.pad[1];
     HIP_TRY(launch_cost(ca, st));
@@ -438,7 +439,8 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
     l.audit = L.audit; l.vcnt = L.vcnt; l.ctrl = L.ctrl;
     l.hsnap = R->snap_dev; l.nchk = L.nchk; l.disc = L.disc;
     l.progress = &R->snap_dev->progress;
-    l.Q = L.Q; l.q_lane = (size_t)L.pad[0] * L.pad[1]; l.q_ld = L.pad[1];
+    l.Q = L.Q; l.QT = L.QT; l.q_lane = (size_t)L.pad[0] * L.pad[1]; l.q_ld = L.pad[1];
+    l.qt_ld = L.pad[0];
     l.spart = L.spart; l.kpart = L.kpart; l.scnt = L.scnt; l.nslots = L.nslots;
     return l;
   };

@@ -186,6 +186,7 @@ struct Layout {
   int* off[2];       // work item offsets per role [W + 1]
   Ctrl* ctrl;
   float* Q;          // materialised cost [W][pad0][pad1] by caller lane, base-2 units
+  float* QT;         // its transpose [W][pad1][pad0]
   double2* agg64[2]; // guarded checks: per row block float64 partials [W][rbmax] (else null)
   float4* gerr[2];   // guarded release, float64 state: per caller lane and row block
                      // [W][rbmax] {sum of mass x export rounding, max export rounding,
@@ -256,8 +257,10 @@ struct Launch {
   int* nchk;                      // [W] check passes per caller lane
   float* disc;                    // [W] shadow mode: screen discrepancy per caller lane (else null)
   const float* Q;                 // materialised cost (caller lane l at Q + l * q_lane)
+  const float* QT;                // and its transpose, the same size
   size_t q_lane;                  // floats per lane
   int q_ld;                       // row stride of Q (padded target count)
+  int qt_ld;                      // row stride of QT (padded source count)
   int* progress;                  // &hsnap->progress as the device addresses it (may be null)
   int seqno;                      // launch sequence number written there
   double2* spart;                 // split float64 launch: group partials
@@ -354,7 +357,8 @@ struct CostArgs {
   const float* X; const float* Y;
   const float* center;
   const SlotInfo* slot;   // ingest layout: slot t = caller lane t
-  float* Q;
+  float* Q;               // [W][pad0][pad1]
+  float* QT;              // [W][pad1][pad0] its transpose
   int W, n_max, m_max, d, pad0, pad1;
 };
 hipError_t launch_cost(const CostArgs& a, hipStream_t st);

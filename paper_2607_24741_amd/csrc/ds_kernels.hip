@@ -30,10 +30,11 @@
 //                     LDS) with the streaming sum as its epilogue, one block
 //                     per (work item, column group) (d > 32 without a
 //                     materialised cost).
-//  k_cost, k_mat_rows, k_mat_cols
-//                     the materialised cost: built once on the matrix cores,
-//                     then streamed from HBM by both half-steps (the default
-//                     for d > 32 up to 16384 points a side).
+//  k_cost, k_mat_rows
+//                     the materialised cost: built once on the matrix cores
+//                     (with its transpose), then streamed by rows from HBM by
+//                     both half-steps (the default for d > 32 up to 16384
+//                     points a side).
 //  k_check64<DR>      float64 verification of the exported potentials (guarded
 //                     release).
 //  k_offsets, k_scan  one block: the work item order and offsets of the
@@ -1787,18 +1788,21 @@ void k_update_f64_split(Launch L) {
 // For large d (or on request) the cost of every lane is built once in base-2
 // units, Q_ij = kappa ||x_i - y_j||^2, and the half-steps stream it from HBM:
 //     lse_i = log2 sum_j 2^(gam_j - Q_ij)   (f-half: rows of Q)
-//     lse_j = log2 sum_i 2^(gam_i - Q_ij)   (g-half: columns of Q)
+//     lse_j = log2 sum_i 2^(gam_i - Q_ij)   (g-half: rows of Q^T)
 // where gam = kappa * potential (no quadratic fold: no point records exist).
-// Q is indexed by caller lane and never moved by compaction. Both kernels use
-// 64-row work items, eight waves, and the column operand staged in LDS.
+// Q and Q^T are indexed by caller lane and never moved by compaction. One
+// kernel serves both half-steps: 64-row work items, eight waves, and the
+// column operand staged in LDS.
 
 // Build: one 128 x 128 tile of a lane's cost per block. The centred
 // coordinates of the tile's rows and columns are staged in LDS kMfreeK at a
 // time (double-buffered, as in the matrix-free half-step), x~ . y~ runs on the
 // matrix cores (four waves of 64 x 64), and every thread also sums the squares
 // of one row's (tid < 128) or one column's staged coordinates in order; then
-// Q = kappa (|x|^2 + |y|^2 - 2 x.y) clamped at 0. The padded region is written
-// too (zero coordinates), so every entry a half-step can touch is finite.
+// Q = kappa (|x|^2 + |y|^2 - 2 x.y) clamped at 0, stored twice: Q by rows of
+// x for the f-half and its transpose for the g-half, so that both half-steps
+// stream contiguous rows. The padded region is written too (zero
+// coordinates), so every entry a half-step can touch is finite.
 //
 // Staging: thread t moves coordinate t % 32 of the stage for rows t / 32 + 8 u
 // (u < 16) of both operands -- 32 threads read one row's 128 contiguous bytes
@@ -1929,6 +1933,11 @@ __global__ __launch_bounds__(256, 2) void k_cost(CostArgs c) {
   __syncthreads();
   const float kap = si.kappa;
   float* Qt = c.Q + (size_t)t * c.pad0 * c.pad1 + (size_t)ti * T * c.pad1 + (size_t)tj * T;
+  // the tile also goes through LDS (rows at an odd stride: conflict-free both
+  // ways), to be written transposed with coalesced stores
+  constexpr int LT = T + 1;
+  static_assert(T * LT <= 2 * STAGE, "the transposed tile fits in the stage buffers");
+  float* tl = sh;   // the stages are done (the barrier above)
   // lane l holds D[i][j] of column j = l % 32 of its tile and rows
   // i = 8 (v / 4) + 4 (l / 32) + v % 4
 #pragma unroll
@@ -1940,14 +1949,31 @@ __global__ __launch_bounds__(256, 2) void k_cost(CostArgs c) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int i = wr * 64 + a * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
-        Qt[(size_t)i * c.pad1 + j] = kap * fmaxf(sh_nrm[i] + ny - 2.f * acc[a][b][v], 0.f);
+        const float q = kap * fmaxf(sh_nrm[i] + ny - 2.f * acc[a][b][v], 0.f);
+        Qt[(size_t)i * c.pad1 + j] = q;
+        tl[i * LT + j] = q;
       }
     }
   }
+  __syncthreads();
+  // Q^T: thread t writes half of row j = t / 2 of the transposed tile, 64
+  // consecutive i (the two threads of a row write its 512 contiguous bytes)
+  float* QTt = c.QT + (size_t)t * c.pad0 * c.pad1 + (size_t)tj * T * c.pad0 + (size_t)ti * T;
+  const int j = tid >> 1, i0 = (tid & 1) * 64;
+#pragma unroll
+  for (int q = 0; q < 64; q += 4) {
+    float4 v;
+    v.x = tl[(i0 + q) * LT + j];
+    v.y = tl[(i0 + q + 1) * LT + j];
+    v.z = tl[(i0 + q + 2) * LT + j];
+    v.w = tl[(i0 + q + 3) * LT + j];
+    *reinterpret_cast<float4*>(QTt + (size_t)j * c.pad0 + i0 + q) = v;
+  }
 }
 
-// f-half (and the final row check): wave w sweeps rows w, w+8, .. of the
-// item, its lanes striding over the columns four at a time.
+// A half-step (and the marginal check) over the rows of Q (f-half) or of Q^T
+// (g-half): wave w sweeps rows w, w+8, .. of the item, its lanes striding
+// over the columns four at a time.
 __global__ __launch_bounds__(512, 2) void k_mat_rows(Launch L) {
   note_progress(L);
   extern __shared__ __align__(16) float sh_gam[];   // the lane's column operand (padc floats)
@@ -2017,7 +2043,7 @@ __global__ __launch_bounds__(512, 2) void k_mat_rows(Launch L) {
       // kRowBatch loads of the row in flight before the first is used (one
       // at a time left each wave waiting for memory on every step); the sum
       // takes the steps in column order
-      constexpr int kRowBatch = 4;
+      constexpr int kRowBatch = 8;
       int j = 4 * lane;
       for (; j + 256 * (kRowBatch - 1) < nc4; j += 256 * kRowBatch) {
         float4 qv[kRowBatch];
@@ -2048,115 +2074,6 @@ __global__ __launch_bounds__(512, 2) void k_mat_rows(Launch L) {
   const float St = (mt.x == -INFINITY) ? 0.f : mt.y * ex2(mt.x - Mt);
   finish_rows<kRowsValu, 1, float>(L, P, s, si, rb, owner, owner && lse_own != INFINITY, fast, M,
                                    lse_own, lm, w, Mt, St, rhat);
-}
-
-// g-half (and the column check): lane l owns target point j = rb * 64 + l
-// (a column of Q); the eight waves split the source points into contiguous
-// chunks, merged per lane in chunk order.
-__global__ __launch_bounds__(512, 2) void k_mat_cols(Launch L) {
-  note_progress(L);
-  extern __shared__ __align__(16) float sh_gam[];   // the lane's column operand (padc floats)
-  __shared__ float2 sh_part[8][kRowsValu];
-  const int b = blockIdx.x;
-  const int pi = b >= L.nb0;
-  const Pass P = L.p[pi];
-  int s, rb, nrows, ncols, c_fin, c_A;     // rows: target points, columns: source points
-  SlotInfo si;
-  if (!place_item<1>(L, P, pass_blocks(L, pi), pi ? b - L.nb0 : b, s, rb, nrows, ncols, si, c_fin,
-                     c_A))
-    return;
-  const bool upd = P.kind == KIND_UPDATE;
-  float rhat = NAN;
-  if (!upd) {
-    const bool chk = check_facts(L, P, s, P.role ? ncols : nrows, rhat);
-    if (!item_live(L, P, s, si, c_fin, c_A) || !chk) return;
-  }
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const float* gcol = P.gam_col + (size_t)s * P.padc;
-  for (int i = threadIdx.x; i < ncols; i += blockDim.x) sh_gam[i] = gcol[i];
-  const int j = rb * kRowsValu + lane;
-  const bool in_prefix = j < nrows;
-  const size_t jdx = (size_t)s * P.padr + j;
-  const float lse_old = P.lse_in[jdx];
-  const bool owner = wave == 0 && in_prefix;
-  float lm = 0.f, w = 0.f;
-  if (owner) lm = P.lm_row[jdx];
-  bool fast = false;
-  float M = 0.f;
-  if (upd) {
-    update_facts(L, P, s, ncols, fast, M);
-    if (!item_live(L, P, s, si, c_fin, c_A)) return;
-  }
-  if (owner) w = P.w_row[(size_t)si.lane * P.w_ld + j];   // caller masses, by lane id
-  const bool live = in_prefix && lse_old != INFINITY;
-  float bias = 0.f;
-  if (live) {
-    if (!upd) bias = -lse_old;
-    else if (fast) bias = -(lse_old + M);
-  }
-  __syncthreads();
-  const int ch = (ncols + 7) / 8;
-  const int i0 = min(ncols, wave * ch), i1 = min(ncols, i0 + ch);
-  const float* q = L.Q + (size_t)si.lane * L.q_lane + j;
-  float mrun = fast ? 0.f : -INFINITY, srun = 0.f;
-  // the column is read kColBatch rows at a time, every load of a batch issued
-  // before the first is used (one dependent load per row left each wave
-  // waiting for memory on every term); the sums take the terms in row order
-  constexpr int kColBatch = 16;
-  if (fast) {
-    // even rows of the chunk into sa, odd ones into sb
-    float sa = 0.f, sb = 0.f;
-    int i = i0;
-    for (; i + kColBatch <= i1; i += kColBatch) {
-      float qv[kColBatch];
-#pragma unroll
-      for (int u = 0; u < kColBatch; ++u) qv[u] = q[(size_t)(i + u) * L.q_ld];
-#pragma unroll
-      for (int u = 0; u < kColBatch; u += 2) {
-        sa += ex2((sh_gam[i + u] + bias) - qv[u]);
-        sb += ex2((sh_gam[i + u + 1] + bias) - qv[u + 1]);
-      }
-    }
-    for (; i + 1 < i1; i += 2) {
-      const float q0 = q[(size_t)i * L.q_ld], q1 = q[(size_t)(i + 1) * L.q_ld];
-      sa += ex2((sh_gam[i] + bias) - q0);
-      sb += ex2((sh_gam[i + 1] + bias) - q1);
-    }
-    if (i < i1) sa += ex2((sh_gam[i] + bias) - q[(size_t)i * L.q_ld]);
-    srun = sa + sb;
-  } else {
-    auto term = [&](int i, float qi) {
-      const float z = (sh_gam[i] + bias) - qi;
-      const float mn = fmaxf(mrun, z);
-      const float mref = (mn == -INFINITY) ? 0.f : mn;
-      srun = srun * ex2(mrun - mref) + ex2(z - mref);
-      mrun = mn;
-    };
-    int i = i0;
-    for (; i + kColBatch <= i1; i += kColBatch) {
-      float qv[kColBatch];
-#pragma unroll
-      for (int u = 0; u < kColBatch; ++u) qv[u] = q[(size_t)(i + u) * L.q_ld];
-#pragma unroll
-      for (int u = 0; u < kColBatch; ++u) term(i + u, qv[u]);
-    }
-    for (; i < i1; ++i) term(i, q[(size_t)i * L.q_ld]);
-  }
-  sh_part[wave][lane] = make_float2(mrun, srun);   // (-inf, 0) for an empty chunk
-  __syncthreads();
-  if (wave != 0) return;
-  float Mt = 0.f, St = 0.f;
-  if (owner) {
-    float mx = -INFINITY;
-#pragma unroll
-    for (int g = 0; g < 8; ++g) mx = fmaxf(mx, sh_part[g][lane].x);
-    Mt = (mx == -INFINITY) ? 0.f : mx;
-#pragma unroll
-    for (int g = 0; g < 8; ++g) St += sh_part[g][lane].y * ex2(sh_part[g][lane].x - Mt);
-  }
-  finish_rows<kRowsValu, 1, float>(L, P, s, si, rb, owner, owner && live, fast, M, lse_old, lm, w,
-                                   Mt, St, rhat);
 }
 
 // ------------------------------------------------------------- block scan
@@ -3066,13 +2983,14 @@ hipError_t launch_update_mat(const Launch& a, int blocks, hipStream_t st, hipEve
   std::call_once(once, [] {
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k_mat_rows),
                               hipFuncAttributeMaxDynamicSharedMemorySize, kMatMaxPts * 4);
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k_mat_cols),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, kMatMaxPts * 4);
   });
-  if (a.p[0].role == 0)
-    hipExtLaunchKernelGGL(k_mat_rows, dim3(blocks), dim3(512), lds, st, e0, e1, 0, a);
-  else
-    hipExtLaunchKernelGGL(k_mat_cols, dim3(blocks), dim3(512), lds, st, e0, e1, 0, a);
+  // the g-half (and column check) streams the rows of the transposed cost
+  Launch b = a;
+  if (a.p[0].role == 1) {
+    b.Q = a.QT;
+    b.q_ld = a.qt_ld;
+  }
+  hipExtLaunchKernelGGL(k_mat_rows, dim3(blocks), dim3(512), lds, st, e0, e1, 0, b);
   return hipGetLastError();
 }
 hipError_t launch_check64(const Launch& a, const GuardArgs& g, int blocks, hipStream_t st) {
