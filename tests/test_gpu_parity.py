@@ -131,11 +131,11 @@ def test_matrix_free_large_d_reduced_ragged():
     _case("c4-reduced-matrix-free", w, 1e-3, flags=F_MATRIX_FREE)
 
 
-def _wide_large_d(n, m, seed):
-    """Two d = 40 lanes, one with many source points and one with many target
-    points (a long column operand for each half-step)."""
+def _wide_large_d(n, m, seed, d=40):
+    """Two large-d lanes (d = 40 unless given), one with many source points and
+    one with many target points (a long column operand for each half-step)."""
     rng = np.random.default_rng(seed)
-    W, d = 2, 40
+    W = 2
     n, m = np.array(n, np.int32), np.array(m, np.int32)
     n_max, m_max = int(n.max()), int(m.max())
     X = np.full((W, n_max, d), np.nan, np.float32)
@@ -157,6 +157,16 @@ def test_large_d_beyond_the_materialised_limit():
     source points and one with 16400 target points)."""
     w = _wide_large_d([16500, 300], [200, 16400], 17)
     _case("large-d beyond 16384 points", w, 1e-3)
+
+
+@pytest.mark.parametrize("flags", [0, F_MATRIX_FREE], ids=["materialised", "matrix-free"])
+def test_large_d_odd_dimension(flags):
+    """d = 37 (neither even nor a multiple of the 32-coordinate stages): the
+    zero-padded point records of the matrix-free kernel, the clamped loads of
+    the cost build and the centre's partial coordinate block, on ragged
+    NaN-padded lanes."""
+    w = _wide_large_d([300, 170], [130, 260], 23, d=37)
+    _case("large-d odd dimension", w, 1e-3, flags=flags)
 
 
 def test_materialised_cost_long_column_operand():
