@@ -166,8 +166,7 @@ typedef struct {
  * launch latencies of one sub-batch overlap the work of the others. Automatic:
  * one sub-batch below 32 lanes, in the static and logical modes (they share
  * one final cycle across the window) and with the materialised cost;
- * otherwise three when W * n_max * m_max * (2 ceil(d/2) + 2) >= 8e8, else
- * two. ds_workspace_bytes accounts for the split. */
+ * otherwise two. ds_workspace_bytes accounts for the split. */
 
 /* Outputs, in caller lane order. Device pointers. */
 typedef struct {

@@ -728,19 +728,14 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
 // so the results are those of one batch bit for bit; the launch latencies of
 // one sub-batch overlap the work of the others. Active mode only (the static
 // and logical modes share one final cycle across the window).
-// Automatic sub-batch count, from the window's padded work per cycle (terms
-// times the contraction length K = 2 ceil(d/2) + 2): a third concurrent
-// sub-batch pays off once a cycle is large enough to hide its launches behind
-// the other two. Measured on the mixture (d = 8, 1024^2) and telemetry (d = 16,
-// 512^2) windows at W = 32..256: two sub-batches were fastest from 3.4e8 to
-// 6.7e8 term-K per cycle, three from 9.1e8.
+// Automatic sub-batch count: two from 32 lanes on. Measured solves (ms) with
+// one, two and three sub-batches: mixture window (W = 64, d = 8) 289 / 259 / --,
+// telemetry (W = 256, d = 16) 529 / 461 / 469, LiDAR-shaped (W = 1024, d = 3)
+// 1870 / 1839 / 1846.
 int parts_of(const ds_problem* pr, const ds_options* op) {
   if (op->streams > 0) return std::min(op->streams, pr->W);
   if (op->mode != DS_MODE_ACTIVE || uses_mat(pr, op)) return 1;
-  if (pr->W < 32) return 1;
-  const double K = 2.0 * ((pr->d + 1) / 2) + 2.0;
-  const double work = (double)pr->W * pr->n_max * pr->m_max * K;
-  return work >= 8.0e8 ? 3 : 2;
+  return pr->W < 32 ? 1 : 2;
 }
 int part_lo(const ds_problem* pr, int parts, int p) {
   return (int)((int64_t)pr->W * p / parts);

@@ -158,16 +158,15 @@ def test_sub_batch_validation_and_size():
              for w in (21, 21, 22)]
     three = _bytes(_problem(W=64), ds._options(1e-3, None, 100, 1, "active", 0, 3))[1]
     assert three == sum(parts) and three >= one
-    # automatic: one below 32 lanes; from 32 lanes two, or three once the padded
-    # work per cycle W * n_max * m_max * (2 ceil(d/2) + 2) reaches 8e8
+    # automatic: one below 32 lanes, two from 32 lanes on (active mode)
     def auto_is(pr, k):
         a = _bytes(pr, ds._options(1e-3, None, 100, 1, "active", 0, 0))[1]
         return a == _bytes(pr, ds._options(1e-3, None, 100, 1, "active", 0, k))[1]
     assert auto_is(_problem(W=16), 1)
-    assert auto_is(_problem(W=40), 2)                                  # 40*100*90*6 = 2.2e6
-    assert auto_is(_problem(W=64, n_max=1024, m_max=1024, d=8), 2)    # 6.7e8
-    assert auto_is(_problem(W=96, n_max=1024, m_max=1024, d=8), 3)    # 1.0e9
-    assert auto_is(_problem(W=256, n_max=512, m_max=512, d=16), 3)    # 1.2e9
+    assert auto_is(_problem(W=40), 2)
+    assert auto_is(_problem(W=64, n_max=1024, m_max=1024, d=8), 2)
+    assert auto_is(_problem(W=256, n_max=512, m_max=512, d=16), 2)
+    assert auto_is(_problem(W=1024, n_max=256, m_max=256, d=3), 2)
 
 
 def test_guarded_release_validation_and_size():

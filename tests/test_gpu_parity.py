@@ -220,8 +220,8 @@ def test_features_full_size_sampled():
 
 def test_lidar_full_size_sampled():
     """Full LiDAR-shaped window (W=1024; n, m uniform on 256..8192, padded to
-    8192; d=3; per-lane eps on 0.005..0.1; tol 1e-3) in its benchmark launch
-    configuration (three sub-batches, mixed lane shapes): (i) fixed work, 8
+    8192; d=3; per-lane eps on 0.005..0.1; tol 1e-3) in the library's
+    automatic launch configuration (two sub-batches, mixed lane shapes): (i) fixed work, 8
     cycles: the lane nearest 2048 x 2048 points against the oracle's state;
     (ii) a real solve: the six smallest lanes against the oracle (depths,
     potentials, residuals), the largest lane's returned potentials
@@ -246,7 +246,7 @@ def test_lidar_full_size_sampled():
     log("[case] c5 full size tol 1e-3")
     g = run_gpu(w, 1e-3)
     st = g["stats"]
-    assert st.sub_batches == 3
+    assert st.sub_batches == 2
     conv = g["status"] == oracle.CONVERGED
     assert np.all(conv | ((g["status"] == oracle.MAX_ITER) & (g["depth"] == 5000)))
     assert np.all(g["residual"][conv] <= 1e-3)
