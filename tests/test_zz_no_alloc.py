@@ -58,6 +58,22 @@ def test_noalloc_matches_solve_on_two_calls():
         log(f"[case] noalloc {name}: depths {got[2].cpu().tolist()}")
 
 
+@pytest.mark.parametrize("path", ["matrix-free", "materialised"])
+def test_noalloc_large_d_paths(path):
+    """The large-d paths through the fixed array: the matrix-free kernel's
+    group partials and arrival words, and the materialised cost with its
+    transpose, all live in it; bit for bit equal to ds_solve."""
+    import paper_2607_24741_amd as ds
+    w = wl.make("c4", W=3, n=200, m=180, hetero=(90, 200), pad_value=np.nan)
+    flags = ds.F_MATRIX_FREE if path == "matrix-free" else 0
+    log(f"[case] noalloc large d ({path}): W={w.W} n_max={w.X.shape[1]} d={w.d}")
+    ref, got = _pair(w, 1e-3, flags=flags)
+    for i, k in enumerate(KEYS):
+        assert got[i].equal(ref[i]), k
+    assert int((got[4] == 0).sum()) == w.W
+    log(f"[case] noalloc large d ({path}): depths {got[2].cpu().tolist()}")
+
+
 def test_noalloc_refuses_a_window_beyond_its_array():
     import torch
     import paper_2607_24741_amd as ds
