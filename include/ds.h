@@ -110,8 +110,11 @@ enum {
                            lanes to verify: only those that could meet tol. With
                            a float32 state every audited lane is verified. The
                            column marginal is evaluated only for lanes whose row
-                           residual met tol. Two extra launches per audit cycle;
-                           n_max, m_max <= 16384.                                */
+                           residual met tol. Three extra launches per audit cycle;
+                           the workspace grows by about 8 KB per 128-row block
+                           and lane with the float64 state (2 KB per 32-row
+                           block with a float32 state) for the verification's
+                           per-row chunk sums; n_max, m_max <= 16384.            */
   DS_F_MATRIX_FREE = 256u, /* d > 32: recompute the cost per tile on the matrix
                            cores (an LDS-tiled contraction over d) instead of
                            materialising it; the default when a side has more

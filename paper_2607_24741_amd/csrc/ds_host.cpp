@@ -9,8 +9,10 @@
 //           block of each checked lane takes its decision on the device
 //           (verifier-gated: the screen alone never retires a lane) and a
 //           retired lane's work items stop running at once.
-// With guarded release a float64 verification launch between the two halves
-// takes the decision instead of the float32 column check.
+// With guarded release float64 verification launches between the two halves
+// (the lanes the outward bound admits, their row marginal, then the column
+// marginal of those whose row residual met tol) take the decision instead of
+// the float32 column check.
 // The host never waits per cycle: the device publishes its control state
 // (retirements, survivor widths, a progress word) to pinned host memory, and
 // when it shows retirements the host launches the compaction (scan + gather
@@ -139,6 +141,12 @@ ds::Layout plan(const ds_problem* pr, const ds_options* op, void* ws) {
     L.gerr[side] = (L.guard && L.es == 2) ? c.take<float4>(W * (size_t)L.rbmax) : nullptr;
   }
   L.row64 = L.guard ? c.take<ds::RowCert>(W) : nullptr;
+  L.vpart = L.guard ? c.take<double>(W * (size_t)L.rbmax * ds::kVChunks * (size_t)L.rows)
+                    : nullptr;
+  L.vscnt = L.guard ? c.take<int>(W * (size_t)L.rbmax) : nullptr;
+  for (int role = 0; role < 2; ++role)
+    L.vlist[role] = L.guard ? c.take<int>(W * (size_t)L.rbmax) : nullptr;
+  L.vlen = L.guard ? c.take<int>(2) : nullptr;
   // partials and arrival words of the launches that split a work item over
   // blocks: the float64 state's narrow launches (at most kSplitSlots items),
   // and every launch of the matrix-free large-d kernel (both passes: at most
@@ -347,6 +355,8 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
   ia.ctrl = L.ctrl;
   HIP_TRY(launch_ingest(ia, maxpad, st));
   if (L.scnt) HIP_TRY(launch_zero_counters(L.scnt, L.nslots, st));
+  if (L.vscnt) HIP_TRY(launch_zero_counters(L.vscnt, W * L.rbmax, st));
+  if (L.vlen) HIP_TRY(launch_zero_counters(L.vlen, 2, st));
   HIP_TRY(launch_offsets(L.bank[0].slot, W, L.rows, L.off[0], L.off[1], L.bank[0].ord[0],
                          L.bank[0].ord[1], L.ctrl, st));
   Ctrl ctrl;
@@ -407,8 +417,8 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
     u.role = role; u.kind = kind;
     return u;
   };
-  // float64 verification launches (guarded release): pass 0 is the row marginal
-  // (rows = x), pass 1 the column marginal
+  // float64 verification launches (guarded release), by role: 0 the row
+  // marginal (rows = x), 1 the column marginal
   GuardArgs ga;
   std::memset(&ga, 0, sizeof(ga));
   for (int role = 0; role < 2; ++role) {
@@ -422,6 +432,8 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
     ga.gerr[role] = L.gerr[role];
   }
   ga.row64 = L.row64;
+  ga.vpart = L.vpart; ga.vscnt = L.vscnt;
+  ga.vlist[0] = L.vlist[0]; ga.vlist[1] = L.vlist[1]; ga.vlen = L.vlen;
   ga.eps = pr->eps; ga.d = pr->d; ga.es = L.es;
   // with the float64 state the update kernels bound how far rounding to the
   // float32 outputs moves the residual, and only lanes within that bound of
@@ -597,13 +609,12 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
       lc.p[0] = make_pass(0, 1, pk1, pk1, pk1);
       lc.p[0].depth = k - 1;
       lc.p[0].verify_all = shadow ? 1 : 0;
-      lc.nb0 = std::max(items[0], 0);
-      HIP_TRY(launch_check64(lc, ga, lc.nb0, st));
+      HIP_TRY(launch_vgate(lc, ga, st));
+      HIP_TRY(launch_verify64(lc, ga, items[0], st));
       Launch lk = make_launch();
-      lk.p[1] = make_pass(1, 1, pk1, pk1, pk1);
-      lk.p[1].depth = k - 1;
-      lk.nb0 = 0;
-      HIP_TRY(launch_check64(lk, ga, std::max(items[1], 0), st));
+      lk.p[0] = make_pass(1, 1, pk1, pk1, pk1);
+      lk.p[0].depth = k - 1;
+      HIP_TRY(launch_verify64(lk, ga, items[1], st));
     }
     if (audit_prev && shadow && !guard) {
       // shadow mode: the row marginal of state k-1 recomputed by a dedicated
@@ -657,16 +668,15 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
     if (guard) {
       // both marginals of state K in float64, every lane still running (the
       // column launch decides)
-      Launch lc = make_launch();
+      Launch lc = make_launch(), lk = make_launch();
       lc.p[0] = make_pass(0, 1, pK, pK, pK);
-      lc.p[1] = make_pass(1, 1, pK, pK, pK);
-      for (Pass& q : lc.p) {
-        q.final_audit = 1; q.depth = K; q.verify_all = 1; q.decide = 1;
+      lk.p[0] = make_pass(1, 1, pK, pK, pK);
+      for (Pass* q : {&lc.p[0], &lk.p[0]}) {
+        q->final_audit = 1; q->depth = K; q->verify_all = 1; q->decide = 1;
       }
-      lc.nb0 = ctrl.items_f;
-      HIP_TRY(launch_check64(lc, ga, ctrl.items_f, st));
-      lc.nb0 = 0;
-      HIP_TRY(launch_check64(lc, ga, ctrl.items_g, st));
+      HIP_TRY(launch_vgate(lc, ga, st));
+      HIP_TRY(launch_verify64(lc, ga, ctrl.items_f, st));
+      HIP_TRY(launch_verify64(lk, ga, ctrl.items_g, st));
     } else {
       Launch lv = make_launch();
       lv.p[0] = make_pass(0, 1, pK, pK, pK);

@@ -56,6 +56,12 @@ constexpr int kMfreeCols = 128;  // columns per step of the matrix-free large-d 
 // coordinates per LDS stage of the matrix-free large-d kernel; its point
 // records are padded to a multiple of this with zeros
 constexpr int kMfreeK = 32;
+// Float64 verification (guarded release): the columns of a lane are cut into
+// kVChunks fixed chunks, each summed per row on its own and the chunk sums
+// added in chunk order; a verification launch strides at most kVerifyBlocks
+// blocks over the (row block, chunk) units of the rows it verifies.
+constexpr int kVChunks = 8;
+constexpr int kVerifyBlocks = 2048;
 constexpr int kMaxW = 4096;
 constexpr int kMaxDSmall = 32;   // matrix-free kernels
 constexpr int kMaxDF64 = 16;     // matrix-free float64-state kernels
@@ -192,6 +198,10 @@ struct Layout {
                      // [W][rbmax] {sum of mass x export rounding, max export rounding,
                      // sum of mass, 0} of each side's potentials (else null)
   RowCert* row64;    // guarded release: [W] latest verified row residual by caller lane
+  double* vpart;     // guarded checks: [W][rbmax][kVChunks][rows] per-row chunk sums (else null)
+  int* vscnt;        // and their arrival words [W][rbmax], zero between launches
+  int* vlist[2];     // guarded checks: the row blocks to verify per pass [W * rbmax]
+  int* vlen;         // and their counts [2]
   double2* spart;    // float64 state: split-launch partials (see Launch::spart)
   float2* kpart;     // matrix-free large d: group partials (see Launch::kpart)
   int* scnt;         // split launches: arrival words [nslots]
@@ -280,6 +290,11 @@ struct GuardArgs {
   double2* agg64[2];      // [W][rbmax] per row block {sum |marginal - mass|, non-finite}
   const float4* gerr[2];  // export rounding per side (float64 state), see Layout::gerr
   RowCert* row64;         // [W] row residual of the audit, read by its column check
+  double* vpart;          // [W][rbmax][kVChunks][rows] per-row chunk sums of a launch
+  int* vscnt;             // [W][rbmax] their arrival words (zero between launches)
+  int* vlist[2];          // per pass: the items to verify, slot * rbmax + row block
+                          // (bit 30: the outward bound had excluded the lane)
+  int* vlen;              // [2] the lists' lengths
   const float* eps;       // caller eps [W]
   int d, es;              // point dimension; state element size in floats
   int bound;              // 1: gate the row check by the outward bound (float64
@@ -363,7 +378,8 @@ struct CostArgs {
 };
 hipError_t launch_cost(const CostArgs& a, hipStream_t st);
 // float64 two-sided check of the audited state (both marginals, two passes)
-hipError_t launch_check64(const Launch& a, const GuardArgs& g, int blocks, hipStream_t st);
+hipError_t launch_vgate(const Launch& a, const GuardArgs& g, hipStream_t st);
+hipError_t launch_verify64(const Launch& a, const GuardArgs& g, int items, hipStream_t st);
 hipError_t launch_scan(const ScanArgs& a, hipStream_t st);
 hipError_t launch_offsets(SlotInfo* slot, int A, int rows, int* off_f, int* off_g, int* ord_f,
                           int* ord_g, Ctrl* ctrl, hipStream_t st);

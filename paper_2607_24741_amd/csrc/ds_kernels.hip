@@ -35,8 +35,11 @@
 //                     (with its transpose), then streamed by rows from HBM by
 //                     both half-steps (the default for d > 32 up to 16384
 //                     points a side).
-//  k_check64<DR>      float64 verification of the exported potentials (guarded
-//                     release).
+//  k_vgate, k_verify64<DR>
+//                     float64 verification of the exported potentials (guarded
+//                     release): the lanes the outward bound admits, then their
+//                     row and column marginals over (row block, column chunk)
+//                     units.
 //  k_offsets, k_scan  one block: the work item order and offsets of the
 //                     initial layout (longest sweeps first); the compaction
 //                     map (survivor ranks, the orders filtered, new offsets)
@@ -96,18 +99,20 @@ __device__ __forceinline__ float2 ld_dev2(const float2* p) {
       __HIP_MEMORY_SCOPE_AGENT);
   return make_float2(__uint_as_float((unsigned)bits), __uint_as_float((unsigned)(bits >> 32)));
 }
-// Arrival of one block of a work item split over kGroups blocks, by one wave,
-// after its partials (or nothing, without work) were stored: one atomic on the
-// item's word, arrivals in its low 16 bits and blocks without work counted
-// above them. True for the last block to arrive, which clears the word for the
-// next launch (a plain device-scope store: nothing reads it again before this
-// launch ends); `skipped` says whether any block of the item had no work.
-__device__ __forceinline__ bool arrive_last(int* word, bool work, bool& skipped) {
+// Arrival of one block of a work item split over `blocks` blocks (kGroups by
+// default), by one wave, after its partials (or nothing, without work) were
+// stored: one atomic on the item's word, arrivals in its low 16 bits and blocks
+// without work counted above them. True for the last block to arrive, which
+// clears the word for the next launch (a plain device-scope store: nothing
+// reads it again before this launch ends); `skipped` says whether any block of
+// the item had no work.
+__device__ __forceinline__ bool arrive_last(int* word, bool work, bool& skipped,
+                                            int blocks = kGroups) {
   __builtin_amdgcn_s_waitcnt(0);   // the partial stores are complete before the arrival counts
   int prev = 0;
   if ((threadIdx.x & 63) == 0) prev = atomicAdd(word, work ? 1 : 1 + (1 << 16));
   prev = __builtin_amdgcn_readfirstlane(prev);
-  const bool last = (prev & 0xFFFF) + 1 == kGroups;
+  const bool last = (prev & 0xFFFF) + 1 == blocks;
   skipped = (prev >> 16) != 0 || !work;
   if (last && (threadIdx.x & 63) == 0)
     __hip_atomic_store(word, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -2399,129 +2404,73 @@ constexpr int kGuardThreads = 256;
 template <int DR>
 constexpr int guard_chunk() { return DR == 0 ? 256 : (2048 / (DR ? DR : 1) < 256 ? 2048 / (DR ? DR : 1) : 256); }
 
-template <int DR>
-__global__ __launch_bounds__(kGuardThreads) void k_check64(Launch L, GuardArgs G) {
-  constexpr int CH = guard_chunk<DR>();
-  constexpr int DS = DR == 0 ? 1 : DR;                       // staged coordinates per column
-  __shared__ double sh_y[DR == 0 ? 1 : CH * DS];
-  __shared__ double sh_pot[CH];
-  __shared__ double sh_acc[kGuardThreads];
-  __shared__ double sh_row[256];
-  __shared__ int sh_bad[256];
-  const int b = blockIdx.x;
-  const int pi = b >= L.nb0;
-  const Pass& P = L.p[pi];
-  int s, rb, nrows, ncols, c_fin, c_A;
-  SlotInfo si;
-  if (!place_item<1>(L, P, pass_blocks(L, pi), pi ? b - L.nb0 : b, s, rb, nrows, ncols, si, c_fin,
-                     c_A))
-    return;
-  // Row pass: the lane's row screen of the audited state against the outward
-  // bound (every lane without one, and every lane in shadow mode, which counts
-  // the verified rows the bound had excluded); column pass: the lanes whose
-  // row residual of this audit met tol. Every item of a lane decides alike.
-  bool checked = true, gate = true;
+// Float64 verification in three launches per audit:
+//  k_vgate       one wave per slot: whether the lane's row marginal is verified
+//                (the outward bound, shadow mode, the final audit); admitted
+//                lanes append their row blocks to the row list;
+//  k_verify64    (row pass) every (row block, column chunk) unit of the list,
+//                over a fixed grid; the lane's last row block records the
+//                certificate and appends the lane's column items when its row
+//                residual met tol (every lane at the final audit);
+//  k_verify64    (column pass) the same over the column list; the lane's last
+//                item decides.
+// The lists hold (slot * rbmax + row block), bit 30 set when the bound had
+// excluded the lane (shadow mode verifies it anyway and counts it). Each list's
+// length is reset by the launch before the one that fills it: the gate empties
+// the column list, the column pass the row list.
+constexpr unsigned kVExcluded = 1u << 30;
+
+__global__ __launch_bounds__(256) void k_vgate(Launch L, GuardArgs G) {
+  if (blockIdx.x == 0 && threadIdx.x == 0) G.vlen[1] = 0;
+  const Pass& P = L.p[0];
+  const int s = (int)(blockIdx.x * 4 + (threadIdx.x >> 6));
+  if (s >= P.A) return;
+  const Ctrl* c = L.ctrl;
+  const int c_fin = c->finished;
+  const int c_A = min(P.A, c->A);
+  // slots past the device-side width hold no lane (their records may never
+  // have been written)
+  if (s >= c_A) return;
+  const SlotInfo si = L.slot[s];
+  if (!item_live(L, P, s, si, c_fin, c_A)) return;
+  bool gate = true, checked = true;
   if (!P.final_audit) {
-    if (P.role == 0) {
-      const LaneAgg g = lane_aggregate(P.agg_screen, s, L.rbmax, row_blocks(nrows, L.rows), false);
-      gate = !isfinite(g.sum) || !G.bound || guard_lower_bound(L, G, si, g.sum) <= (double)L.tol;
-      checked = gate || P.verify_all;
-    } else {
-      const RowCert rc = G.row64[si.lane];
-      checked = rc.depth == P.depth && !rc.bad && rc.r <= (double)L.tol;
-    }
+    const LaneAgg g = lane_aggregate(P.agg_screen, s, L.rbmax, row_blocks(si.n, L.rows), false);
+    gate = !isfinite(g.sum) || !G.bound || guard_lower_bound(L, G, si, g.sum) <= (double)L.tol;
+    checked = gate || P.verify_all;
   }
-  if (!item_live(L, P, s, si, c_fin, c_A) || !checked) return;
+  if (!checked) return;
+  const int lane = threadIdx.x & 63;
+  const int nit = row_blocks(si.n, L.rows);
+  int base = 0;
+  if (lane == 0) base = atomicAdd(&G.vlen[0], nit);
+  base = __builtin_amdgcn_readfirstlane(base);
+  const unsigned tag = gate ? 0u : kVExcluded;
+  for (int k = lane; k < nit; k += 64)
+    G.vlist[0][base + k] = (int)((unsigned)(s * L.rbmax + k) | tag);
+}
+
+// The lane-level end of a verified item, by one thread: the item's
+// {sum |marginal - mass|, non-finite} goes out, the item counts in for its
+// lane, and the lane's last item takes the marginal's residual (items in row
+// block order) and the pass's consequences.
+__device__ void verify_item_done(const Launch& L, const GuardArgs& G, const Pass& P, int s,
+                                 const SlotInfo& si, int rb, double part_sum, int bad,
+                                 bool excluded) {
   const int lane_id = si.lane;
-  const int R = L.rows;                        // 32 to 256 rows per item
-  const int nph = kGuardThreads / R;           // column phases
-  const int tid = threadIdx.x;
-  const int r = tid % R, ph = tid / R;
-  const int d = G.d;
-  const double inv_eps = 1.0 / (double)G.eps[lane_id];
-  const float* wr = P.w_row + (size_t)lane_id * P.w_ld;
-  const float* wc = G.w_col[pi] + (size_t)lane_id * G.w_ld_col[pi];
-  const float* ycol = G.xy_col[pi] + (size_t)lane_id * G.ld_col[pi] * d;
-  const int i = rb * R + r;
-  const bool live = i < nrows && wr[i] != 0.f;
-  const double fi = live ? (double)export_potential(P.gam_out, P.rec_row, (size_t)s * P.padr + i,
-                                                    L.dp, G.es, si)
-                         : 0.0;
-  const float* xi = G.xy_row[pi] + ((size_t)lane_id * G.ld_row[pi] + (live ? i : 0)) * d;
-  double xr[DS];
-#pragma unroll
-  for (int k = 0; k < DS; ++k) xr[k] = (DR != 0 && k < d) ? (double)xi[k] : 0.0;
-  double acc = 0.0;
-#pragma unroll 1
-  for (int c0 = 0; c0 < ncols; c0 += CH) {
-    __syncthreads();   // every thread is done with the previous chunk
-    for (int t = tid; t < CH; t += kGuardThreads) {
-      const int j = c0 + t;
-      sh_pot[t] = (j < ncols && wc[j] != 0.f)
-                      ? (double)export_potential(P.gam_col, P.rec_col, (size_t)s * P.padc + j,
-                                                 L.dp, G.es, si)
-                      : -(double)INFINITY;   // past the prefix or removed (zero mass)
-    }
-    if (DR != 0) {
-      for (int e = tid; e < CH * DS; e += kGuardThreads) {
-        const int t = e / DS, k = e % DS;
-        sh_y[e] = (c0 + t < ncols && k < d) ? (double)ycol[(size_t)(c0 + t) * d + k] : 0.0;
-      }
-    }
-    __syncthreads();
-    if (!live) continue;
-#pragma unroll 1
-    for (int t = ph; t < CH && c0 + t < ncols; t += nph) {
-      const double gj = sh_pot[t];
-      if (gj == -(double)INFINITY) continue;
-      double C = 0.0;
-      if (DR != 0) {
-#pragma unroll
-        for (int k = 0; k < DS; ++k) {
-          const double df = xr[k] - sh_y[t * DS + k];
-          C = fma(df, df, C);
-        }
-      } else {
-        const float* yj = ycol + (size_t)(c0 + t) * d;
-#pragma unroll 4
-        for (int k = 0; k < d; ++k) {
-          const double df = (double)xi[k] - (double)yj[k];
-          C = fma(df, df, C);
-        }
-      }
-      acc += exp((fi + gj - C) * inv_eps);
-    }
-  }
-  // row totals: the phases' partial sums in phase order, |marginal - mass|
-  sh_acc[tid] = acc;
-  __syncthreads();
-  if (ph == 0) {
-    double tot = 0.0;
-    for (int q = 0; q < nph; ++q) tot += sh_acc[q * R + r];
-    sh_row[r] = live ? fabs(tot - (double)wr[i]) : 0.0;
-    sh_bad[r] = live && !isfinite(tot);
-  }
-  __syncthreads();
-  if (tid != 0) return;
-  double part = 0.0;
-  int bad = 0;
-  for (int q = 0; q < R; ++q) {
-    if (rb * R + q >= nrows) break;
-    part += sh_row[q];
-    bad |= sh_bad[q];
-  }
+  const int R = L.rows;
   unsigned long long* dst =
       reinterpret_cast<unsigned long long*>(G.agg64[P.role] + (size_t)s * L.rbmax + rb);
-  __hip_atomic_store(dst, (unsigned long long)__double_as_longlong(part), __ATOMIC_RELAXED,
+  __hip_atomic_store(dst, (unsigned long long)__double_as_longlong(part_sum), __ATOMIC_RELAXED,
                      __HIP_MEMORY_SCOPE_AGENT);
   __hip_atomic_store(dst + 1, (unsigned long long)__double_as_longlong(bad ? 1.0 : 0.0),
                      __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   wait_mem();
-  const int total = row_blocks(P.role ? si.m : si.n, R);   // the lane's blocks in this pass
+  const int total = row_blocks(P.role ? si.m : si.n, R);   // the lane's items in this pass
   const int prev = atomicAdd(&L.vcnt[lane_id], 1);
   if (prev + 1 != total) return;
   atomicExch(&L.vcnt[lane_id], 0);
-  // last block of the lane: this marginal's residual, in block order
+  // last item of the lane: this marginal's residual, in row block order
   double rr = 0.0;
   bool fin = true;
   {
@@ -2544,11 +2493,19 @@ __global__ __launch_bounds__(kGuardThreads) void k_check64(Launch L, GuardArgs G
     rc.bad = fin ? 0 : 1;
     G.row64[lane_id] = rc;
     L.audit[s].rhat = (float)rr;
-    if (P.final_audit) return;   // the column pass decides
-    atomicAdd(&L.ctrl->screen_pos, 1);
-    if (!gate && fin && rr <= (double)L.tol) atomicAdd(&L.ctrl->guard_missed, 1);
-    if (!fin) retire_lane(L, P, s, si, 2, (float)rr, NAN);
-    else if (rr > (double)L.tol) atomicAdd(&L.ctrl->check_fail, 1);
+    bool col = P.final_audit;   // the final audit's column pass decides every lane
+    if (!P.final_audit) {
+      atomicAdd(&L.ctrl->screen_pos, 1);
+      if (excluded && fin && rr <= (double)L.tol) atomicAdd(&L.ctrl->guard_missed, 1);
+      if (!fin) retire_lane(L, P, s, si, 2, (float)rr, NAN);
+      else if (rr > (double)L.tol) atomicAdd(&L.ctrl->check_fail, 1);
+      else col = true;
+    }
+    if (col) {
+      const int nit = row_blocks(si.m, R);
+      const int base = atomicAdd(&G.vlen[1], nit);
+      for (int k = 0; k < nit; ++k) G.vlist[1][base + k] = s * L.rbmax + k;
+    }
     return;
   }
   // column pass: the decision on both residuals of the audit
@@ -2569,6 +2526,150 @@ __global__ __launch_bounds__(kGuardThreads) void k_check64(Launch L, GuardArgs G
   if (!fin) retire_lane(L, P, s, si, 2, (float)rrow, (float)rcol);
   else if (rmax <= (double)L.tol) retire_lane(L, P, s, si, 0, (float)rrow, (float)rcol);
   else atomicAdd(&L.ctrl->check_fail, 1);
+}
+
+// One pass of the float64 marginal evaluation (L.p[0]: role 0 rows = x, role 1
+// rows = y) over the units of its list: unit u is column chunk u % kVChunks of
+// listed item u / kVChunks, a row block of L.rows rows. The lane's columns are
+// cut into kVChunks fixed chunks; per chunk, each row's terms are summed by
+// kGuardThreads / rows column phases, the phase sums added in phase order, and
+// the chunk sum stored (device scope). The item's last chunk to arrive adds
+// every row's chunk sums in chunk order: the bits do not depend on the grid.
+// A listed lane cannot retire or finish the window before all of its items
+// are done (only its own last item decides, and the window finishes only
+// when its last active lane retires), so every unit has work and every item
+// receives kVChunks arrivals. Blocks stride over the units: the loop is
+// bounded by the list's length, fixed before the launch.
+template <int DR>
+__global__ __launch_bounds__(kGuardThreads) void k_verify64(Launch L, GuardArgs G) {
+  constexpr int CH = guard_chunk<DR>();
+  constexpr int DS = DR == 0 ? 1 : DR;                       // staged coordinates per column
+  __shared__ double sh_y[DR == 0 ? 1 : CH * DS];
+  __shared__ double sh_pot[CH];
+  __shared__ double sh_acc[kGuardThreads];
+  __shared__ double sh_row[256];
+  __shared__ int sh_bad[256];
+  __shared__ int sh_last;
+  const Pass& P = L.p[0];
+  const int role = P.role;
+  // the column pass empties the row list for the next audit (nothing in this
+  // launch reads it)
+  if (role == 1 && blockIdx.x == 0 && threadIdx.x == 0) G.vlen[0] = 0;
+  const int units = G.vlen[role] * kVChunks;
+  const int* list = G.vlist[role];
+  const int tid = threadIdx.x;
+  const int R = L.rows;                        // 32 to 256 rows per item
+  const int nph = kGuardThreads / R;           // column phases
+  const int r = tid % R, ph = tid / R;
+  const int d = G.d;
+#pragma unroll 1
+  for (int u = (int)blockIdx.x; u < units; u += (int)gridDim.x) {
+    const unsigned e = (unsigned)list[u / kVChunks];
+    const int q = u % kVChunks;
+    const bool excluded = (e & kVExcluded) != 0;
+    const int sr = (int)(e & ~kVExcluded);
+    const int s = sr / L.rbmax, rb = sr % L.rbmax;
+    const SlotInfo si = L.slot[s];
+    const int lane_id = si.lane;
+    const int nrows = role ? si.m : si.n, ncols = role ? si.n : si.m;
+    const double inv_eps = 1.0 / (double)G.eps[lane_id];
+    const float* wr = P.w_row + (size_t)lane_id * P.w_ld;
+    const float* wc = G.w_col[role] + (size_t)lane_id * G.w_ld_col[role];
+    const float* ycol = G.xy_col[role] + (size_t)lane_id * G.ld_col[role] * d;
+    const int i = rb * R + r;
+    const bool live = i < nrows && wr[i] != 0.f;
+    double* vp = G.vpart + ((size_t)s * L.rbmax + rb) * kVChunks * R;
+    const double fi = live ? (double)export_potential(P.gam_out, P.rec_row,
+                                                      (size_t)s * P.padr + i, L.dp, G.es, si)
+                           : 0.0;
+    const float* xi = G.xy_row[role] + ((size_t)lane_id * G.ld_row[role] + (live ? i : 0)) * d;
+    double xr[DS];
+#pragma unroll
+    for (int k = 0; k < DS; ++k) xr[k] = (DR != 0 && k < d) ? (double)xi[k] : 0.0;
+    const int cpc = (ncols + kVChunks - 1) / kVChunks;   // columns per chunk
+    const int c_lo = min(ncols, q * cpc), c_hi = min(ncols, c_lo + cpc);
+    double acc = 0.0;
+#pragma unroll 1
+    for (int c0 = c_lo; c0 < c_hi; c0 += CH) {
+      __syncthreads();   // every thread is done with the previous stage
+      for (int t = tid; t < CH; t += kGuardThreads) {
+        const int j = c0 + t;
+        sh_pot[t] = (j < c_hi && wc[j] != 0.f)
+                        ? (double)export_potential(P.gam_col, P.rec_col, (size_t)s * P.padc + j,
+                                                   L.dp, G.es, si)
+                        : -(double)INFINITY;   // past the chunk or removed (zero mass)
+      }
+      if (DR != 0) {
+        for (int x = tid; x < CH * DS; x += kGuardThreads) {
+          const int t = x / DS, k = x % DS;
+          sh_y[x] = (c0 + t < c_hi && k < d) ? (double)ycol[(size_t)(c0 + t) * d + k] : 0.0;
+        }
+      }
+      __syncthreads();
+      if (!live) continue;
+#pragma unroll 1
+      for (int t = ph; t < CH && c0 + t < c_hi; t += nph) {
+        const double gj = sh_pot[t];
+        if (gj == -(double)INFINITY) continue;
+        double C = 0.0;
+        if (DR != 0) {
+#pragma unroll
+          for (int k = 0; k < DS; ++k) {
+            const double df = xr[k] - sh_y[t * DS + k];
+            C = fma(df, df, C);
+          }
+        } else {
+          const float* yj = ycol + (size_t)(c0 + t) * d;
+#pragma unroll 4
+          for (int k = 0; k < d; ++k) {
+            const double df = (double)xi[k] - (double)yj[k];
+            C = fma(df, df, C);
+          }
+        }
+        acc += exp((fi + gj - C) * inv_eps);
+      }
+    }
+    // the chunk sum of every row: its phases in phase order
+    sh_acc[tid] = acc;
+    __syncthreads();
+    if (ph == 0) {
+      double tot = 0.0;
+      for (int v = 0; v < nph; ++v) tot += sh_acc[v * R + r];
+      st_dev_d(vp + (size_t)q * R + r, tot);
+    }
+    wait_mem();   // this wave's chunk sums are stored before the block arrives
+    __syncthreads();
+    if (tid < 64) {
+      bool skipped;
+      const bool last = arrive_last(&G.vscnt[sr], true, skipped, kVChunks);
+      if (tid == 0) sh_last = last ? 1 : 0;
+    }
+    __syncthreads();
+    if (sh_last) {
+      // the item's last chunk: row totals (chunk sums in chunk order)
+      if (tid < R) {
+        const int i2 = rb * R + tid;
+        const bool lv = i2 < nrows && wr[i2] != 0.f;
+        double tot = 0.0;
+        if (lv)
+          for (int v = 0; v < kVChunks; ++v) tot += ld_dev_d(vp + (size_t)v * R + tid);
+        sh_row[tid] = lv ? fabs(tot - (double)wr[i2]) : 0.0;
+        sh_bad[tid] = lv && !isfinite(tot);
+      }
+      __syncthreads();
+      if (tid == 0) {
+        double part_sum = 0.0;
+        int bad = 0;
+        for (int v = 0; v < R; ++v) {
+          if (rb * R + v >= nrows) break;
+          part_sum += sh_row[v];
+          bad |= sh_bad[v];
+        }
+        verify_item_done(L, G, P, s, si, rb, part_sum, bad, excluded);
+      }
+    }
+    __syncthreads();   // sh_last, sh_row and sh_acc are free for the next unit
+  }
 }
 
 
@@ -2993,15 +3094,27 @@ hipError_t launch_update_mat(const Launch& a, int blocks, hipStream_t st, hipEve
   hipExtLaunchKernelGGL(k_mat_rows, dim3(blocks), dim3(512), lds, st, e0, e1, 0, b);
   return hipGetLastError();
 }
-hipError_t launch_check64(const Launch& a, const GuardArgs& g, int blocks, hipStream_t st) {
-  if (blocks <= 0) return hipSuccess;
+hipError_t launch_vgate(const Launch& a, const GuardArgs& g, hipStream_t st) {
+  if (g.vlist[0] == nullptr || g.vlen == nullptr) return hipErrorInvalidValue;
+  const int A = a.p[0].A;
+  hipLaunchKernelGGL(k_vgate, dim3((unsigned)std::max(1, (A + 3) / 4)), dim3(256), 0, st, a, g);
+  return hipGetLastError();
+}
+hipError_t launch_verify64(const Launch& a, const GuardArgs& g, int items, hipStream_t st) {
   if (a.rows != 32 && a.rows != 64 && a.rows != 128 && a.rows != 256) return hipErrorInvalidValue;
-  const dim3 grid(blocks), block(kGuardThreads);
-  if (g.d <= 4) hipLaunchKernelGGL(k_check64<4>, grid, block, 0, st, a, g);
-  else if (g.d <= 8) hipLaunchKernelGGL(k_check64<8>, grid, block, 0, st, a, g);
-  else if (g.d <= 16) hipLaunchKernelGGL(k_check64<16>, grid, block, 0, st, a, g);
-  else if (g.d <= 32) hipLaunchKernelGGL(k_check64<32>, grid, block, 0, st, a, g);
-  else hipLaunchKernelGGL(k_check64<0>, grid, block, 0, st, a, g);
+  if (g.vpart == nullptr || g.vscnt == nullptr || g.vlist[0] == nullptr || g.vlist[1] == nullptr ||
+      g.vlen == nullptr)
+    return hipErrorInvalidValue;
+  // items: the host's upper bound on the role's work items (the list holds at
+  // most these); at least one block, so that the column pass always empties
+  // the row list
+  const long long units = (long long)std::max(items, 1) * kVChunks;
+  const dim3 grid((unsigned)std::min<long long>(units, kVerifyBlocks)), block(kGuardThreads);
+  if (g.d <= 4) hipLaunchKernelGGL(k_verify64<4>, grid, block, 0, st, a, g);
+  else if (g.d <= 8) hipLaunchKernelGGL(k_verify64<8>, grid, block, 0, st, a, g);
+  else if (g.d <= 16) hipLaunchKernelGGL(k_verify64<16>, grid, block, 0, st, a, g);
+  else if (g.d <= 32) hipLaunchKernelGGL(k_verify64<32>, grid, block, 0, st, a, g);
+  else hipLaunchKernelGGL(k_verify64<0>, grid, block, 0, st, a, g);
   return hipGetLastError();
 }
 hipError_t launch_cost(const CostArgs& a, hipStream_t st) {

@@ -170,10 +170,14 @@ def test_sub_batch_validation_and_size():
 
 
 def test_guarded_release_validation_and_size():
-    """DS_F_GUARD keeps two float64 partials per row block and lane and one
-    row certificate per lane; with the float64 state also the export-rounding
-    sums of both sides per row block and lane (the outward bound), which a
-    float32 state does not have. At most 16384 points per side."""
+    """DS_F_GUARD keeps two float64 partials per row block and lane, one row
+    certificate per lane, and for the float64 verification its per-row sums of
+    the eight column chunks (8 B per row and chunk), an arrival word and two
+    list entries per row block (4 B each) and the two list lengths (one
+    256-byte slice of the workspace); with the float64 state also the
+    export-rounding sums of both sides per row block and lane (the outward
+    bound), which a float32 state does not have. At most 16384 points per
+    side."""
     op = ds._options(1e-3, None, 100, 1, "active", 0, 1)
     opg = ds._options(1e-3, None, 100, 1, "active", ds.F_GUARD, 1)
     code, n0 = _bytes(_problem(W=4, n_max=256, m_max=256, d=8), op)
@@ -184,12 +188,15 @@ def test_guarded_release_validation_and_size():
     c3, g64 = _bytes(big, opg)
     c4, p64 = _bytes(big, op)
     assert c3 == 0 and c4 == 0
-    # agg64 (2 x 16 B) and the rounding sums (2 x 16 B) per row block, 16 B per lane
-    assert g64 - p64 == W * rb * 64 + W * 16
+    # agg64 (2 x 16 B) and the rounding sums (2 x 16 B) per row block, 16 B per
+    # lane, per row block the chunk sums (8 chunks x 128 rows x 8 B), its word
+    # and two list entries, and the list lengths
+    assert g64 - p64 == W * rb * 64 + W * 16 + W * rb * (8 * 128 * 8 + 12) + 256
     f32 = ds._options(1e-3, None, 100, 1, "active", ds.F_GUARD | ds.F_FAST32, 1)
     f0 = ds._options(1e-3, None, 100, 1, "active", ds.F_FAST32, 1)
     rb32 = 8192 // 32                 # float32 matrix-core kernel: 32-row blocks
-    assert _bytes(big, f32)[1] - _bytes(big, f0)[1] == W * rb32 * 32 + W * 16
+    assert (_bytes(big, f32)[1] - _bytes(big, f0)[1]
+            == W * rb32 * 32 + W * 16 + W * rb32 * (8 * 32 * 8 + 12) + 256)
     assert _bytes(_problem(W=2, n_max=17000, m_max=100, d=3), opg)[0] == 4
     assert _bytes(_problem(W=2, n_max=17000, m_max=100, d=3), op)[0] == 0
 
