@@ -595,13 +595,14 @@ def test_guard_outward_bound_excludes_no_ready_lane(name):
 
 
 @pytest.mark.parametrize("shape", ["uniform", "mixed"])
-def test_guard_verification_blocks_per_item_are_bitwise_identical(shape):
+def test_guard_verification_grid_is_bitwise_identical(shape):
     """The float64 verification cuts every lane's columns into eight fixed
-    chunks and adds each row's chunk sums in chunk order; a launch gives each
-    row block one to eight blocks (fewer when it verifies more rows). The
-    final audit of a max_iter window verifies both marginals of every lane:
-    over 4096 row blocks (one block each), over 2048 (two), over 1024 (four),
-    four lanes (eight). A lane's outputs must not depend on which."""
+    chunks and adds each row's chunk sums in chunk order; its launches stride
+    at most 2048 blocks over the (row block, chunk) units of the lanes they
+    verify. The final audit of a max_iter window verifies both marginals of
+    every lane: over 4096 row blocks (each block takes about sixteen units in
+    turn), over 2048, over 1024, and four lanes (one unit per block). A lane's
+    outputs must not depend on which."""
     if shape == "uniform":
         make = lambda lanes: wl.make("c2", lanes=lanes, n=1024, m=1024)
         W = 520                                   # 8 row blocks per lane
@@ -610,13 +611,13 @@ def test_guard_verification_blocks_per_item_are_bitwise_identical(shape):
         make = lambda lanes: wl.make("c5", lanes=lanes, n=1024, m=1024, hetero=(600, 1024))
         W = 720                                   # 5 to 8 row blocks per lane
         middle = list(range(0, W, 3))             # 240 lanes
-    half = list(range(1, W, 2))                   # two blocks per row block
+    half = list(range(1, W, 2))
     few = [3, 77, 200, W - 1]
-    log(f"[case] guard blocks per item {shape}: W={W}, 3 cycles, tol 1e-9")
+    log(f"[case] guard verification grid {shape}: W={W}, 3 cycles, tol 1e-9")
     g = run_gpu(make(list(range(W))), 1e-9, max_iter=3, flags=F_GUARD, streams=1)
     assert np.all(g["status"] == oracle.MAX_ITER)
     for lanes in (half, middle, few):
-        log(f"[case] guard blocks per item {shape}: {len(lanes)} lanes")
+        log(f"[case] guard verification grid {shape}: {len(lanes)} lanes")
         gs = run_gpu(make(lanes), 1e-9, max_iter=3, flags=F_GUARD, streams=1)
         for q, t in enumerate(lanes):
             for k in ("f", "g", "residual", "row_residual", "col_residual", "status", "depth"):
