@@ -322,7 +322,7 @@ struct PartOut {
 // lane_base: the caller's index of this sub-batch's first lane (error messages
 // name lanes by the caller's index)
 ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* res, void* ws,
-                  hipStream_t st, DeviceRes* R, PartOut& out, int lane_base) {
+                  hipStream_t st, DeviceRes* R, PartOut& out, int lane_base, int parts) {
   using namespace ds;
   Layout L = plan(pr, op, ws);
   const int W = pr->W, d = pr->d;
@@ -490,7 +490,8 @@ ds_err solve_part(const ds_problem* pr, const ds_options* op, const ds_result* r
     // (the float64 kernel's items hold 64 to 256 rows: fewer items per width)
     const int medium = use_mfma ? kMediumItemsMfma * kRowsMfma / L.rows
                        : (precise && !uniform) ? kMediumItemsF64Mixed
-                                               : kMediumItemsValu * kRowsValu / L.rows;
+                       : (precise && parts == 1) ? kMediumItemsF64Solo
+                                                 : kMediumItemsValu * kRowsValu / L.rows;
     if (items < medium) return VAR_NARROW;
     return (use_mfma && tpg[role] <= 2) ? VAR_MEDIUM4 : VAR_MEDIUM;
   };
@@ -866,7 +867,8 @@ ds_err ds_solve(const ds_problem* pr, const ds_options* op, const ds_result* res
     const ds_problem sp = sub_problem(pr, lo, hi);
     const ds_result sr = sub_result(pr, res, lo);
     hipStream_t s = p == 0 ? st : Rs[p]->stream;
-    errs[p] = solve_part(&sp, op, &sr, static_cast<char*>(ws) + off[p], s, Rs[p], outs[p], lo);
+    errs[p] = solve_part(&sp, op, &sr, static_cast<char*>(ws) + off[p], s, Rs[p], outs[p], lo,
+                         parts);
     if (errs[p] != DS_OK) msgs[p] = g_last_error;
     if (p > 0 && errs[p] == DS_OK) {
       const hipError_t he = hipEventRecord(Rs[p]->join_ev, s);

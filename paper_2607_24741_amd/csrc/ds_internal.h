@@ -81,6 +81,14 @@ constexpr int kMediumItemsValu = 256;
 // heterogeneous items balanced up to this many items (measured on LiDAR-shaped
 // lanes: 8-wave blocks faster up to 8.7k items, 4-wave blocks from 12.6k)
 constexpr int kMediumItemsF64Mixed = 10000;
+// float64 kernel, uniform shapes, a call of one sub-batch: eight-wave blocks (one
+// column group per wave) up to this many items, so that a launch of 17 to 32
+// mixture lanes (d = 8, 128-row items) spreads over twice the waves with half
+// the sweep each (one-sub-batch mixture solve 274 against 284 ms; the telemetry
+// window unchanged). With two sub-batches the streams' launches already share
+// the chip, and the four-wave layout stays faster from 128 items (255 against
+// 260 ms); 512 or more items were slower either way.
+constexpr int kMediumItemsF64Solo = 256;
 
 // Per physical slot lane descriptor; moved by compaction with the rest of the
 // lane-indexed state.
