@@ -221,9 +221,11 @@ struct Layout {
 // rows per work item of the float64-state kernel: two per lane, so that each
 // column value read from LDS serves two terms. At d = 16 one row per lane left
 // the sweep bound by those reads (605 against 535 ms per telemetry solve, at
-// two waves per SIMD with a few spilled registers); four per lane at d = 3
-// measured slower (2087 against 1980 ms per LiDAR-shaped solve: lower
-// occupancy, fewer work items in narrow launches)
+// two waves per SIMD with a few spilled registers); four per lane measured
+// slower at d = 3 (2087 against 1980 ms per LiDAR-shaped solve: lower
+// occupancy, fewer work items in narrow launches) and at d = 16 (633 against
+// 521 ms per telemetry solve: all 256 registers and more spills, half the
+// work items per launch)
 __host__ __device__ constexpr int rows_f64(int) { return 128; }
 
 // work items of one lane-side: one per block of `rows` rows (all columns)
