@@ -1263,12 +1263,20 @@ __device__ __forceinline__ double potential_f64(double gam, double nrm, double k
 // bookkeeping, not the column loop) and still run faster than one row.
 template <int D>
 constexpr int f64_waves_per_simd() { return D <= 4 ? 4 : (D <= 7 ? 3 : 2); }
+// The split kernel sweeps one or a few tiles per wave: at d = 8 it prefetches
+// one column ahead instead of two, which frees the registers for a third wave
+// per SIMD (narrow launches of 10 to 12 mixture lanes then run in one round of
+// blocks instead of two). From d = 9 the same bound spills in the sweep.
+template <int D>
+constexpr int kSplitPrefetch() { return D == 8 ? 1 : 2; }
+template <int D>
+constexpr int f64_split_waves_per_simd() { return D == 8 ? 3 : f64_waves_per_simd<D>(); }
 
 // One 32-column tile of the float64 half-step for R rows per lane (the tile in
 // LDS at `cur`, column stride DG, the column operand in slot D). Anchored sums
 // add the tile's float32 sums in float64; otherwise a streaming maximum and a
 // rescaled sum over steps of four columns.
-template <int D, int R, int DG>
+template <int D, int R, int DG, int PFMAX = 2>
 __device__ __forceinline__ void f64_tile(const double* cur, const double (&xr)[R][D],
                                          const double (&bias)[R], bool fast, double (&mrun)[R],
                                          double (&srun)[R]) {
@@ -1300,7 +1308,8 @@ __device__ __forceinline__ void f64_tile(const double* cur, const double (&xr)[R
     // current column computes (software pipelining; the compiler alone waited
     // on nearly every read at the occupancy these register counts allow).
     // Two ahead measured best up to d = 12; at d = 16 registers allow one.
-    constexpr int PF = D <= 12 ? 2 : 1;
+    // (PFMAX: a caller's cap, for a register budget of more waves per SIMD.)
+    constexpr int PF = D <= 12 && PFMAX >= 2 ? 2 : 1;
     float tacc[R][2];
 #pragma unroll
     for (int r = 0; r < R; ++r) tacc[r][0] = tacc[r][1] = 0.f;
@@ -1636,7 +1645,7 @@ __device__ __forceinline__ double ld_dev_d(const double* p) {
 // leaves unchecked (a fact of the previous launch, the same for every block)
 // is dropped by all of its blocks before arriving.
 template <int D>
-__global__ __launch_bounds__(64 * kSubGroups, (f64_waves_per_simd<D>()))
+__global__ __launch_bounds__(64 * kSubGroups, (f64_split_waves_per_simd<D>()))
 void k_update_f64_split(Launch L) {
   note_progress(L);
   constexpr int ROWS = rows_f64(D);
@@ -1713,7 +1722,7 @@ void k_update_f64_split(Launch L) {
       double* nxt = sh_tile[q][((t - sA) & 1) ^ 1];
       const bool more = t + 1 < sB;
       if (more) st.fetch(rec_lane, gam_lane, t + 1, lane);
-      f64_tile<D, R, DG>(cur, xr, bias, fast, mrun, srun);
+      f64_tile<D, R, DG, kSplitPrefetch<D>()>(cur, xr, bias, fast, mrun, srun);
       __builtin_amdgcn_wave_barrier();
       if (more) st.stash(nxt, lane);
     }
