@@ -74,6 +74,26 @@ def test_noalloc_large_d_paths(path):
     log(f"[case] noalloc large d ({path}): depths {got[2].cpu().tolist()}")
 
 
+def test_noalloc_guarded_release_on_two_calls():
+    """Guarded release through the fixed array: its float64 verification lists,
+    per-row chunk sums and arrival words live in it too, and must start each
+    call from a clean state. Two calls in a row, the second on a smaller window
+    of mixed shapes, each bit for bit equal to ds_solve."""
+    import paper_2607_24741_amd as ds
+    first = wl.make("c2", W=6, n=200, m=176)
+    second = wl.make("c5", W=4, n=150, m=140, hetero=(30, 150), pad_value=np.nan)
+    for name, w, tol in (("mixture lanes, W=6", first, 1e-2),
+                         ("ragged LiDAR-shaped lanes, W=4 (smaller)", second, 1e-3)):
+        log(f"[case] noalloc guarded {name}: n_max={w.X.shape[1]} m_max={w.Y.shape[1]} d={w.d}")
+        ref, got = _pair(w, tol, flags=ds.F_GUARD)
+        for i, k in enumerate(KEYS):
+            assert got[i].equal(ref[i]), k
+        sr, sg = ref[-1], got[-1]
+        assert sg.check_pair_evals == sr.check_pair_evals > 0
+        assert sg.row_residual.equal(sr.row_residual) and sg.col_residual.equal(sr.col_residual)
+        log(f"[case] noalloc guarded {name}: depths {got[2].cpu().tolist()}")
+
+
 def test_noalloc_refuses_a_window_beyond_its_array():
     import torch
     import paper_2607_24741_amd as ds
