@@ -1263,6 +1263,13 @@ __device__ __forceinline__ double potential_f64(double gam, double nrm, double k
 // bookkeeping, not the column loop) and still run faster than one row.
 template <int D>
 constexpr int f64_waves_per_simd() { return D <= 4 ? 4 : (D <= 7 ? 3 : 2); }
+// Where the wide sweep's registers run out (d >= 14 spills a few), the
+// finish's own row data (masses, log masses, the old lse) is read after the
+// sweep instead of before it: telemetry solve (d = 16) 511 against 523 ms.
+// Below that the wait at the end of each item costs more (mixture 271
+// against 265 ms, LiDAR-shaped 1879 against 1858 ms).
+template <int D>
+constexpr bool kLateFinishLoads() { return D >= 14; }
 // The split kernel sweeps one or a few tiles per wave: at d = 8 it prefetches
 // one column ahead instead of two, which frees the registers for a third wave
 // per SIMD (narrow launches of 10 to 12 mixture lanes then run in one round of
@@ -1509,7 +1516,7 @@ void k_update_f64(Launch L) {
     owner[r] = wave == 0 && in_prefix[r];
     lm[r] = 0.0;
     w[r] = 0.f;
-    if (owner[r]) lm[r] = reinterpret_cast<const double*>(P.lm_row)[ridx];
+    if (!kLateFinishLoads<D>() && owner[r]) lm[r] = reinterpret_cast<const double*>(P.lm_row)[ridx];
     const double* rrow = reinterpret_cast<const double*>(P.rec_row) + ridx * DP;
 #pragma unroll
     for (int k = 0; k < D; ++k) xr[r][k] = rrow[k];
@@ -1536,7 +1543,8 @@ void k_update_f64(Launch L) {
 #pragma unroll
   for (int r = 0; r < R; ++r) {
     const int i = rb * ROWS + 64 * r + lane;
-    if (owner[r]) w[r] = P.w_row[(size_t)si.lane * P.w_ld + i];   // caller masses, by lane id
+    if (!kLateFinishLoads<D>() && owner[r])
+      w[r] = P.w_row[(size_t)si.lane * P.w_ld + i];   // caller masses, by lane id
     live[r] = in_prefix[r] && (lse_old[r] != (double)INFINITY);
     bias[r] = 0.0;
     if (live[r]) {
@@ -1591,6 +1599,21 @@ void k_update_f64(Launch L) {
   }
   __syncthreads();
   if (wave != 0) return;
+  if (kLateFinishLoads<D>()) {
+    // the finish's row data, read after the sweep so that the sweep keeps
+    // those registers (the row's lse is read again: the launch does not
+    // write it)
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int i = rb * ROWS + 64 * r + lane;
+      const size_t ridx = (size_t)s * P.padr + i;
+      lse_old[r] = reinterpret_cast<const double*>(P.lse_in)[ridx];
+      if (owner[r]) {
+        lm[r] = reinterpret_cast<const double*>(P.lm_row)[ridx];
+        w[r] = P.w_row[(size_t)si.lane * P.w_ld + i];
+      }
+    }
+  }
   double Mt[R], St[R];
 #pragma unroll
   for (int r = 0; r < R; ++r) {
